@@ -1,0 +1,16 @@
+"""fp64 CPU reference for multi-cartridge prefix attention.
+
+TEST INFRASTRUCTURE ONLY: used by the tests, the smoke check and the bench's
+CPU-baseline leg to check and time the HIP library. The library never imports
+it, and it shares no code with the library.
+"""
+from .attention import (  # noqa: F401
+    backward,
+    forward,
+    head_backward,
+    head_forward,
+    key_grads,
+    row_keys,
+    rows_forward_backward,
+    visible_mask,
+)

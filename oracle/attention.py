@@ -1,0 +1,230 @@
+"""fp64 reference for multi-cartridge prefix attention (forward and backward).
+
+TEST INFRASTRUCTURE ONLY. Nothing in the library's product path may import,
+call or execute this module; only the tests, the smoke check and the bench's
+CPU-baseline leg use it. It shares no code with the HIP library.
+
+What is computed (paper, Section "Cartridges at Scale (CAS) Training",
+Background paragraph; Section "Inference"; Limitations, "Cartridge KV
+position"):
+
+* A cartridge is a trainable KV prefix injected into an attention layer.
+  Several cartridges are concatenated in order and placed before the query
+  tokens; the query tokens then see each other under ordinary causal masking.
+  So for batch row b, query head h and query position t, with key/value head
+  kv = floor(h / group_size), the visible keys are every token of every
+  cartridge of row b in order, then the row's own tokens 0..t.
+* Softmax attention over the visible keys: scores s_j = scale * q . k_j,
+  row log-sum-exp LSE = m + ln sum_j exp(s_j - m) with m = max_j s_j,
+  probabilities P_j = exp(s_j - LSE), output O = sum_j P_j v_j.
+* Only the cartridges' keys and values are trained and the model is frozen,
+  so the backward returns dK/dV for each cartridge (plus dQ, and dK/dV of the
+  self tokens, which flow into the frozen model below). Given dO:
+  D = dO . O, dP_j = dO . v_j, dS_j = P_j (dP_j - D),
+  dQ = scale * sum_j dS_j k_j, dK_j += scale * dS_j q, dV_j += P_j dO.
+  A cartridge referenced several times (by several rows, or twice in one row)
+  is one tensor, so its gradient is the sum over every reference.
+
+Readings where the paper is silent: contiguous GQA groups (kv = h // g);
+inclusive causal diagonal (j <= t); keys and queries arrive post-RoPE, so no
+positional operation is applied here; LSE in natural log.
+
+Everything runs in float64 with two-pass softmax (max, then sum), no tiling
+and no online rescaling; matrix products use numpy's matmul as a primitive.
+"""
+from __future__ import annotations
+
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+
+def _f64(x) -> np.ndarray:
+    return np.asarray(x, dtype=np.float64)
+
+
+def visible_mask(n_prefix: int, q_len: int, t_idx: Sequence[int]) -> np.ndarray:
+    """Boolean [len(t_idx), n_prefix + q_len]: prefix keys always visible,
+    self key j visible to query t iff j <= t."""
+    t = np.asarray(t_idx, dtype=np.int64)[:, None]
+    j = np.arange(q_len, dtype=np.int64)[None, :]
+    self_vis = j <= t
+    pre = np.ones((t.shape[0], n_prefix), dtype=bool)
+    return np.concatenate([pre, self_vis], axis=1)
+
+
+def row_keys(cart_k: Sequence, cart_v: Sequence, row: Sequence[int], k_self_b, v_self_b,
+             kv: int):
+    """Concatenated key/value matrices [n_prefix + q_len, D] of one batch row
+    and one KV head, in prefix order, plus the number of prefix tokens."""
+    ks = [_f64(cart_k[c])[:, kv, :] for c in row]
+    vs = [_f64(cart_v[c])[:, kv, :] for c in row]
+    n_prefix = int(sum(k.shape[0] for k in ks))
+    K = np.concatenate(ks + [_f64(k_self_b)[:, kv, :]], axis=0)
+    V = np.concatenate(vs + [_f64(v_self_b)[:, kv, :]], axis=0)
+    return K, V, n_prefix
+
+
+def head_forward(qh: np.ndarray, K: np.ndarray, V: np.ndarray, n_prefix: int, q_len: int,
+                 t_idx: Sequence[int], scale: float):
+    """Forward for the query rows ``t_idx`` of one (row, head).
+
+    Returns O [T, D], LSE [T] and the probability matrix P [T, N]."""
+    mask = visible_mask(n_prefix, q_len, t_idx)
+    S = float(scale) * (qh @ K.T)
+    S = np.where(mask, S, -np.inf)
+    m = S.max(axis=1)
+    l = np.exp(S - m[:, None]).sum(axis=1)
+    lse = m + np.log(l)
+    P = np.exp(S - lse[:, None])          # exp(-inf) = 0 on hidden keys
+    O = P @ V
+    return O, lse, P
+
+
+def head_backward(qh: np.ndarray, K: np.ndarray, V: np.ndarray, n_prefix: int, q_len: int,
+                  t_idx: Sequence[int], scale: float, dOh: np.ndarray, Oh: np.ndarray,
+                  lse: np.ndarray, key_cols: Optional[np.ndarray] = None):
+    """Backward for the query rows ``t_idx`` of one (row, head).
+
+    ``Oh`` and ``lse`` are this oracle's own forward results for those rows.
+    Returns dQ [T, D] (only meaningful when ``key_cols`` is None) and the
+    contributions of these rows to dK and dV over the key columns
+    ``key_cols`` (all keys when None)."""
+    mask = visible_mask(n_prefix, q_len, t_idx)
+    if key_cols is not None:
+        mask = mask[:, key_cols]
+        K = K[key_cols]
+        V = V[key_cols]
+    S = float(scale) * (qh @ K.T)
+    P = np.where(mask, np.exp(S - lse[:, None]), 0.0)
+    Dr = (dOh * Oh).sum(axis=1)
+    dP = dOh @ V.T
+    dS = P * (dP - Dr[:, None])
+    dQ = float(scale) * (dS @ K)
+    dK = float(scale) * (dS.T @ qh)
+    dV = P.T @ dOh
+    return dQ, dK, dV
+
+
+def forward(q, k_self, v_self, cart_k: Sequence, cart_v: Sequence, rows: Sequence[Sequence[int]],
+            scale: float, group_size: int):
+    """O [B, Sq, Hq, D] and LSE [B, Hq, Sq] over [cartridges of the row || causal self]."""
+    q = _f64(q)
+    B, Sq, Hq, Dh = q.shape
+    O = np.zeros((B, Sq, Hq, Dh))
+    LSE = np.zeros((B, Hq, Sq))
+    t_all = np.arange(Sq)
+    for b in range(B):
+        for h in range(Hq):
+            kv = h // group_size
+            K, V, npre = row_keys(cart_k, cart_v, rows[b], k_self[b], v_self[b], kv)
+            o, lse, _ = head_forward(q[b, :, h, :], K, V, npre, Sq, t_all, scale)
+            O[b, :, h, :] = o
+            LSE[b, h, :] = lse
+    return O, LSE
+
+
+def backward(q, k_self, v_self, cart_k: Sequence, cart_v: Sequence, rows: Sequence[Sequence[int]],
+             scale: float, group_size: int, d_o, O=None, LSE=None):
+    """Gradients of sum(dO * O).
+
+    Returns dq, dk_self, dv_self, dcart_k, dcart_v; dcart_* hold one entry per
+    cartridge tensor (None for cartridges no row references) and sum over all
+    references of that cartridge."""
+    q = _f64(q)
+    d_o = _f64(d_o)
+    B, Sq, Hq, Dh = q.shape
+    Hkv = np.asarray(k_self).shape[2]
+    if O is None or LSE is None:
+        O, LSE = forward(q, k_self, v_self, cart_k, cart_v, rows, scale, group_size)
+    dq = np.zeros_like(q)
+    dk_self = np.zeros((B, Sq, Hkv, Dh))
+    dv_self = np.zeros((B, Sq, Hkv, Dh))
+    dck: List[Optional[np.ndarray]] = [None] * len(cart_k)
+    dcv: List[Optional[np.ndarray]] = [None] * len(cart_k)
+    for b in range(B):
+        for c in rows[b]:
+            if dck[c] is None:
+                shp = np.asarray(cart_k[c]).shape
+                dck[c] = np.zeros(shp)
+                dcv[c] = np.zeros(shp)
+    t_all = np.arange(Sq)
+    for b in range(B):
+        for h in range(Hq):
+            kv = h // group_size
+            K, V, npre = row_keys(cart_k, cart_v, rows[b], k_self[b], v_self[b], kv)
+            dQh, dK, dV = head_backward(q[b, :, h, :], K, V, npre, Sq, t_all, scale,
+                                        d_o[b, :, h, :], O[b, :, h, :], LSE[b, h, :])
+            dq[b, :, h, :] = dQh
+            off = 0
+            for c in rows[b]:
+                L = np.asarray(cart_k[c]).shape[0]
+                dck[c][:, kv, :] += dK[off:off + L]
+                dcv[c][:, kv, :] += dV[off:off + L]
+                off += L
+            dk_self[b, :, kv, :] += dK[off:]
+            dv_self[b, :, kv, :] += dV[off:]
+    return dq, dk_self, dv_self, dck, dcv
+
+
+# ---------------------------------------------------------------------------
+# Sampled evaluation for large shapes: the same definitions, evaluated only on
+# chosen query rows or chosen key columns.
+# ---------------------------------------------------------------------------
+
+def rows_forward_backward(q, k_self, v_self, cart_k, cart_v, rows, scale, group_size,
+                          b: int, h: int, t_idx: Sequence[int], d_o=None):
+    """O, LSE (and dQ when ``d_o`` is given) for query rows ``t_idx`` of (b, h)."""
+    q = _f64(q)
+    Sq = q.shape[1]
+    kv = h // group_size
+    K, V, npre = row_keys(cart_k, cart_v, rows[b], k_self[b], v_self[b], kv)
+    t_idx = np.asarray(t_idx)
+    o, lse, _ = head_forward(q[b, t_idx, h, :], K, V, npre, Sq, t_idx, scale)
+    if d_o is None:
+        return o, lse, None
+    dQ, _, _ = head_backward(q[b, t_idx, h, :], K, V, npre, Sq, t_idx, scale,
+                             _f64(d_o)[b, t_idx, h, :], o, lse)
+    return o, lse, dQ
+
+
+def key_grads(q, k_self, v_self, cart_k, cart_v, rows, scale, group_size, d_o, kv: int,
+              cart: int, tok_idx: Sequence[int]):
+    """dK, dV [len(tok_idx), D] for KV head ``kv`` at tokens ``tok_idx`` of
+    cartridge ``cart`` (summed over every reference to it), or of the self
+    keys of batch row ``-cart - 1`` when ``cart`` is negative.
+
+    Each contributing (row, head) is evaluated with its full forward, since
+    every query's LSE and O enter the gradient."""
+    q = _f64(q)
+    d_o = _f64(d_o)
+    B, Sq, Hq, Dh = q.shape
+    tok_idx = np.asarray(tok_idx, dtype=np.int64)
+    dK = np.zeros((len(tok_idx), Dh))
+    dV = np.zeros((len(tok_idx), Dh))
+    t_all = np.arange(Sq)
+    for b in range(B):
+        if cart < 0:
+            if b != -cart - 1:
+                continue
+            uses = [None]
+        else:
+            uses = []
+            off = 0
+            for c in rows[b]:
+                if c == cart:
+                    uses.append(off)
+                off += np.asarray(cart_k[c]).shape[0]
+            if not uses:
+                continue
+        for hh in range(group_size):
+            h = kv * group_size + hh
+            K, V, npre = row_keys(cart_k, cart_v, rows[b], k_self[b], v_self[b], kv)
+            o, lse, _ = head_forward(q[b, :, h, :], K, V, npre, Sq, t_all, scale)
+            for off in uses:
+                cols = (npre + tok_idx) if off is None else (off + tok_idx)
+                _, dk, dv = head_backward(q[b, :, h, :], K, V, npre, Sq, t_all, scale,
+                                          d_o[b, :, h, :], o, lse, key_cols=cols)
+                dK += dk
+                dV += dv
+    return dK, dV
