@@ -73,24 +73,44 @@ def uniform(key: int, n: int) -> np.ndarray:
     return (bits.astype(np.float64) + 0.5) * (2.0 ** -53)
 
 
-def normal(key: int, n: int, std: float = 1.0, chunk: int = 1 << 24) -> np.ndarray:
-    """``n`` float64 draws from N(0, std^2) by Box-Muller."""
+def _normal_chunk(key: int, p0: int, p1: int, n: int, std: float, out: np.ndarray) -> None:
+    with np.errstate(over="ignore"):
+        bits = raw_u64(key, 2 * (p1 - p0), start=2 * p0) >> np.uint64(11)
+    u = (bits.astype(np.float64) + 0.5) * (2.0 ** -53)
+    u1, u2 = u[0::2], u[1::2]
+    r = np.sqrt(-2.0 * np.log(u1)) * std
+    ang = 2.0 * np.pi * u2
+    z = np.empty(2 * (p1 - p0), dtype=np.float64)
+    z[0::2] = r * np.cos(ang)
+    z[1::2] = r * np.sin(ang)
+    lo = 2 * p0
+    hi = min(n, 2 * p1)
+    out[lo:hi] = z[: hi - lo]
+
+
+_POOL = None
+
+
+def _pool():
+    global _POOL
+    if _POOL is None:
+        import concurrent.futures
+        import os
+        _POOL = concurrent.futures.ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1))
+    return _POOL
+
+
+def normal(key: int, n: int, std: float = 1.0, chunk: int = 1 << 17) -> np.ndarray:
+    """``n`` float64 draws from N(0, std^2) by Box-Muller (chunks evaluated on a
+    thread pool; the values do not depend on the chunking)."""
     out = np.empty(n, dtype=np.float64)
     npairs = (n + 1) // 2
-    for p0 in range(0, npairs, chunk):
-        p1 = min(npairs, p0 + chunk)
-        with np.errstate(over="ignore"):
-            bits = raw_u64(key, 2 * (p1 - p0), start=2 * p0) >> np.uint64(11)
-        u = (bits.astype(np.float64) + 0.5) * (2.0 ** -53)
-        u1, u2 = u[0::2], u[1::2]
-        r = np.sqrt(-2.0 * np.log(u1)) * std
-        ang = 2.0 * np.pi * u2
-        z = np.empty(2 * (p1 - p0), dtype=np.float64)
-        z[0::2] = r * np.cos(ang)
-        z[1::2] = r * np.sin(ang)
-        lo = 2 * p0
-        hi = min(n, 2 * p1)
-        out[lo:hi] = z[: hi - lo]
+    spans = [(p0, min(npairs, p0 + chunk)) for p0 in range(0, npairs, chunk)]
+    if len(spans) <= 1:
+        for p0, p1 in spans:
+            _normal_chunk(key, p0, p1, n, std, out)
+        return out
+    list(_pool().map(lambda s: _normal_chunk(key, s[0], s[1], n, std, out), spans))
     return out
 
 

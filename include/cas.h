@@ -1,0 +1,225 @@
+/*
+ * libcas: multi-cartridge prefix attention for AMD Instinct MI355X (gfx950).
+ *
+ * One attention layer of a frozen LLM in which each query token attends over
+ * a concatenation of trainable KV prefixes ("cartridges") followed by the
+ * row's own tokens under causal masking, with the backward pass that returns
+ * dQ and the dK/dV of every cartridge and of the self tokens.
+ *
+ * The operation (paper: Section "Cartridges at Scale (CAS) Training",
+ * Background paragraph, for the cartridge as a trainable KV prefix whose keys
+ * and values alone receive gradients; Section "Inference" for the
+ * concatenation of several cartridges in order ahead of the prompt; the
+ * Limitations paragraph "Cartridge KV position" for ordinary causal masking of
+ * the tokens that follow; the Budget Manager and Pool rotation paragraphs for
+ * cartridges that move between host memory and the GPU):
+ *
+ *   For batch row b, query head h, query position t and kv = h / group_size,
+ *   the visible keys are, in order, every token of every segment of row b,
+ *   then self tokens 0..t. With s_j = softmax_scale * q . k_j:
+ *     LSE = ln sum_j exp(s_j),  P_j = exp(s_j - LSE),  O = sum_j P_j v_j.
+ *   Backward, given dO:  D = dO . O,  dS_j = P_j (dO . v_j - D),
+ *     dQ = scale * sum_j dS_j k_j,  dK_j += scale * dS_j q,  dV_j += P_j dO,
+ *   summed over every query (all heads of the group) that sees key j.
+ *
+ * Keys and queries are taken as given (post-RoPE); no positional operation is
+ * applied. All calls are asynchronous on the caller's HIP stream; results are
+ * valid once the stream reaches them.
+ *
+ * Thread safety: calls may be made from several host threads; the error
+ * message is thread-local.
+ */
+#ifndef CAS_H_
+#define CAS_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CAS_ABI_VERSION 1
+
+typedef enum {
+  CAS_OK = 0,
+  CAS_ERR_INVALID_ARGUMENT = 1, /* bad pointer, size, shape, segment table or aliasing */
+  CAS_ERR_UNSUPPORTED = 2,      /* valid but not implemented (head_dim, dtype, table size) */
+  CAS_ERR_ALIGNMENT = 3,        /* pointer or stride not a multiple of 16 bytes */
+  CAS_ERR_NOT_PINNED = 4,       /* staging source is pageable host memory */
+  CAS_ERR_WORKSPACE = 5,        /* workspace NULL or smaller than the size query returned */
+  CAS_ERR_HIP = 6               /* a HIP runtime call failed; see cas_last_error_message */
+} cas_status_t;
+
+typedef enum {
+  CAS_DTYPE_BF16 = 0, /* bfloat16 tensors; MFMA in bf16 with fp32 accumulation */
+  CAS_DTYPE_FP32 = 1  /* float32 tensors; MFMA in fp32 (no down-conversion anywhere) */
+} cas_dtype_t;
+
+/*
+ * One cartridge block as seen by one batch row (one entry of the segment table).
+ *
+ * k, v:   device pointers. Element (token j, kv head h, channel c) lives at
+ *         base + j*stride_tok + h*stride_head + c (in elements of the dtype).
+ *         The channel stride is 1. Token-major [len, Hkv, d] and head-major
+ *         [Hkv, len, d] storage, and padded token strides, are all expressible.
+ * dk, dv: device pointers with the same strides, receiving the gradient
+ *         (backward only; ignored by the forward). NULL means "do not return
+ *         this gradient".
+ * len:    tokens, >= 0. A zero-length entry is skipped and its pointers are
+ *         not read.
+ *
+ * Entries with equal (k, v, len, stride_tok, stride_head) are the same
+ * cartridge, referenced several times (by several rows, or twice in one row);
+ * they must carry equal dk and dv, which then receive the SUM over all
+ * references. Any other overlap between a gradient buffer and any tensor the
+ * call reads or writes is rejected with CAS_ERR_INVALID_ARGUMENT.
+ */
+typedef struct {
+  const void *k;
+  const void *v;
+  void *dk;
+  void *dv;
+  int64_t len;
+  int64_t stride_tok;
+  int64_t stride_head;
+} cas_segment_t;
+
+/*
+ * Problem description, read only during the call (the host arrays may be
+ * reused as soon as the call returns).
+ *
+ * Shapes (contiguous, in elements of dtype):
+ *   q, o, d_o, dq:                [batch, q_len, num_kv_heads*group_size, head_dim]
+ *   k_self, v_self, dk_self, dv_self: [batch, q_len, num_kv_heads, head_dim]
+ *   lse (always float32, natural log): [batch, num_kv_heads*group_size, q_len]
+ * Query head h reads kv head h / group_size (contiguous GQA groups).
+ * head_dim is 64 or 128. softmax_scale must be finite and > 0.
+ * seg_offsets is a host array of batch+1 non-decreasing int32 with
+ * seg_offsets[0] == 0; row b uses segments[seg_offsets[b] .. seg_offsets[b+1]).
+ * segments may be NULL when seg_offsets[batch] == 0.
+ */
+typedef struct {
+  cas_dtype_t dtype;
+  int32_t batch;
+  int32_t q_len;
+  int32_t num_kv_heads;
+  int32_t group_size;
+  int32_t head_dim;
+  float softmax_scale;
+  const cas_segment_t *segments;
+  const int32_t *seg_offsets;
+} cas_problem_t;
+
+/*
+ * Bytes of device workspace a forward (backward == 0) or backward
+ * (backward != 0) call on this problem needs, written to *bytes. The size
+ * depends only on the problem and the current tuning (cas_set_tuning), not on
+ * the device. Workspace is caller-owned, 256-byte aligned, and may be reused
+ * by the next call once the stream has passed the previous one.
+ */
+cas_status_t cas_prefix_attn_workspace_size(const cas_problem_t *p, int backward, size_t *bytes);
+
+/*
+ * Forward: writes o (dtype) and, when lse != NULL, the row log-sum-exp lse
+ * (float32, natural log). All tensors are device memory, 16-byte aligned
+ * (lse 4-byte aligned). hip_stream is a hipStream_t (NULL = default stream).
+ * Validation happens before anything is enqueued; on error nothing is
+ * launched and the outputs are untouched.
+ */
+cas_status_t cas_prefix_attn_fwd(const cas_problem_t *p, const void *q, const void *k_self,
+                                 const void *v_self, void *o, float *lse, void *workspace,
+                                 size_t ws_bytes, void *hip_stream);
+
+/*
+ * Backward of sum(d_o * o): consumes q, the self and segment K/V, and the o
+ * and lse written by cas_prefix_attn_fwd on the same inputs, and OVERWRITES
+ * dq, dk_self, dv_self and every non-NULL segments[i].dk / .dv (NULL outputs
+ * are skipped). Gradients are returned in the input dtype; accumulation is in
+ * fp32. Same pointer, alignment, stream and error rules as the forward.
+ */
+cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const void *k_self,
+                                 const void *v_self, const void *o, const float *lse,
+                                 const void *d_o, void *dq, void *dk_self, void *dv_self,
+                                 void *workspace, size_t ws_bytes, void *hip_stream);
+
+/*
+ * Cartridge staging (paper: Budget Manager and Pool rotation paragraphs,
+ * cartridges offloaded to host memory and moved back onto the GPU).
+ * Enqueues n host->device copies on side_stream (a hipStream_t) and, when
+ * done_event (a hipEvent_t) is non-NULL, records it after the last copy so a
+ * compute stream can hipStreamWaitEvent on it. Every host_src must lie in
+ * pinned (page-locked) host memory, else CAS_ERR_NOT_PINNED and nothing is
+ * enqueued: a pageable copy would silently serialise with the host. The
+ * caller keeps host_src alive and unmodified until the event completes.
+ */
+typedef struct {
+  const void *host_src;
+  void *dev_dst;
+  size_t bytes;
+} cas_stage_copy_t;
+
+cas_status_t cas_cartridge_stage(const cas_stage_copy_t *copies, int32_t n, void *side_stream,
+                                 void *done_event);
+
+/* Static description of a status code. */
+const char *cas_status_string(cas_status_t s);
+/* Message of the last failed call on this thread ("" if none). */
+const char *cas_last_error_message(void);
+/* CAS_ABI_VERSION of the built library. */
+int32_t cas_abi_version(void);
+
+/*
+ * Tuning knobs (process-wide; 0 = automatic). They change the launch plan,
+ * never the result beyond rounding order.
+ *   fwd_splits:  key-axis splits of the forward (partial O/LSE merged after)
+ *   dq_splits:   key-axis splits of the dQ pass (fp32 partials summed after)
+ */
+typedef struct {
+  int32_t fwd_splits;
+  int32_t dq_splits;
+} cas_tuning_t;
+
+cas_status_t cas_set_tuning(const cas_tuning_t *t);
+cas_status_t cas_get_tuning(cas_tuning_t *t);
+
+/*
+ * Launch plan of a problem (host-side; no device access). For tests and
+ * profiling tools.
+ */
+typedef struct {
+  int32_t fwd_splits;       /* key-axis splits used by the forward */
+  int32_t dq_splits;        /* key-axis splits used by the dQ pass */
+  int32_t fwd_workgroups;   /* forward grid size */
+  int32_t dkdv_workgroups;  /* dK/dV grid size */
+  int32_t unique_segments;  /* distinct cartridges after alias folding */
+  int32_t total_key_tiles;  /* dK/dV key tiles over unique cartridges and self */
+  int64_t max_prefix_len;   /* longest row prefix, tokens */
+  size_t ws_fwd_bytes;
+  size_t ws_bwd_bytes;
+} cas_plan_info_t;
+
+cas_status_t cas_plan_info(const cas_problem_t *p, cas_plan_info_t *out);
+
+/*
+ * Per-kernel timing with HIP events, recorded on the stream each kernel is
+ * launched on (a profiling aid; off by default). While enabled, every kernel
+ * a call launches is bracketed by two events. cas_timing_read waits for the
+ * recorded events and returns, per kernel name, the number of launches and
+ * their summed duration since the last reset.
+ */
+typedef struct {
+  char name[48];
+  int32_t launches;
+  double total_ms;
+} cas_kernel_time_t;
+
+cas_status_t cas_timing_enable(int enable);
+cas_status_t cas_timing_reset(void);
+cas_status_t cas_timing_read(cas_kernel_time_t *out, int32_t cap, int32_t *n_out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CAS_H_ */

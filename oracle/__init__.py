@@ -10,6 +10,7 @@ from .attention import (  # noqa: F401
     head_backward,
     head_forward,
     key_grads,
+    key_grads_many,
     row_keys,
     rows_forward_backward,
     visible_mask,

@@ -228,3 +228,43 @@ def key_grads(q, k_self, v_self, cart_k, cart_v, rows, scale, group_size, d_o, k
                 dK += dk
                 dV += dv
     return dK, dV
+
+
+def key_grads_many(q, k_self, v_self, cart_k, cart_v, rows, scale, group_size, d_o, kv: int,
+                   targets):
+    """``key_grads`` for several (cart, tok_idx) targets of one KV head, sharing
+    each contributing (row, head) forward. Returns [(dK, dV), ...]."""
+    q = _f64(q)
+    d_o = _f64(d_o)
+    B, Sq, Hq, Dh = q.shape
+    out = [(np.zeros((len(t), Dh)), np.zeros((len(t), Dh))) for _, t in targets]
+    t_all = np.arange(Sq)
+    for b in range(B):
+        cols_per_target = []
+        for cart, toks in targets:
+            toks = np.asarray(toks, dtype=np.int64)
+            cols = []
+            if cart < 0:
+                if b == -cart - 1:
+                    cols.append(None)
+            else:
+                off = 0
+                for c in rows[b]:
+                    if c == cart:
+                        cols.append(off)
+                    off += np.asarray(cart_k[c]).shape[0]
+            cols_per_target.append((toks, cols))
+        if not any(cols for _, cols in cols_per_target):
+            continue
+        K, V, npre = row_keys(cart_k, cart_v, rows[b], k_self[b], v_self[b], kv)
+        for hh in range(group_size):
+            h = kv * group_size + hh
+            o, lse, _ = head_forward(q[b, :, h, :], K, V, npre, Sq, t_all, scale)
+            for i, (toks, cols) in enumerate(cols_per_target):
+                for off in cols:
+                    kc = (npre + toks) if off is None else (off + toks)
+                    _, dk, dv = head_backward(q[b, :, h, :], K, V, npre, Sq, t_all, scale,
+                                              d_o[b, :, h, :], o, lse, key_cols=kc)
+                    out[i][0][:] += dk
+                    out[i][1][:] += dv
+    return out

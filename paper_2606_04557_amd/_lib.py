@@ -1,0 +1,95 @@
+"""ctypes declarations mirroring include/cas.h."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcas.so")
+
+CAS_OK = 0
+CAS_ERR_INVALID_ARGUMENT = 1
+CAS_ERR_UNSUPPORTED = 2
+CAS_ERR_ALIGNMENT = 3
+CAS_ERR_NOT_PINNED = 4
+CAS_ERR_WORKSPACE = 5
+CAS_ERR_HIP = 6
+
+CAS_DTYPE_BF16 = 0
+CAS_DTYPE_FP32 = 1
+
+# Every function include/cas.h declares.
+EXPORTS = [
+    "cas_prefix_attn_workspace_size", "cas_prefix_attn_fwd", "cas_prefix_attn_bwd",
+    "cas_cartridge_stage", "cas_status_string", "cas_last_error_message", "cas_abi_version",
+    "cas_set_tuning", "cas_get_tuning", "cas_plan_info", "cas_timing_enable",
+    "cas_timing_reset", "cas_timing_read",
+]
+
+
+class Segment(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("dk", ctypes.c_void_p),
+                ("dv", ctypes.c_void_p), ("len", ctypes.c_int64), ("stride_tok", ctypes.c_int64),
+                ("stride_head", ctypes.c_int64)]
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("batch", ctypes.c_int32), ("q_len", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("group_size", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
+                ("segments", ctypes.POINTER(Segment)), ("seg_offsets", ctypes.POINTER(ctypes.c_int32))]
+
+
+class StageCopy(ctypes.Structure):
+    _fields_ = [("host_src", ctypes.c_void_p), ("dev_dst", ctypes.c_void_p), ("bytes", ctypes.c_size_t)]
+
+
+class Tuning(ctypes.Structure):
+    _fields_ = [("fwd_splits", ctypes.c_int32), ("dq_splits", ctypes.c_int32)]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("fwd_splits", ctypes.c_int32), ("dq_splits", ctypes.c_int32),
+                ("fwd_workgroups", ctypes.c_int32), ("dkdv_workgroups", ctypes.c_int32),
+                ("unique_segments", ctypes.c_int32), ("total_key_tiles", ctypes.c_int32),
+                ("max_prefix_len", ctypes.c_int64), ("ws_fwd_bytes", ctypes.c_size_t),
+                ("ws_bwd_bytes", ctypes.c_size_t)]
+
+
+class KernelTime(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 48), ("launches", ctypes.c_int32), ("total_ms", ctypes.c_double)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libcas.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libcas is not built ({path} missing): run paper_2606_04557_amd.build")
+    lib = ctypes.CDLL(path)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    P = ctypes.POINTER
+    lib.cas_prefix_attn_workspace_size.argtypes = [P(Problem), ctypes.c_int, P(sz)]
+    lib.cas_prefix_attn_fwd.argtypes = [P(Problem), vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.cas_prefix_attn_bwd.argtypes = [P(Problem), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.cas_cartridge_stage.argtypes = [P(StageCopy), i32, vp, vp]
+    lib.cas_status_string.argtypes = [ctypes.c_int]
+    lib.cas_status_string.restype = ctypes.c_char_p
+    lib.cas_last_error_message.argtypes = []
+    lib.cas_last_error_message.restype = ctypes.c_char_p
+    lib.cas_abi_version.restype = i32
+    lib.cas_set_tuning.argtypes = [P(Tuning)]
+    lib.cas_get_tuning.argtypes = [P(Tuning)]
+    lib.cas_plan_info.argtypes = [P(Problem), P(PlanInfo)]
+    lib.cas_timing_enable.argtypes = [ctypes.c_int]
+    lib.cas_timing_reset.argtypes = []
+    lib.cas_timing_read.argtypes = [P(KernelTime), i32, P(i32)]
+    for name in ("cas_prefix_attn_workspace_size", "cas_prefix_attn_fwd", "cas_prefix_attn_bwd",
+                 "cas_cartridge_stage", "cas_set_tuning", "cas_get_tuning", "cas_plan_info",
+                 "cas_timing_enable", "cas_timing_reset", "cas_timing_read"):
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib

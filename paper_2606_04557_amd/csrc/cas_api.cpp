@@ -1,0 +1,772 @@
+// libcas host side: argument validation, launch planning, segment-table
+// upload, kernel launches, cartridge staging and optional kernel timing.
+//
+// Validation is pure host code and runs before any HIP call, so every error
+// path can be exercised on a machine without a GPU.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "../../include/cas.h"
+#include "cas_internal.h"
+
+using namespace cas;
+
+namespace {
+
+thread_local std::string g_err;
+
+cas_status_t fail(cas_status_t s, const std::string &msg) {
+  g_err = msg;
+  return s;
+}
+
+std::mutex g_tuning_mu;
+cas_tuning_t g_tuning = {0, 0};
+
+cas_tuning_t tuning() {
+  std::lock_guard<std::mutex> lk(g_tuning_mu);
+  return g_tuning;
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+struct Interval {
+  uintptr_t lo, hi;   // [lo, hi)
+  bool write;
+  uintptr_t owner;    // identical writes of one owner may coincide (aliased cartridge)
+  const char *what;
+};
+
+// Every write interval must be disjoint from every other interval (reads and
+// writes) of a different owner.
+bool overlap_free(std::vector<Interval> &iv, std::string &msg) {
+  std::sort(iv.begin(), iv.end(), [](const Interval &a, const Interval &b) { return a.lo < b.lo; });
+  uintptr_t max_hi_any = 0, max_hi_wr = 0;
+  int any_idx = -1, wr_idx = -1;
+  for (size_t i = 0; i < iv.size(); ++i) {
+    const Interval &x = iv[i];
+    if (x.hi <= x.lo) continue;
+    if (x.write && any_idx >= 0 && max_hi_any > x.lo &&
+        !(iv[any_idx].write && iv[any_idx].owner == x.owner && iv[any_idx].lo == x.lo &&
+          iv[any_idx].hi == x.hi)) {
+      msg = std::string("output ") + x.what + " overlaps " + iv[any_idx].what;
+      return false;
+    }
+    if (!x.write && wr_idx >= 0 && max_hi_wr > x.lo) {
+      msg = std::string("input ") + x.what + " overlaps output " + iv[wr_idx].what;
+      return false;
+    }
+    if (x.hi > max_hi_any) {
+      max_hi_any = x.hi;
+      any_idx = (int)i;
+    }
+    if (x.write && x.hi > max_hi_wr) {
+      max_hi_wr = x.hi;
+      wr_idx = (int)i;
+    }
+  }
+  return true;
+}
+
+struct Plan {
+  DType dt;
+  int esize;
+  int B, Sq, Hkv, g, Hq, D, nrows;
+  float scale;
+  std::vector<DevSeg> segs;
+  std::vector<DevRow> rows;
+  std::vector<DevCart> carts;
+  std::vector<int32_t> uses;
+  int64_t max_prefix = 0;
+  int fwd_splits = 1, dq_splits = 1;
+  int nqblk_fwd = 0, nqblk_dq = 0;
+  int cart_tiles = 0, self_tiles = 0;
+  bool want_self_grad = false;
+  // workspace layout
+  size_t off_segs = 0, off_rows = 0, off_carts = 0, off_uses = 0, table_bytes = 0;
+  size_t off_part_o = 0, off_part_lse = 0, ws_fwd = 0;
+  size_t off_dvec = 0, off_lse2 = 0, off_part_dq = 0, ws_bwd = 0;
+};
+
+constexpr int kTargetWgs = 512;   // two workgroups per CU on a 256-CU MI355X
+
+int auto_splits(int64_t base_wgs, int64_t min_row_tiles) {
+  if (base_wgs >= (kTargetWgs * 3) / 4) return 1;
+  int64_t s = ceil_div(kTargetWgs, std::max<int64_t>(1, base_wgs));
+  s = std::min<int64_t>(s, std::max<int64_t>(1, min_row_tiles / 8));
+  return (int)std::max<int64_t>(1, std::min<int64_t>(s, kMaxSplits));
+}
+
+// Shapes, segment table and planning. `bwd` additionally folds aliases and
+// builds the dK/dV work list. Pure host code.
+cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
+  if (!p) return fail(CAS_ERR_INVALID_ARGUMENT, "problem is NULL");
+  if (p->dtype != CAS_DTYPE_BF16 && p->dtype != CAS_DTYPE_FP32)
+    return fail(CAS_ERR_INVALID_ARGUMENT, "unknown dtype");
+  if (p->batch < 1 || p->q_len < 1 || p->num_kv_heads < 1 || p->group_size < 1 || p->head_dim < 1)
+    return fail(CAS_ERR_INVALID_ARGUMENT, "batch, q_len, num_kv_heads, group_size and head_dim must be >= 1");
+  if (p->head_dim != 64 && p->head_dim != 128)
+    return fail(CAS_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (!std::isfinite(p->softmax_scale) || !(p->softmax_scale > 0.0f))
+    return fail(CAS_ERR_INVALID_ARGUMENT, "softmax_scale must be finite and > 0");
+  const int64_t Hq = (int64_t)p->num_kv_heads * p->group_size;
+  const int64_t nrows = (int64_t)p->group_size * p->q_len;
+  if (Hq > (1 << 16) || nrows > (1 << 28))
+    return fail(CAS_ERR_UNSUPPORTED, "num_kv_heads*group_size or group_size*q_len too large");
+  if ((int64_t)p->batch * p->q_len * Hq * p->head_dim > (int64_t)1 << 40)
+    return fail(CAS_ERR_UNSUPPORTED, "query tensor too large");
+  if (!p->seg_offsets) return fail(CAS_ERR_INVALID_ARGUMENT, "seg_offsets is NULL");
+  if (p->seg_offsets[0] != 0) return fail(CAS_ERR_INVALID_ARGUMENT, "seg_offsets[0] must be 0");
+  for (int b = 0; b < p->batch; ++b)
+    if (p->seg_offsets[b + 1] < p->seg_offsets[b])
+      return fail(CAS_ERR_INVALID_ARGUMENT, "seg_offsets must be non-decreasing");
+  const int32_t nent = p->seg_offsets[p->batch];
+  if (nent > (1 << 20)) return fail(CAS_ERR_UNSUPPORTED, "more than 2^20 segment entries");
+  if (nent > 0 && !p->segments) return fail(CAS_ERR_INVALID_ARGUMENT, "segments is NULL");
+
+  pl.dt = p->dtype == CAS_DTYPE_BF16 ? kBF16 : kFP32;
+  pl.esize = p->dtype == CAS_DTYPE_BF16 ? 2 : 4;
+  pl.B = p->batch;
+  pl.Sq = p->q_len;
+  pl.Hkv = p->num_kv_heads;
+  pl.g = p->group_size;
+  pl.Hq = (int)Hq;
+  pl.D = p->head_dim;
+  pl.nrows = (int)nrows;
+  pl.scale = p->softmax_scale;
+
+  const int D = pl.D, es = pl.esize, Hkv = pl.Hkv;
+  int64_t min_row_tiles = INT64_MAX;
+  pl.rows.resize(pl.B);
+  for (int b = 0; b < pl.B; ++b) {
+    DevRow r{};
+    r.seg_begin = (int32_t)pl.segs.size();
+    int64_t tiles = 0, plen = 0;
+    for (int i = p->seg_offsets[b]; i < p->seg_offsets[b + 1]; ++i) {
+      const cas_segment_t &s = p->segments[i];
+      if (s.len < 0) return fail(CAS_ERR_INVALID_ARGUMENT, "segment " + std::to_string(i) + ": negative len");
+      if (s.len == 0) continue;
+      if (!s.k || !s.v) return fail(CAS_ERR_INVALID_ARGUMENT, "segment " + std::to_string(i) + ": NULL k or v");
+      if (s.stride_tok < 1 || s.stride_head < 0 || (Hkv > 1 && s.stride_head < 1))
+        return fail(CAS_ERR_INVALID_ARGUMENT, "segment " + std::to_string(i) + ": bad strides");
+      if (!aligned16(s.k) || !aligned16(s.v) || !aligned16(s.dk) || !aligned16(s.dv) ||
+          (s.stride_tok * es) % 16 != 0 || (s.stride_head * es) % 16 != 0)
+        return fail(CAS_ERR_ALIGNMENT, "segment " + std::to_string(i) +
+                                           ": pointers and strides must be multiples of 16 bytes");
+      if (s.len > (1 << 30)) return fail(CAS_ERR_UNSUPPORTED, "segment longer than 2^30 tokens");
+      DevSeg d{};
+      d.k = s.k;
+      d.v = s.v;
+      d.stride_tok = s.stride_tok;
+      d.stride_head = s.stride_head;
+      d.len = (int32_t)s.len;
+      d.tile_begin = (int32_t)tiles;
+      tiles += ceil_div(s.len, kKeyTile);
+      plen += s.len;
+      pl.segs.push_back(d);
+    }
+    if (plen + pl.Sq > (int64_t)1 << 30)
+      return fail(CAS_ERR_UNSUPPORTED, "row " + std::to_string(b) + ": prefix longer than 2^30 tokens");
+    r.seg_end = (int32_t)pl.segs.size();
+    r.prefix_tiles = (int32_t)tiles;
+    pl.rows[b] = r;
+    pl.max_prefix = std::max(pl.max_prefix, plen);
+    min_row_tiles = std::min(min_row_tiles, tiles + 1);
+  }
+
+  const cas_tuning_t tu = tuning();
+  pl.nqblk_fwd = (int)ceil_div(pl.nrows, kRowsPerWg);
+  pl.nqblk_dq = (int)ceil_div(pl.nrows, kDqRowsPerWg);
+  const int64_t base_fwd = (int64_t)pl.B * Hkv * pl.nqblk_fwd;
+  const int64_t base_dq = (int64_t)pl.B * Hkv * pl.nqblk_dq;
+  pl.fwd_splits = tu.fwd_splits > 0 ? std::min(tu.fwd_splits, kMaxSplits) : auto_splits(base_fwd, min_row_tiles);
+  pl.dq_splits = tu.dq_splits > 0 ? std::min(tu.dq_splits, kMaxSplits) : auto_splits(base_dq, min_row_tiles);
+  if (base_fwd * pl.fwd_splits > INT32_MAX || base_dq * pl.dq_splits > INT32_MAX)
+    return fail(CAS_ERR_UNSUPPORTED, "grid too large");
+
+  if (bwd) {
+    // Fold entries that name the same cartridge storage into one cartridge.
+    std::map<std::tuple<uintptr_t, uintptr_t, int64_t, int64_t, int64_t>, int> index;
+    std::vector<std::vector<int32_t>> users;
+    std::vector<const cas_segment_t *> first;
+    for (int b = 0; b < pl.B; ++b) {
+      for (int i = p->seg_offsets[b]; i < p->seg_offsets[b + 1]; ++i) {
+        const cas_segment_t &s = p->segments[i];
+        if (s.len == 0) continue;
+        auto key = std::make_tuple((uintptr_t)s.k, (uintptr_t)s.v, s.len, s.stride_tok, s.stride_head);
+        auto it = index.find(key);
+        int u;
+        if (it == index.end()) {
+          u = (int)first.size();
+          index.emplace(key, u);
+          first.push_back(&s);
+          users.emplace_back();
+        } else {
+          u = it->second;
+          if (first[u]->dk != s.dk || first[u]->dv != s.dv)
+            return fail(CAS_ERR_INVALID_ARGUMENT, "segment " + std::to_string(i) +
+                                                      ": entries sharing k/v storage must share dk/dv");
+        }
+        users[u].push_back(b);
+      }
+    }
+    int64_t tiles = 0;
+    for (size_t u = 0; u < first.size(); ++u) {
+      const cas_segment_t &s = *first[u];
+      if (!s.dk && !s.dv) continue;
+      DevCart c{};
+      c.k = s.k;
+      c.v = s.v;
+      c.dk = s.dk;
+      c.dv = s.dv;
+      c.stride_tok = s.stride_tok;
+      c.stride_head = s.stride_head;
+      c.len = (int32_t)s.len;
+      c.tile_begin = (int32_t)tiles;
+      c.use_begin = (int32_t)pl.uses.size();
+      for (int32_t b : users[u]) pl.uses.push_back(b);
+      c.use_end = (int32_t)pl.uses.size();
+      tiles += ceil_div(s.len, kDkdvKeyTile);
+      pl.carts.push_back(c);
+      // A gradient buffer must not overlap itself under its strides.
+      int64_t s1 = s.stride_tok, n1 = s.len, s2 = s.stride_head, n2 = Hkv;
+      if (s1 > s2 || n1 == 1) {
+        std::swap(s1, s2);
+        std::swap(n1, n2);
+      }
+      bool ok = true;
+      if (n1 > 1 && s1 < D) ok = false;
+      if (n2 > 1 && (s2 < D || (n1 > 1 && s2 < s1 * n1))) ok = false;
+      if (!ok)
+        return fail(CAS_ERR_INVALID_ARGUMENT, "cartridge gradient layout overlaps itself");
+    }
+    if (tiles > INT32_MAX / 2) return fail(CAS_ERR_UNSUPPORTED, "too many key tiles");
+    pl.cart_tiles = (int)tiles;
+  }
+
+  // Workspace layout.
+  size_t off = 0;
+  pl.off_segs = off;
+  off = align_up(off + pl.segs.size() * sizeof(DevSeg), 256);
+  pl.off_rows = off;
+  off = align_up(off + pl.rows.size() * sizeof(DevRow), 256);
+  if (bwd) {
+    pl.off_carts = off;
+    off = align_up(off + pl.carts.size() * sizeof(DevCart), 256);
+    pl.off_uses = off;
+    off = align_up(off + pl.uses.size() * sizeof(int32_t), 256);
+  }
+  pl.table_bytes = off;
+  const size_t plane = (size_t)pl.B * Hkv * pl.nrows;
+  if (!bwd) {
+    if (pl.fwd_splits > 1) {
+      pl.off_part_o = off;
+      off = align_up(off + (size_t)pl.fwd_splits * plane * D * 4, 256);
+      pl.off_part_lse = off;
+      off = align_up(off + (size_t)pl.fwd_splits * plane * 4, 256);
+    }
+    pl.ws_fwd = off;
+  } else {
+    pl.off_dvec = off;
+    off = align_up(off + plane * 4, 256);
+    pl.off_lse2 = off;
+    off = align_up(off + plane * 4, 256);
+    if (pl.dq_splits > 1) {
+      pl.off_part_dq = off;
+      off = align_up(off + (size_t)pl.dq_splits * plane * D * 4, 256);
+    }
+    pl.ws_bwd = off;
+  }
+  return CAS_OK;
+}
+
+void add_segment_intervals(const Plan &pl, const cas_problem_t *p, bool with_grads,
+                           std::vector<Interval> &iv) {
+  const int es = pl.esize;
+  for (int i = 0; i < p->seg_offsets[p->batch]; ++i) {
+    const cas_segment_t &s = p->segments[i];
+    if (s.len == 0) continue;
+    const uintptr_t span = (uintptr_t)(((s.len - 1) * s.stride_tok + (pl.Hkv - 1) * s.stride_head + pl.D) * es);
+    iv.push_back({(uintptr_t)s.k, (uintptr_t)s.k + span, false, 0, "segment k"});
+    iv.push_back({(uintptr_t)s.v, (uintptr_t)s.v + span, false, 0, "segment v"});
+    if (with_grads) {
+      // Entries of one aliased cartridge carry identical (dk, dv) intervals.
+      if (s.dk) iv.push_back({(uintptr_t)s.dk, (uintptr_t)s.dk + span, true, (uintptr_t)s.dk, "segment dk"});
+      if (s.dv) iv.push_back({(uintptr_t)s.dv, (uintptr_t)s.dv + span, true, (uintptr_t)s.dv, "segment dv"});
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Pinned staging ring for segment tables (host -> workspace copies).
+// ---------------------------------------------------------------------------
+constexpr size_t kSlotBytes = 1 << 20;
+constexpr int kSlots = 8;
+
+struct Ring {
+  char *host = nullptr;
+  hipEvent_t ev[kSlots] = {};
+  bool used[kSlots] = {};
+  int next = 0;
+};
+
+std::mutex g_ring_mu;
+std::map<int, Ring> g_rings;
+
+cas_status_t upload_tables(const Plan &pl, bool bwd, void *ws, hipStream_t stream) {
+  if (pl.table_bytes > kSlotBytes)
+    return fail(CAS_ERR_UNSUPPORTED, "segment table larger than " + std::to_string(kSlotBytes) + " bytes");
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  std::lock_guard<std::mutex> lk(g_ring_mu);
+  Ring &r = g_rings[dev];
+  if (!r.host) {
+    e = hipHostMalloc((void **)&r.host, kSlotBytes * kSlots, hipHostMallocDefault);
+    if (e != hipSuccess) {
+      r.host = nullptr;
+      return fail(CAS_ERR_HIP, std::string("hipHostMalloc: ") + hipGetErrorString(e));
+    }
+    for (int i = 0; i < kSlots; ++i) {
+      e = hipEventCreateWithFlags(&r.ev[i], hipEventDisableTiming);
+      if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipEventCreate: ") + hipGetErrorString(e));
+    }
+  }
+  const int slot = r.next;
+  r.next = (r.next + 1) % kSlots;
+  if (r.used[slot]) {
+    e = hipEventSynchronize(r.ev[slot]);
+    if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipEventSynchronize: ") + hipGetErrorString(e));
+  }
+  char *h = r.host + (size_t)slot * kSlotBytes;
+  std::memset(h, 0, pl.table_bytes);
+  if (!pl.segs.empty()) std::memcpy(h + pl.off_segs, pl.segs.data(), pl.segs.size() * sizeof(DevSeg));
+  std::memcpy(h + pl.off_rows, pl.rows.data(), pl.rows.size() * sizeof(DevRow));
+  if (bwd) {
+    if (!pl.carts.empty()) std::memcpy(h + pl.off_carts, pl.carts.data(), pl.carts.size() * sizeof(DevCart));
+    if (!pl.uses.empty()) std::memcpy(h + pl.off_uses, pl.uses.data(), pl.uses.size() * sizeof(int32_t));
+  }
+  e = hipMemcpyAsync(ws, h, pl.table_bytes, hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipMemcpyAsync: ") + hipGetErrorString(e));
+  e = hipEventRecord(r.ev[slot], stream);
+  if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipEventRecord: ") + hipGetErrorString(e));
+  r.used[slot] = true;
+  return CAS_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Optional per-kernel timing.
+// ---------------------------------------------------------------------------
+struct TimedLaunch {
+  const char *name;
+  hipEvent_t a, b;
+};
+
+std::mutex g_time_mu;
+bool g_timing = false;
+std::vector<TimedLaunch> g_pending;
+std::vector<hipEvent_t> g_event_pool;
+std::map<std::string, std::pair<int, double>> g_totals;
+
+hipEvent_t pooled_event() {
+  if (!g_event_pool.empty()) {
+    hipEvent_t e = g_event_pool.back();
+    g_event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <typename F>
+hipError_t timed(const char *name, hipStream_t s, F &&launch) {
+  bool on;
+  {
+    std::lock_guard<std::mutex> lk(g_time_mu);
+    on = g_timing;
+  }
+  if (!on) return launch();
+  hipEvent_t a, b;
+  {
+    std::lock_guard<std::mutex> lk(g_time_mu);
+    a = pooled_event();
+    b = pooled_event();
+  }
+  if (!a || !b) return hipErrorOutOfMemory;
+  hipError_t e = hipEventRecord(a, s);
+  if (e != hipSuccess) return e;
+  e = launch();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(b, s);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(g_time_mu);
+  g_pending.push_back({name, a, b});
+  return hipSuccess;
+}
+
+cas_status_t hip_fail(const char *what, hipError_t e) {
+  return fail(CAS_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+cas_status_t check_workspace(void *ws, size_t have, size_t need) {
+  if (need > 0 && !ws) return fail(CAS_ERR_WORKSPACE, "workspace is NULL");
+  if (have < need)
+    return fail(CAS_ERR_WORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes, have " +
+                                       std::to_string(have));
+  if (!aligned16(ws)) return fail(CAS_ERR_ALIGNMENT, "workspace must be 16-byte aligned");
+  return CAS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t cas_abi_version(void) { return CAS_ABI_VERSION; }
+
+const char *cas_status_string(cas_status_t s) {
+  switch (s) {
+    case CAS_OK: return "CAS_OK";
+    case CAS_ERR_INVALID_ARGUMENT: return "CAS_ERR_INVALID_ARGUMENT";
+    case CAS_ERR_UNSUPPORTED: return "CAS_ERR_UNSUPPORTED";
+    case CAS_ERR_ALIGNMENT: return "CAS_ERR_ALIGNMENT";
+    case CAS_ERR_NOT_PINNED: return "CAS_ERR_NOT_PINNED";
+    case CAS_ERR_WORKSPACE: return "CAS_ERR_WORKSPACE";
+    case CAS_ERR_HIP: return "CAS_ERR_HIP";
+  }
+  return "CAS_ERR_UNKNOWN";
+}
+
+const char *cas_last_error_message(void) { return g_err.c_str(); }
+
+cas_status_t cas_set_tuning(const cas_tuning_t *t) {
+  if (!t) return fail(CAS_ERR_INVALID_ARGUMENT, "tuning is NULL");
+  if (t->fwd_splits < 0 || t->dq_splits < 0 || t->fwd_splits > kMaxSplits || t->dq_splits > kMaxSplits)
+    return fail(CAS_ERR_INVALID_ARGUMENT, "splits must be in [0, " + std::to_string(kMaxSplits) + "]");
+  std::lock_guard<std::mutex> lk(g_tuning_mu);
+  g_tuning = *t;
+  return CAS_OK;
+}
+
+cas_status_t cas_get_tuning(cas_tuning_t *t) {
+  if (!t) return fail(CAS_ERR_INVALID_ARGUMENT, "tuning is NULL");
+  *t = tuning();
+  return CAS_OK;
+}
+
+cas_status_t cas_prefix_attn_workspace_size(const cas_problem_t *p, int backward, size_t *bytes) {
+  if (!bytes) return fail(CAS_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  Plan pl;
+  cas_status_t s = build_plan(p, backward != 0, pl);
+  if (s != CAS_OK) return s;
+  *bytes = backward ? pl.ws_bwd : pl.ws_fwd;
+  return CAS_OK;
+}
+
+cas_status_t cas_plan_info(const cas_problem_t *p, cas_plan_info_t *out) {
+  if (!out) return fail(CAS_ERR_INVALID_ARGUMENT, "out is NULL");
+  Plan pf, pb;
+  cas_status_t s = build_plan(p, false, pf);
+  if (s != CAS_OK) return s;
+  s = build_plan(p, true, pb);
+  if (s != CAS_OK) return s;
+  out->fwd_splits = pf.fwd_splits;
+  out->dq_splits = pb.dq_splits;
+  out->fwd_workgroups = pf.nqblk_fwd * pf.Hkv * pf.B * pf.fwd_splits;
+  const int self_tiles = (int)ceil_div(pb.Sq, kDkdvKeyTile);
+  out->dkdv_workgroups = (pb.cart_tiles + pb.B * self_tiles) * pb.Hkv;
+  out->unique_segments = (int32_t)pb.carts.size();
+  out->total_key_tiles = pb.cart_tiles + pb.B * self_tiles;
+  out->max_prefix_len = pf.max_prefix;
+  out->ws_fwd_bytes = pf.ws_fwd;
+  out->ws_bwd_bytes = pb.ws_bwd;
+  return CAS_OK;
+}
+
+cas_status_t cas_prefix_attn_fwd(const cas_problem_t *p, const void *q, const void *k_self,
+                                 const void *v_self, void *o, float *lse, void *workspace,
+                                 size_t ws_bytes, void *hip_stream) {
+  Plan pl;
+  cas_status_t s = build_plan(p, false, pl);
+  if (s != CAS_OK) return s;
+  if (!q || !k_self || !v_self || !o) return fail(CAS_ERR_INVALID_ARGUMENT, "q, k_self, v_self and o must be non-NULL");
+  if (!aligned16(q) || !aligned16(k_self) || !aligned16(v_self) || !aligned16(o) || ((uintptr_t)lse & 3u))
+    return fail(CAS_ERR_ALIGNMENT, "tensors must be 16-byte aligned (lse 4-byte)");
+  const uintptr_t qbytes = (uintptr_t)pl.B * pl.Sq * pl.Hq * pl.D * pl.esize;
+  const uintptr_t kvbytes = (uintptr_t)pl.B * pl.Sq * pl.Hkv * pl.D * pl.esize;
+  std::vector<Interval> iv;
+  iv.push_back({(uintptr_t)q, (uintptr_t)q + qbytes, false, 0, "q"});
+  iv.push_back({(uintptr_t)k_self, (uintptr_t)k_self + kvbytes, false, 0, "k_self"});
+  iv.push_back({(uintptr_t)v_self, (uintptr_t)v_self + kvbytes, false, 0, "v_self"});
+  iv.push_back({(uintptr_t)o, (uintptr_t)o + qbytes, true, (uintptr_t)o, "o"});
+  if (lse) iv.push_back({(uintptr_t)lse, (uintptr_t)lse + (uintptr_t)pl.B * pl.Hq * pl.Sq * 4, true, (uintptr_t)lse, "lse"});
+  add_segment_intervals(pl, p, false, iv);
+  std::string msg;
+  if (!overlap_free(iv, msg)) return fail(CAS_ERR_INVALID_ARGUMENT, msg);
+  s = check_workspace(workspace, ws_bytes, pl.ws_fwd);
+  if (s != CAS_OK) return s;
+
+  hipStream_t stream = (hipStream_t)hip_stream;
+  s = upload_tables(pl, false, workspace, stream);
+  if (s != CAS_OK) return s;
+  char *ws = (char *)workspace;
+  FwdParams fp{};
+  fp.q = q;
+  fp.k_self = k_self;
+  fp.v_self = v_self;
+  fp.o = o;
+  fp.lse = lse;
+  fp.part_o = pl.fwd_splits > 1 ? (float *)(ws + pl.off_part_o) : nullptr;
+  fp.part_lse = pl.fwd_splits > 1 ? (float *)(ws + pl.off_part_lse) : nullptr;
+  fp.segs = (const DevSeg *)(ws + pl.off_segs);
+  fp.rows = (const DevRow *)(ws + pl.off_rows);
+  fp.B = pl.B;
+  fp.Sq = pl.Sq;
+  fp.Hkv = pl.Hkv;
+  fp.g = pl.g;
+  fp.nrows = pl.nrows;
+  fp.nqblk = pl.nqblk_fwd;
+  fp.splits = pl.fwd_splits;
+  fp.scale_log2 = pl.scale * 1.4426950408889634f;
+  hipError_t e = timed("fwd", stream, [&] { return launch_fwd(fp, pl.dt, pl.D, stream); });
+  if (e != hipSuccess) return hip_fail("fwd launch", e);
+  if (pl.fwd_splits > 1) {
+    MergeParams mp{};
+    mp.part_o = fp.part_o;
+    mp.part_lse = fp.part_lse;
+    mp.o = o;
+    mp.lse = lse;
+    mp.B = pl.B;
+    mp.Sq = pl.Sq;
+    mp.Hkv = pl.Hkv;
+    mp.g = pl.g;
+    mp.nrows = pl.nrows;
+    mp.splits = pl.fwd_splits;
+    e = timed("fwd_merge", stream, [&] { return launch_fwd_merge(mp, pl.dt, pl.D, stream); });
+    if (e != hipSuccess) return hip_fail("fwd_merge launch", e);
+  }
+  return CAS_OK;
+}
+
+cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const void *k_self,
+                                 const void *v_self, const void *o, const float *lse,
+                                 const void *d_o, void *dq, void *dk_self, void *dv_self,
+                                 void *workspace, size_t ws_bytes, void *hip_stream) {
+  Plan pl;
+  cas_status_t s = build_plan(p, true, pl);
+  if (s != CAS_OK) return s;
+  if (!q || !k_self || !v_self || !o || !lse || !d_o)
+    return fail(CAS_ERR_INVALID_ARGUMENT, "q, k_self, v_self, o, lse and d_o must be non-NULL");
+  if (!aligned16(q) || !aligned16(k_self) || !aligned16(v_self) || !aligned16(o) || !aligned16(d_o) ||
+      !aligned16(dq) || !aligned16(dk_self) || !aligned16(dv_self) || ((uintptr_t)lse & 3u))
+    return fail(CAS_ERR_ALIGNMENT, "tensors must be 16-byte aligned (lse 4-byte)");
+  const uintptr_t qbytes = (uintptr_t)pl.B * pl.Sq * pl.Hq * pl.D * pl.esize;
+  const uintptr_t kvbytes = (uintptr_t)pl.B * pl.Sq * pl.Hkv * pl.D * pl.esize;
+  std::vector<Interval> iv;
+  iv.push_back({(uintptr_t)q, (uintptr_t)q + qbytes, false, 0, "q"});
+  iv.push_back({(uintptr_t)k_self, (uintptr_t)k_self + kvbytes, false, 0, "k_self"});
+  iv.push_back({(uintptr_t)v_self, (uintptr_t)v_self + kvbytes, false, 0, "v_self"});
+  iv.push_back({(uintptr_t)o, (uintptr_t)o + qbytes, false, 0, "o"});
+  iv.push_back({(uintptr_t)lse, (uintptr_t)lse + (uintptr_t)pl.B * pl.Hq * pl.Sq * 4, false, 0, "lse"});
+  iv.push_back({(uintptr_t)d_o, (uintptr_t)d_o + qbytes, false, 0, "d_o"});
+  if (dq) iv.push_back({(uintptr_t)dq, (uintptr_t)dq + qbytes, true, (uintptr_t)dq, "dq"});
+  if (dk_self) iv.push_back({(uintptr_t)dk_self, (uintptr_t)dk_self + kvbytes, true, (uintptr_t)dk_self, "dk_self"});
+  if (dv_self) iv.push_back({(uintptr_t)dv_self, (uintptr_t)dv_self + kvbytes, true, (uintptr_t)dv_self, "dv_self"});
+  add_segment_intervals(pl, p, true, iv);
+  std::string msg;
+  if (!overlap_free(iv, msg)) return fail(CAS_ERR_INVALID_ARGUMENT, msg);
+  s = check_workspace(workspace, ws_bytes, pl.ws_bwd);
+  if (s != CAS_OK) return s;
+
+  hipStream_t stream = (hipStream_t)hip_stream;
+  s = upload_tables(pl, true, workspace, stream);
+  if (s != CAS_OK) return s;
+  char *ws = (char *)workspace;
+  float *dvec = (float *)(ws + pl.off_dvec);
+  float *lse2 = (float *)(ws + pl.off_lse2);
+  const float scale_log2 = pl.scale * 1.4426950408889634f;
+
+  PreParams pp{};
+  pp.o = o;
+  pp.d_o = d_o;
+  pp.lse = lse;
+  pp.dvec = dvec;
+  pp.lse2 = lse2;
+  pp.B = pl.B;
+  pp.Sq = pl.Sq;
+  pp.Hkv = pl.Hkv;
+  pp.g = pl.g;
+  pp.nrows = pl.nrows;
+  hipError_t e = timed("bwd_pre", stream, [&] { return launch_bwd_pre(pp, pl.dt, pl.D, stream); });
+  if (e != hipSuccess) return hip_fail("bwd_pre launch", e);
+
+  const int self_tiles = (dk_self || dv_self) ? (int)ceil_div(pl.Sq, kDkdvKeyTile) : 0;
+  const int gx = pl.cart_tiles + pl.B * self_tiles;
+  if (gx > 0) {
+    DkdvParams kp{};
+    kp.q = q;
+    kp.k_self = k_self;
+    kp.v_self = v_self;
+    kp.d_o = d_o;
+    kp.dvec = dvec;
+    kp.lse2 = lse2;
+    kp.dk_self = dk_self;
+    kp.dv_self = dv_self;
+    kp.carts = (const DevCart *)(ws + pl.off_carts);
+    kp.uses = (const int32_t *)(ws + pl.off_uses);
+    kp.n_carts = (int32_t)pl.carts.size();
+    kp.cart_tiles = pl.cart_tiles;
+    kp.self_tiles = std::max(self_tiles, 1);
+    kp.B = pl.B;
+    kp.Sq = pl.Sq;
+    kp.Hkv = pl.Hkv;
+    kp.g = pl.g;
+    kp.nrows = pl.nrows;
+    kp.scale_log2 = scale_log2;
+    kp.scale = pl.scale;
+    e = timed("dkdv", stream, [&] { return launch_dkdv(kp, pl.dt, pl.D, gx, stream); });
+    if (e != hipSuccess) return hip_fail("dkdv launch", e);
+  }
+
+  if (dq) {
+    DqParams dp{};
+    dp.q = q;
+    dp.k_self = k_self;
+    dp.v_self = v_self;
+    dp.d_o = d_o;
+    dp.dvec = dvec;
+    dp.lse2 = lse2;
+    dp.dq = dq;
+    dp.part_dq = pl.dq_splits > 1 ? (float *)(ws + pl.off_part_dq) : nullptr;
+    dp.segs = (const DevSeg *)(ws + pl.off_segs);
+    dp.rows = (const DevRow *)(ws + pl.off_rows);
+    dp.B = pl.B;
+    dp.Sq = pl.Sq;
+    dp.Hkv = pl.Hkv;
+    dp.g = pl.g;
+    dp.nrows = pl.nrows;
+    dp.nqblk = pl.nqblk_dq;
+    dp.splits = pl.dq_splits;
+    dp.scale_log2 = scale_log2;
+    dp.scale = pl.scale;
+    e = timed("dq", stream, [&] { return launch_dq(dp, pl.dt, pl.D, stream); });
+    if (e != hipSuccess) return hip_fail("dq launch", e);
+    if (pl.dq_splits > 1) {
+      DqReduceParams rp{};
+      rp.part_dq = dp.part_dq;
+      rp.dq = dq;
+      rp.B = pl.B;
+      rp.Sq = pl.Sq;
+      rp.Hkv = pl.Hkv;
+      rp.g = pl.g;
+      rp.nrows = pl.nrows;
+      rp.splits = pl.dq_splits;
+      rp.scale = pl.scale;
+      e = timed("dq_reduce", stream, [&] { return launch_dq_reduce(rp, pl.dt, pl.D, stream); });
+      if (e != hipSuccess) return hip_fail("dq_reduce launch", e);
+    }
+  }
+  return CAS_OK;
+}
+
+cas_status_t cas_cartridge_stage(const cas_stage_copy_t *copies, int32_t n, void *side_stream,
+                                 void *done_event) {
+  if (n < 0) return fail(CAS_ERR_INVALID_ARGUMENT, "n must be >= 0");
+  if (n > 0 && !copies) return fail(CAS_ERR_INVALID_ARGUMENT, "copies is NULL");
+  for (int i = 0; i < n; ++i) {
+    if (copies[i].bytes == 0) continue;
+    if (!copies[i].host_src || !copies[i].dev_dst)
+      return fail(CAS_ERR_INVALID_ARGUMENT, "copy " + std::to_string(i) + ": NULL pointer");
+  }
+  for (int i = 0; i < n; ++i) {
+    const cas_stage_copy_t &c = copies[i];
+    if (c.bytes == 0) continue;
+    const void *ends[2] = {c.host_src, (const char *)c.host_src + c.bytes - 1};
+    for (const void *ptr : ends) {
+      hipPointerAttribute_t a;
+      hipError_t e = hipPointerGetAttributes(&a, ptr);
+      if (e != hipSuccess || a.type != hipMemoryTypeHost) {
+        (void)hipGetLastError();
+        return fail(CAS_ERR_NOT_PINNED, "copy " + std::to_string(i) + ": host_src is not pinned host memory");
+      }
+    }
+    hipPointerAttribute_t d;
+    hipError_t e = hipPointerGetAttributes(&d, c.dev_dst);
+    if (e != hipSuccess || d.type != hipMemoryTypeDevice) {
+      (void)hipGetLastError();
+      return fail(CAS_ERR_INVALID_ARGUMENT, "copy " + std::to_string(i) + ": dev_dst is not device memory");
+    }
+  }
+  hipStream_t s = (hipStream_t)side_stream;
+  for (int i = 0; i < n; ++i) {
+    const cas_stage_copy_t &c = copies[i];
+    if (c.bytes == 0) continue;
+    hipError_t e = hipMemcpyAsync(c.dev_dst, c.host_src, c.bytes, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_fail("hipMemcpyAsync", e);
+  }
+  if (done_event) {
+    hipError_t e = hipEventRecord((hipEvent_t)done_event, s);
+    if (e != hipSuccess) return hip_fail("hipEventRecord", e);
+  }
+  return CAS_OK;
+}
+
+cas_status_t cas_timing_enable(int enable) {
+  std::lock_guard<std::mutex> lk(g_time_mu);
+  g_timing = enable != 0;
+  return CAS_OK;
+}
+
+cas_status_t cas_timing_reset(void) {
+  std::lock_guard<std::mutex> lk(g_time_mu);
+  for (auto &t : g_pending) {
+    (void)hipEventSynchronize(t.b);
+    g_event_pool.push_back(t.a);
+    g_event_pool.push_back(t.b);
+  }
+  g_pending.clear();
+  g_totals.clear();
+  return CAS_OK;
+}
+
+cas_status_t cas_timing_read(cas_kernel_time_t *out, int32_t cap, int32_t *n_out) {
+  if (!n_out || (cap > 0 && !out)) return fail(CAS_ERR_INVALID_ARGUMENT, "NULL output");
+  std::lock_guard<std::mutex> lk(g_time_mu);
+  for (auto &t : g_pending) {
+    hipError_t e = hipEventSynchronize(t.b);
+    if (e != hipSuccess) return hip_fail("hipEventSynchronize", e);
+    float ms = 0.0f;
+    e = hipEventElapsedTime(&ms, t.a, t.b);
+    if (e != hipSuccess) return hip_fail("hipEventElapsedTime", e);
+    auto &acc = g_totals[t.name];
+    acc.first += 1;
+    acc.second += ms;
+    g_event_pool.push_back(t.a);
+    g_event_pool.push_back(t.b);
+  }
+  g_pending.clear();
+  int32_t i = 0;
+  for (auto &kv : g_totals) {
+    if (i < cap) {
+      std::memset(out[i].name, 0, sizeof(out[i].name));
+      std::strncpy(out[i].name, kv.first.c_str(), sizeof(out[i].name) - 1);
+      out[i].launches = kv.second.first;
+      out[i].total_ms = kv.second.second;
+    }
+    ++i;
+  }
+  *n_out = i;
+  return CAS_OK;
+}
+
+}  // extern "C"

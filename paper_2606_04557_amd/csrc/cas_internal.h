@@ -1,0 +1,140 @@
+// Internal layouts shared by the libcas host planner and its HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cas {
+
+// Work decomposition (gfx950: 64-lane waves, 4 SIMDs per CU).
+constexpr int kThreads = 256;       // 4 waves per workgroup
+constexpr int kWaves = kThreads / 64;
+constexpr int kRowsPerWave = 64;    // packed query rows a wave owns in fwd / dQ
+constexpr int kRowsPerWg = kRowsPerWave * kWaves;   // 256
+constexpr int kDqRowsPerWave = 32;  // dQ holds Q, dO and the dQ sums in registers
+constexpr int kDqRowsPerWg = kDqRowsPerWave * kWaves;  // 128
+constexpr int kKeyTile = 64;        // keys per LDS tile in fwd / dQ
+constexpr int kDkdvKeysPerWave = 32;
+constexpr int kDkdvKeyTile = kDkdvKeysPerWave * kWaves;  // 128 keys per dK/dV workgroup
+constexpr int kDkdvQBlock = 64;     // query rows per LDS block in dK/dV
+constexpr int kMaxSplits = 32;
+
+// A "packed row" r of (batch b, kv head kvh) is query position t = r / g of
+// query head kvh*g + r % g: the g heads of one position are adjacent rows, so
+// one K/V tile in LDS serves the whole GQA group.
+
+// Prefix entry of one batch row (forward and dQ walks).
+struct DevSeg {
+  const void *k;
+  const void *v;
+  int64_t stride_tok;
+  int64_t stride_head;
+  int32_t len;
+  int32_t tile_begin;   // first kKeyTile tile of this entry within the row's prefix
+};
+
+struct DevRow {
+  int32_t seg_begin;
+  int32_t seg_end;
+  int32_t prefix_tiles;  // kKeyTile tiles over the row's whole prefix
+  int32_t pad;
+};
+
+// Distinct cartridge after alias folding (dK/dV pass).
+struct DevCart {
+  const void *k;
+  const void *v;
+  void *dk;
+  void *dv;
+  int64_t stride_tok;
+  int64_t stride_head;
+  int32_t len;
+  int32_t tile_begin;   // first kDkdvKeyTile tile in the dK/dV grid
+  int32_t use_begin;    // uses[use_begin .. use_end) = batch rows referencing it
+  int32_t use_end;
+};
+
+enum DType : int32_t { kBF16 = 0, kFP32 = 1 };
+
+struct FwdParams {
+  const void *q;
+  const void *k_self;
+  const void *v_self;
+  void *o;
+  float *lse;
+  float *part_o;      // [splits][B][Hkv][nrows][D] when splits > 1
+  float *part_lse;    // [splits][B][Hkv][nrows]
+  const DevSeg *segs;
+  const DevRow *rows;
+  int32_t B, Sq, Hkv, g, nrows, nqblk, splits;
+  float scale_log2;   // softmax_scale * log2(e)
+};
+
+struct MergeParams {
+  const float *part_o;
+  const float *part_lse;
+  void *o;
+  float *lse;
+  int32_t B, Sq, Hkv, g, nrows, splits;
+};
+
+struct PreParams {
+  const void *o;
+  const void *d_o;
+  const float *lse;
+  float *dvec;   // [B][Hkv][nrows]  rowsum(dO * O)
+  float *lse2;   // [B][Hkv][nrows]  LSE * log2(e)
+  int32_t B, Sq, Hkv, g, nrows;
+};
+
+struct DqParams {
+  const void *q;
+  const void *k_self;
+  const void *v_self;
+  const void *d_o;
+  const float *dvec;
+  const float *lse2;
+  void *dq;
+  float *part_dq;   // [splits][B][Hkv][nrows][D] when splits > 1
+  const DevSeg *segs;
+  const DevRow *rows;
+  int32_t B, Sq, Hkv, g, nrows, nqblk, splits;
+  float scale_log2;
+  float scale;
+};
+
+struct DqReduceParams {
+  const float *part_dq;
+  void *dq;
+  int32_t B, Sq, Hkv, g, nrows, splits;
+  float scale;
+};
+
+struct DkdvParams {
+  const void *q;
+  const void *k_self;
+  const void *v_self;
+  const void *d_o;
+  const float *dvec;
+  const float *lse2;
+  void *dk_self;
+  void *dv_self;
+  const DevCart *carts;
+  const int32_t *uses;
+  int32_t n_carts;
+  int32_t cart_tiles;       // dK/dV tiles over all distinct cartridges
+  int32_t self_tiles;       // dK/dV tiles per batch row over the self keys
+  int32_t B, Sq, Hkv, g, nrows;
+  float scale_log2;
+  float scale;
+};
+
+// Kernel launchers (defined in the .hip files).
+hipError_t launch_fwd(const FwdParams &p, DType dt, int D, hipStream_t s);
+hipError_t launch_fwd_merge(const MergeParams &p, DType dt, int D, hipStream_t s);
+hipError_t launch_bwd_pre(const PreParams &p, DType dt, int D, hipStream_t s);
+hipError_t launch_dq(const DqParams &p, DType dt, int D, hipStream_t s);
+hipError_t launch_dq_reduce(const DqReduceParams &p, DType dt, int D, hipStream_t s);
+hipError_t launch_dkdv(const DkdvParams &p, DType dt, int D, int grid_x, hipStream_t s);
+
+}  // namespace cas

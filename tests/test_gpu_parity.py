@@ -1,0 +1,179 @@
+"""GPU parity: libcas (through the C ABI) against the fp64 oracle on the same
+seeded input bits.
+
+Bars: max |gpu - oracle| / max |oracle| <= 1e-5 for fp32 inputs and <= 2e-2
+for bf16 inputs, per output tensor (per cartridge for dK/dV); LSE absolute
+error <= 1e-5 (fp32) / 1e-3 (bf16). Small cases compare every element; the
+benchmark-size cases compare sampled rows and keys the oracle evaluates one by
+one, plus whole-tensor properties.
+"""
+import numpy as np
+import pytest
+
+import casgen
+import oracle
+from gpu_util import GpuCase, LSE_TOL, TOL, full_oracle, host, rel_err
+
+pytestmark = pytest.mark.gpu
+
+
+def _sync():
+    import torch
+    torch.cuda.synchronize()
+
+
+def _check_full(case, label=""):
+    import torch
+    wl = case.wl
+    o, lse = case.fwd()
+    dq, dks, dvs = case.bwd(o, lse)
+    _sync()
+    O, LSE, (rdq, rdks, rdvs, rdck, rdcv) = full_oracle(case)
+    tol = TOL[wl.dtype]
+    errs = {
+        "o": rel_err(host(o), O),
+        "lse": float(np.abs(host(lse) - LSE).max()),
+        "dq": rel_err(host(dq), rdq),
+        "dk_self": rel_err(host(dks), rdks),
+        "dv_self": rel_err(host(dvs), rdvs),
+    }
+    for c in case.dk:
+        errs[f"dk[{c}]"] = rel_err(host(case.dk[c]), rdck[c])
+        errs[f"dv[{c}]"] = rel_err(host(case.dv[c]), rdcv[c])
+    print(label, {k: f"{v:.2e}" for k, v in errs.items()})
+    for k, v in errs.items():
+        lim = LSE_TOL[wl.dtype] if k == "lse" else tol
+        assert v <= lim, (label, k, v, errs)
+    # Padding between tokens of padded-stride gradients is never written.
+    for (kind, c), base in case.bases.items():
+        if base.dim() == 2 and base.shape[1] > wl.num_kv_heads * wl.head_dim:
+            assert torch.isnan(base[:, wl.num_kv_heads * wl.head_dim:].float()).all(), (kind, c)
+    return o, lse
+
+
+def test_c1_fp32_full():
+    """The tiny fp32 configuration, every output element."""
+    _check_full(GpuCase(casgen.config(1)), "C1")
+
+
+def test_c1_fp32_forced_splits():
+    import paper_2606_04557_amd as cas
+    try:
+        cas.set_tuning(fwd_splits=3, dq_splits=2)
+        _check_full(GpuCase(casgen.config(1)), "C1 split")
+    finally:
+        cas.set_tuning(0, 0)
+
+
+SMALL = [
+    # ragged cartridge tails, a zero-length and a one-token cartridge, mixed layouts, 2.3 q-blocks
+    dict(name="ragged", dtype="bf16", batch=2, q_len=150, num_q_heads=8, num_kv_heads=2,
+         head_dim=128, cart_lens=[100, 0, 1, 64, 130, 257], rows=[[0, 1, 2], [3, 4, 5]],
+         layouts=["tok", "tok", "padded", "head", "padded", "head"]),
+    dict(name="d64_g1", dtype="bf16", batch=1, q_len=70, num_q_heads=4, num_kv_heads=4,
+         head_dim=64, cart_lens=[33, 64], rows=[[0, 1]]),
+    dict(name="g3", dtype="bf16", batch=1, q_len=90, num_q_heads=6, num_kv_heads=2, head_dim=128,
+         cart_lens=[200], rows=[[0]]),
+    # one cartridge referenced by every row, twice in the last one
+    dict(name="alias", dtype="bf16", batch=3, q_len=40, num_q_heads=4, num_kv_heads=1,
+         head_dim=128, cart_lens=[70, 129], rows=[[0, 1], [1, 0], [0, 0]]),
+    dict(name="no_prefix", dtype="bf16", batch=2, q_len=257, num_q_heads=4, num_kv_heads=2,
+         head_dim=128, cart_lens=[], rows=[[], []]),
+    dict(name="fp32_d128", dtype="fp32", batch=1, q_len=33, num_q_heads=4, num_kv_heads=2,
+         head_dim=128, cart_lens=[65, 3], rows=[[0, 1]]),
+    dict(name="fp32_alias", dtype="fp32", batch=2, q_len=20, num_q_heads=2, num_kv_heads=1,
+         head_dim=64, cart_lens=[31], rows=[[0], [0]]),
+]
+
+
+@pytest.mark.parametrize("spec", SMALL, ids=[s["name"] for s in SMALL])
+def test_small_full(spec):
+    spec = dict(spec)
+    name = spec.pop("name")
+    wl = casgen.custom(name, seed=100 + len(name), cart_std=0.5, **spec)
+    _check_full(GpuCase(wl), name)
+
+
+@pytest.mark.parametrize("spec", SMALL[:4], ids=[s["name"] for s in SMALL[:4]])
+def test_small_forced_splits(spec):
+    import paper_2606_04557_amd as cas
+    spec = dict(spec)
+    name = spec.pop("name")
+    wl = casgen.custom(name, seed=200 + len(name), cart_std=0.5, **spec)
+    try:
+        cas.set_tuning(fwd_splits=5, dq_splits=3)
+        _check_full(GpuCase(wl), name + " split")
+    finally:
+        cas.set_tuning(0, 0)
+
+
+def _sampled_check(case, n_rows=24, key_targets=None, seed=0, forward_only=False):
+    """Oracle evaluated on sampled query rows (O, LSE, dQ) and sampled keys (dK, dV)."""
+    wl = case.wl
+    o, lse = case.fwd()
+    grads = None
+    if not forward_only:
+        grads = case.bwd(o, lse)
+    _sync()
+    args = case.oracle_args()
+    d_o = None if forward_only else case.oracle_do()
+    rng = np.random.default_rng(seed)
+    B, Sq, Hq = wl.batch, wl.q_len, wl.num_q_heads
+    picks = [(int(rng.integers(B)), int(rng.integers(Hq)), int(rng.integers(Sq))) for _ in range(n_rows)]
+    picks += [(0, 0, 0), (B - 1, Hq - 1, Sq - 1), (0, Hq // 2, min(Sq - 1, 63)),
+              (B - 1, 1, min(Sq - 1, 64))]
+    go, glse = host(o), host(lse)
+    gdq = host(grads[0]) if grads else None
+    ro, rl, rq, vo, vl, vq = [], [], [], [], [], []
+    for (b, h, t) in picks:
+        oo, ll, dd = oracle.rows_forward_backward(*args, b=b, h=h, t_idx=[t], d_o=d_o)
+        ro.append(oo[0]); rl.append(ll[0]); vo.append(go[b, t, h]); vl.append(glse[b, h, t])
+        if grads:
+            rq.append(dd[0]); vq.append(gdq[b, t, h])
+    tol = TOL[wl.dtype]
+    e_o = rel_err(np.array(vo), np.array(ro))
+    e_l = float(np.abs(np.array(vl) - np.array(rl)).max())
+    print(wl.name, "sampled O", f"{e_o:.2e}", "LSE", f"{e_l:.2e}")
+    assert e_o <= tol and e_l <= LSE_TOL[wl.dtype]
+    if grads:
+        e_q = rel_err(np.array(vq), np.array(rq))
+        print(wl.name, "sampled dQ", f"{e_q:.2e}")
+        assert e_q <= tol
+        for kv, targets in (key_targets or {}).items():
+            res = oracle.key_grads_many(*args, d_o, kv=kv, targets=targets)
+            for (cart, toks), (rk, rv) in zip(targets, res):
+                if cart >= 0:
+                    gk = host(case.dk[cart][toks, kv])
+                    gv = host(case.dv[cart][toks, kv])
+                else:
+                    gk = host(grads[1][-cart - 1, toks, kv])
+                    gv = host(grads[2][-cart - 1, toks, kv])
+                ek, ev = rel_err(gk, rk), rel_err(gv, rv)
+                print(wl.name, f"kv{kv} cart{cart} dK {ek:.2e} dV {ev:.2e}")
+                assert ek <= tol and ev <= tol
+    return o, lse, grads
+
+
+def _gradient_sums(case, grads):
+    """Whole-tensor property: per (row, kv head) with no cartridge shared between
+    rows, the dV rows over all visible keys sum to the sum of dO over the group's
+    query rows (softmax rows sum to one)."""
+    import torch
+    wl = case.wl
+    g = wl.group_size
+    do = case.d_o.float()
+    for b in range(wl.batch):
+        tot = grads[2][b].float().sum(0)                      # [Hkv, D]
+        for c in wl.rows[b]:
+            tot = tot + case.dv[c].float().sum(0)
+        exp = do[b].view(wl.q_len, wl.num_kv_heads, g, wl.head_dim).sum((0, 2))
+        err = (tot - exp).abs().max().item() / exp.abs().max().item()
+        print(wl.name, "sum dV rel err", f"{err:.2e}")
+        assert err <= 2e-2
+
+
+def test_c2_full_size_sampled():
+    case = GpuCase(casgen.config(2))
+    targets = {3: [(0, [0, 511, 1023]), (13, [5, 1000]), (-1, [0, 1023]), (-4, [512])]}
+    o, lse, grads = _sampled_check(case, key_targets=targets)
+    _gradient_sums(case, grads)

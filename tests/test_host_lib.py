@@ -1,0 +1,245 @@
+"""Host-side checks of libcas that need no GPU: the library loads, exports
+every function include/cas.h declares, validates arguments before touching
+the device, and plans launches (splits, alias folding, workspace sizes).
+
+Device pointers here are fabricated addresses: every call either fails
+validation (which happens before any HIP call) or is a pure planning query.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_04557_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def test_exports_match_header(lib):
+    hdr = open(os.path.join(ROOT, "include", "cas.h")).read()
+    declared = sorted(set(re.findall(r"\b(cas_[a-z_0-9]+)\s*\(", hdr)))
+    assert declared == sorted(_lib.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert lib.cas_abi_version() == 1
+    assert lib.cas_status_string(_lib.CAS_ERR_NOT_PINNED) == b"CAS_ERR_NOT_PINNED"
+
+
+BASE = 1 << 32     # fabricated, 16-byte aligned device addresses
+
+
+class Fake:
+    """Builds a cas_problem_t over fabricated addresses."""
+
+    def __init__(self, B=1, Sq=8, Hkv=2, g=2, D=64, dtype=_lib.CAS_DTYPE_BF16, scale=0.125,
+                 rows=((16, 8),), grads=True):
+        self.B, self.Sq, self.Hkv, self.g, self.D = B, Sq, Hkv, g, D
+        es = 2 if dtype == _lib.CAS_DTYPE_BF16 else 4
+        self.es = es
+        self.next = BASE
+        nent = sum(len(r) for r in rows)
+        self.segs = (_lib.Segment * max(1, nent))()
+        self.offs = (ctypes.c_int32 * (B + 1))()
+        i = 0
+        for b in range(B):
+            self.offs[b] = i
+            for L in rows[b]:
+                s = self.segs[i]
+                nbytes = max(1, L) * Hkv * D * es
+                s.k, s.v = self.alloc(nbytes), self.alloc(nbytes)
+                if grads:
+                    s.dk, s.dv = self.alloc(nbytes), self.alloc(nbytes)
+                s.len, s.stride_tok, s.stride_head = L, Hkv * D, D
+                i += 1
+        self.offs[B] = i
+        self.p = _lib.Problem(dtype, B, Sq, Hkv, g, D, scale,
+                              ctypes.cast(self.segs, ctypes.POINTER(_lib.Segment)),
+                              ctypes.cast(self.offs, ctypes.POINTER(ctypes.c_int32)))
+        qn = B * Sq * Hkv * g * D * es
+        kvn = B * Sq * Hkv * D * es
+        self.q, self.ks, self.vs, self.o, self.do = (self.alloc(qn), self.alloc(kvn), self.alloc(kvn),
+                                                      self.alloc(qn), self.alloc(qn))
+        self.lse = self.alloc(B * Hkv * g * Sq * 4)
+        self.dq, self.dks, self.dvs = self.alloc(qn), self.alloc(kvn), self.alloc(kvn)
+        self.ws = self.alloc(1 << 30)
+
+    def alloc(self, n):
+        a = self.next
+        self.next += (n + 4095) // 4096 * 4096 + 4096
+        return a
+
+    def fwd(self, lib, ws_bytes=1 << 30, **over):
+        a = dict(q=self.q, ks=self.ks, vs=self.vs, o=self.o, lse=self.lse, ws=self.ws)
+        a.update(over)
+        return lib.cas_prefix_attn_fwd(ctypes.byref(self.p), a["q"], a["ks"], a["vs"], a["o"], a["lse"],
+                                       a["ws"], ws_bytes, None)
+
+    def bwd(self, lib, ws_bytes=1 << 30, **over):
+        a = dict(q=self.q, ks=self.ks, vs=self.vs, o=self.o, lse=self.lse, do=self.do, dq=self.dq,
+                 dks=self.dks, dvs=self.dvs, ws=self.ws)
+        a.update(over)
+        return lib.cas_prefix_attn_bwd(ctypes.byref(self.p), a["q"], a["ks"], a["vs"], a["o"], a["lse"],
+                                       a["do"], a["dq"], a["dks"], a["dvs"], a["ws"], ws_bytes, None)
+
+
+def _msg(lib):
+    return lib.cas_last_error_message().decode()
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("batch", 0, _lib.CAS_ERR_INVALID_ARGUMENT),
+    ("q_len", 0, _lib.CAS_ERR_INVALID_ARGUMENT),
+    ("num_kv_heads", -1, _lib.CAS_ERR_INVALID_ARGUMENT),
+    ("group_size", 0, _lib.CAS_ERR_INVALID_ARGUMENT),
+    ("head_dim", 96, _lib.CAS_ERR_UNSUPPORTED),
+    ("softmax_scale", 0.0, _lib.CAS_ERR_INVALID_ARGUMENT),
+    ("softmax_scale", float("inf"), _lib.CAS_ERR_INVALID_ARGUMENT),
+    ("dtype", 7, _lib.CAS_ERR_INVALID_ARGUMENT),
+])
+def test_shape_validation(lib, field, value, code):
+    f = Fake()
+    setattr(f.p, field, value)
+    assert f.fwd(lib) == code, _msg(lib)
+    assert f.bwd(lib) == code
+    n = ctypes.c_size_t(0)
+    assert lib.cas_prefix_attn_workspace_size(ctypes.byref(f.p), 0, ctypes.byref(n)) == code
+
+
+def test_segment_table_validation(lib):
+    f = Fake(B=2, rows=((16, 8), (4,)))
+    f.offs[1] = 3
+    f.offs[2] = 2                                   # decreasing offsets
+    assert f.fwd(lib) == _lib.CAS_ERR_INVALID_ARGUMENT
+    f = Fake()
+    f.offs[0] = 1
+    assert f.fwd(lib) == _lib.CAS_ERR_INVALID_ARGUMENT
+    f = Fake()
+    f.segs[0].len = -1
+    assert f.fwd(lib) == _lib.CAS_ERR_INVALID_ARGUMENT
+    f = Fake()
+    f.segs[1].k = None                              # len > 0 with NULL k
+    assert f.fwd(lib) == _lib.CAS_ERR_INVALID_ARGUMENT
+    f = Fake()
+    f.segs[1].stride_tok = 0
+    assert f.fwd(lib) == _lib.CAS_ERR_INVALID_ARGUMENT
+    f = Fake()
+    f.p.segments = None
+    assert f.fwd(lib) == _lib.CAS_ERR_INVALID_ARGUMENT
+    # A zero-length entry is skipped even with NULL pointers.
+    f = Fake(rows=((16, 0, 8),))
+    f.segs[1].k = f.segs[1].v = None
+    n = ctypes.c_size_t(0)
+    assert lib.cas_prefix_attn_workspace_size(ctypes.byref(f.p), 0, ctypes.byref(n)) == _lib.CAS_OK
+
+
+def test_alignment_validation(lib):
+    f = Fake()
+    f.segs[0].k = f.segs[0].k + 8
+    assert f.fwd(lib) == _lib.CAS_ERR_ALIGNMENT
+    f = Fake()
+    f.segs[0].stride_tok = f.Hkv * f.D + 4           # 8-byte token stride remainder in bf16
+    assert f.fwd(lib) == _lib.CAS_ERR_ALIGNMENT
+    f = Fake()
+    assert f.fwd(lib, q=f.q + 2) == _lib.CAS_ERR_ALIGNMENT
+    assert f.fwd(lib, lse=f.lse + 2) == _lib.CAS_ERR_ALIGNMENT
+    assert f.bwd(lib, dq=f.dq + 4) == _lib.CAS_ERR_ALIGNMENT
+
+
+def test_pointer_and_overlap_validation(lib):
+    f = Fake()
+    assert f.fwd(lib, q=None) == _lib.CAS_ERR_INVALID_ARGUMENT
+    assert f.bwd(lib, lse=None) == _lib.CAS_ERR_INVALID_ARGUMENT
+    # Output overlapping an input.
+    assert f.fwd(lib, o=f.q + 16) == _lib.CAS_ERR_INVALID_ARGUMENT
+    assert "overlaps" in _msg(lib)
+    assert f.bwd(lib, dq=f.segs[0].k) == _lib.CAS_ERR_INVALID_ARGUMENT
+    # Two outputs overlapping.
+    assert f.bwd(lib, dks=f.dq) == _lib.CAS_ERR_INVALID_ARGUMENT
+    # A cartridge gradient written into another cartridge's keys.
+    f = Fake(rows=((16, 8),))
+    f.segs[1].dk = f.segs[0].k
+    assert f.bwd(lib) == _lib.CAS_ERR_INVALID_ARGUMENT
+
+
+def test_alias_rules(lib):
+    f = Fake(B=2, rows=((16,), (16,)))
+    # Point row 1's entry at row 0's cartridge, including its gradients: allowed.
+    for a in ("k", "v", "dk", "dv"):
+        setattr(f.segs[1], a, getattr(f.segs[0], a))
+    info = _lib.PlanInfo()
+    assert lib.cas_plan_info(ctypes.byref(f.p), ctypes.byref(info)) == _lib.CAS_OK
+    assert info.unique_segments == 1
+    # Same k/v storage with a different gradient buffer: rejected.
+    f.segs[1].dk = f.alloc(16 * f.Hkv * f.D * 2)
+    assert f.bwd(lib) == _lib.CAS_ERR_INVALID_ARGUMENT
+    assert "share dk/dv" in _msg(lib)
+
+
+def test_gradient_layout_self_overlap(lib):
+    f = Fake(rows=((16,),))
+    f.segs[0].stride_head = 8                      # heads overlap within a token
+    assert f.bwd(lib) == _lib.CAS_ERR_INVALID_ARGUMENT
+    # Head-major storage is fine: [Hkv, len, D].
+    f = Fake(rows=((16,),))
+    f.segs[0].stride_tok, f.segs[0].stride_head = f.D, 16 * f.D
+    n = ctypes.c_size_t(0)
+    assert lib.cas_prefix_attn_workspace_size(ctypes.byref(f.p), 1, ctypes.byref(n)) == _lib.CAS_OK
+
+
+def test_workspace_validation(lib):
+    f = Fake()
+    n = ctypes.c_size_t(0)
+    assert lib.cas_prefix_attn_workspace_size(ctypes.byref(f.p), 1, ctypes.byref(n)) == _lib.CAS_OK
+    assert n.value > 0
+    assert f.bwd(lib, ws_bytes=n.value - 1) == _lib.CAS_ERR_WORKSPACE
+    assert f.bwd(lib, ws=None) == _lib.CAS_ERR_WORKSPACE
+
+
+def test_tuning_roundtrip(lib):
+    t = _lib.Tuning(3, 5)
+    assert lib.cas_set_tuning(ctypes.byref(t)) == _lib.CAS_OK
+    r = _lib.Tuning()
+    assert lib.cas_get_tuning(ctypes.byref(r)) == _lib.CAS_OK
+    assert (r.fwd_splits, r.dq_splits) == (3, 5)
+    f = Fake()
+    info = _lib.PlanInfo()
+    assert lib.cas_plan_info(ctypes.byref(f.p), ctypes.byref(info)) == _lib.CAS_OK
+    assert (info.fwd_splits, info.dq_splits) == (3, 5)
+    bad = _lib.Tuning(-1, 0)
+    assert lib.cas_set_tuning(ctypes.byref(bad)) == _lib.CAS_ERR_INVALID_ARGUMENT
+    z = _lib.Tuning(0, 0)
+    assert lib.cas_set_tuning(ctypes.byref(z)) == _lib.CAS_OK
+
+
+def test_plans_of_benchmark_shapes(lib):
+    """Occupancy planning on the benchmark shapes (256-CU target)."""
+    # 16 x 2048 cartridges, B=2, 32/8 heads, Sq=2048: 512 forward workgroups, no split.
+    f = Fake(B=2, Sq=2048, Hkv=8, g=4, D=128, rows=((2048,) * 16, (2048,) * 16))
+    info = _lib.PlanInfo()
+    assert lib.cas_plan_info(ctypes.byref(f.p), ctypes.byref(info)) == _lib.CAS_OK
+    assert info.fwd_splits == 1 and info.fwd_workgroups == 512
+    assert info.unique_segments == 32
+    assert info.total_key_tiles == 32 * 16 + 2 * 16
+    assert info.max_prefix_len == 32768
+    # B=1, Sq=512: only 64 base workgroups, so the key axis is split.
+    f = Fake(B=1, Sq=512, Hkv=8, g=4, D=128, rows=((1000,) * 64,))
+    assert lib.cas_plan_info(ctypes.byref(f.p), ctypes.byref(info)) == _lib.CAS_OK
+    assert info.fwd_splits == 8 and info.fwd_workgroups == 512
+    assert info.dq_splits == 4
+    assert info.ws_fwd_bytes >= 8 * 512 * 32 * 128 * 4
+
+
+def test_stage_validation_without_device(lib):
+    assert lib.cas_cartridge_stage(None, -1, None, None) == _lib.CAS_ERR_INVALID_ARGUMENT
+    assert lib.cas_cartridge_stage(None, 2, None, None) == _lib.CAS_ERR_INVALID_ARGUMENT
+    arr = (_lib.StageCopy * 1)()
+    arr[0].host_src, arr[0].dev_dst, arr[0].bytes = None, BASE, 64
+    assert lib.cas_cartridge_stage(arr, 1, None, None) == _lib.CAS_ERR_INVALID_ARGUMENT
+    # Zero copies is a no-op.
+    assert lib.cas_cartridge_stage(None, 0, None, None) == _lib.CAS_OK
