@@ -1,0 +1,208 @@
+#!/usr/bin/env python3
+"""Throughput of multi-cartridge prefix attention, forward + backward, on one
+MI355X.
+
+One step is one pass of the whole path over one batch: cas_prefix_attn_fwd
+(O, LSE) then cas_prefix_attn_bwd (dQ, self dK/dV and every cartridge's
+dK/dV), through the C ABI. Default workload: bf16, batch 2, 32 query / 8 KV
+heads of 128 channels, 16 cartridges of 2048 tokens per row (32K-token
+prefix) and 2048 causal query tokens, seeded synthetic inputs resident in HBM
+before timing.
+
+value = algorithmic TFLOP/s: 12 * head_dim * visible (query, key) pairs per
+step (forward 4d: QK^T and PV; backward 8d: dV, dP, dQ, dK) over the measured
+step time.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # 256 CUs x 2.4 GHz x 4096 dense bf16 FLOP/clk/CU
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+METRIC = "prefix-attn fwd+bwd TFLOP/s & MFMA util, 8B GQA shape, 16×2K cartridges"
+
+# FLOPs per visible (query, key) pair per query head, in units of head_dim,
+# that each kernel must execute for its own outputs.
+KERNEL_FLOPS_PER_PAIR = {"fwd": 4, "dkdv": 8, "dq": 6}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(wl, T, heads: int = 1):
+    """The fp64 oracle, as it stands, on a bounded sample of the same workload:
+    the full forward and backward of `heads` (batch row 0) query heads over
+    that row's whole key axis."""
+    import numpy as np
+    import casgen
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = sum(i.get("num_threads", 1) for i in threadpool_info()) or 1
+    except Exception:
+        cores = 1
+    f = lambda a: None if a is None else casgen.to_float(a, wl.dtype)
+    q, ks, vs, do = f(T["q"]), f(T["k_self"]), f(T["v_self"]), f(T["d_o"])
+    ck = [f(a) for a in T["cart_k"]]
+    cv = [f(a) for a in T["cart_v"]]
+    Sq = wl.q_len
+    t_all = np.arange(Sq)
+    elapsed = 0.0
+    pairs = 0
+    for h in range(heads):
+        kv = h // wl.group_size
+        K, V, npre = oracle.row_keys(ck, cv, wl.rows[0], ks[0], vs[0], kv)
+        qh = q[0, :, h, :].astype(np.float64)
+        doh = do[0, :, h, :].astype(np.float64)
+        t0 = time.perf_counter()
+        o, lse, _ = oracle.head_forward(qh, K, V, npre, Sq, t_all, float(wl.scale))
+        oracle.head_backward(qh, K, V, npre, Sq, t_all, float(wl.scale), doh, o, lse)
+        elapsed += time.perf_counter() - t0
+        pairs += Sq * npre + Sq * (Sq + 1) // 2
+    tflops = 12.0 * wl.head_dim * pairs / elapsed / 1e12
+    return {"value": tflops, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"batch row 0, {heads} of {wl.num_q_heads} query heads: full fp64 forward+backward "
+                      f"({Sq} queries x {npre + Sq} keys each), {elapsed:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=3, help="workload 1-4 (5 is forward-only)")
+    ap.add_argument("--cpu-heads", type=int, default=1, help="oracle heads timed for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic", default=None,
+                    help="JSON file with measured HBM bytes per launch of the dominant kernel")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no "
+              "multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import casgen
+    import paper_2606_04557_amd as cas
+
+    cas.load()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    wl = casgen.config(args.config)
+    if wl.forward_only:
+        print("bench.py times forward+backward; pick config 1-4", file=sys.stderr)
+        sys.exit(2)
+    log(f"generating {wl.name}: {wl.description}")
+    T = casgen.make_tensors(wl)
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+
+    def dev(a):
+        import numpy as np
+        if wl.dtype == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(a).cuda()
+
+    q, k_self, v_self, d_o = dev(T["q"]), dev(T["k_self"]), dev(T["v_self"]), dev(T["d_o"])
+    used = sorted({c for r in wl.rows for c in r})
+    K = {c: dev(T["cart_k"][c]) for c in used}
+    V = {c: dev(T["cart_v"][c]) for c in used}
+    dK = {c: torch.empty_like(K[c]) for c in used}
+    dV = {c: torch.empty_like(V[c]) for c in used}
+    rows = [[cas.Segment(K[c], V[c], dK[c], dV[c]) for c in r] for r in wl.rows]
+    Hkv, g, scale = wl.num_kv_heads, wl.group_size, float(wl.scale)
+    o = torch.empty_like(q)
+    lse = torch.empty((wl.batch, wl.num_q_heads, wl.q_len), dtype=torch.float32, device="cuda")
+    dq = torch.empty_like(q)
+    dks, dvs = torch.empty_like(k_self), torch.empty_like(v_self)
+    prob = cas.Problem.from_tensors(q, rows, Hkv, g, scale)
+    ws = torch.empty(max(cas.workspace_size(prob, False), cas.workspace_size(prob, True)),
+                     dtype=torch.uint8, device="cuda")
+    plan = cas.plan_info(prob)
+    log("plan", plan)
+
+    def step():
+        cas.prefix_attn_fwd(q, k_self, v_self, rows, Hkv, g, scale, o=o, lse=lse, workspace=ws)
+        cas.prefix_attn_bwd(q, k_self, v_self, rows, Hkv, g, scale, o, lse, d_o, dq=dq,
+                            dk_self=dks, dv_self=dvs, workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} done; timing {args.steps} steps")
+    cas.timing_reset()
+    cas.timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    cas.timing_enable(False)
+    ktimes = cas.timing_read()
+    ms = (t1 - t0) * 1e3 / args.steps
+    flops_step = wl.flops(12)
+    value = flops_step / (ms * 1e-3) / 1e12
+    log("kernel times", ktimes)
+
+    # Dominant kernel: the one with the largest total time in the timed region.
+    dom = max(ktimes, key=lambda k: ktimes[k][1])
+    launches, total = ktimes[dom]
+    avg_ms = total / launches
+    per_pair = KERNEL_FLOPS_PER_PAIR.get(dom)
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
+    achieved = wl.flops(per_pair) / (avg_ms * 1e-3) / 1e12 if per_pair else None
+    traffic = None
+    if args.traffic and os.path.exists(args.traffic):
+        with open(args.traffic) as fh:
+            traffic = json.load(fh).get(dom)
+    roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                "frac": (achieved / peak) if achieved else None, "traffic": traffic,
+                "avg_launch_ms": avg_ms,
+                "flops_per_launch": wl.flops(per_pair) if per_pair else None}
+    kernels = {k: {"launches": n, "avg_ms": t / n} for k, (n, t) in ktimes.items()}
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded Gaussian Q/K/V/dO; no model weights or datasets)",
+        "config": {"workload": f"{wl.name}: {wl.description}", "batch": wl.batch,
+                   "q_len": wl.q_len, "num_q_heads": wl.num_q_heads, "num_kv_heads": Hkv,
+                   "head_dim": wl.head_dim, "cartridges_per_row": len(wl.rows[0]),
+                   "prefix_tokens_per_row": wl.prefix_len(0), "parallelism": "single GPU"},
+        "mfma_frac_of_step": value / peak,
+        "tflops_fa14": wl.flops(14) / (ms * 1e-3) / 1e12,
+        "query_tokens_per_s": wl.batch * wl.q_len / (ms * 1e-3),
+        "kernels": kernels,
+        "roofline": roofline,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the fp64 oracle on a bounded sample")
+        out["cpu_baseline"] = cpu_baseline(wl, T, heads=args.cpu_heads)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -185,8 +185,9 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
   }
 
   const cas_tuning_t tu = tuning();
-  pl.nqblk_fwd = (int)ceil_div(pl.nrows, kRowsPerWg);
-  pl.nqblk_dq = (int)ceil_div(pl.nrows, kDqRowsPerWg);
+  const bool bf16 = pl.dt == kBF16;
+  pl.nqblk_fwd = (int)ceil_div(pl.nrows, bf16 ? kBf16RowsPerWg : kRowsPerWg);
+  pl.nqblk_dq = (int)ceil_div(pl.nrows, bf16 ? kBf16RowsPerWg : kDqRowsPerWg);
   const int64_t base_fwd = (int64_t)pl.B * Hkv * pl.nqblk_fwd;
   const int64_t base_dq = (int64_t)pl.B * Hkv * pl.nqblk_dq;
   pl.fwd_splits = tu.fwd_splits > 0 ? std::min(tu.fwd_splits, kMaxSplits) : auto_splits(base_fwd, min_row_tiles);

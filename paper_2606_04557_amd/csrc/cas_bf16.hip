@@ -1,0 +1,646 @@
+// bf16 fast path of multi-cartridge prefix attention for gfx950.
+//
+// All three kernels use 512-thread workgroups (8 waves, two per SIMD, so one
+// wave's softmax VALU work overlaps the other's MFMA work), swizzled row tiles
+// in LDS filled by asynchronous direct global->LDS copies, double buffering
+// (the copy of tile i+1 is in flight while tile i is computed; one barrier per
+// tile), and ds_read_b64_tr_b16 for every operand that is reduced along its
+// row axis (V in the forward, K in dQ, Q and dO in dK/dV).
+#include "cas_device.h"
+
+namespace cas {
+
+namespace {
+
+constexpr int kNW = 8;                 // waves per workgroup
+constexpr int kFastThreads = kNW * 64;
+constexpr int kKT = 64;                // keys per tile (forward, dQ)
+constexpr int kFastRowsPerWave = 32;
+constexpr int kFastRowsPerWg = kNW * kFastRowsPerWave;   // 256
+constexpr float kRescaleSlack = 8.0f;  // lazy softmax rescale threshold (log2 units)
+
+struct TileInfo {
+  const __bf16 *kp;
+  const __bf16 *vp;
+  int64_t st;
+  int nvalid;
+  int self0;   // first self key of the tile, or -1 for a cartridge tile
+};
+
+// Key tile `tile` of batch row b: prefix tiles walk the segment table (seg is
+// the walk position, advanced monotonically), then causal self tiles.
+__device__ __forceinline__ TileInfo key_tile(const DevSeg *segs, int &seg, int ptiles, int tile,
+                                             const __bf16 *k_self, const __bf16 *v_self, int b,
+                                             int Sq, int Hkv, int kvh, int D) {
+  TileInfo ti;
+  if (tile < ptiles) {
+    // seg is wave-uniform: readfirstlane keeps the descriptor loads scalar
+    // (s_load), off the vector-memory counter the tile copies use.
+    for (;;) {
+      const DevSeg sd = load_const(segs, __builtin_amdgcn_readfirstlane(seg));
+      if (tile < sd.tile_begin + (sd.len + kKT - 1) / kKT) break;
+      ++seg;
+    }
+    const DevSeg sd = load_const(segs, __builtin_amdgcn_readfirstlane(seg));
+    const int key0 = (tile - sd.tile_begin) * kKT;
+    const int64_t off = kvh * sd.stride_head + (int64_t)key0 * sd.stride_tok;
+    ti.kp = (const __bf16 *)sd.k + off;
+    ti.vp = (const __bf16 *)sd.v + off;
+    ti.st = sd.stride_tok;
+    ti.nvalid = min(kKT, sd.len - key0);
+    ti.self0 = -1;
+  } else {
+    const int s0 = (tile - ptiles) * kKT;
+    const int64_t off = (((int64_t)b * Sq + s0) * Hkv + kvh) * D;
+    ti.kp = k_self + off;
+    ti.vp = v_self + off;
+    ti.st = (int64_t)Hkv * D;
+    ti.nvalid = min(kKT, Sq - s0);
+    ti.self0 = s0;
+  }
+  return ti;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Forward.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(kFastThreads) void fwd_bf16_kernel(FwdParams p) {
+  constexpr int NSTEP = D / 16;
+  constexpr int DT = D / 32;
+  constexpr int TB = kKT * D * 2;
+  __shared__ __attribute__((aligned(1024))) char kb0[TB];
+  __shared__ __attribute__((aligned(1024))) char vb0[TB];
+  __shared__ __attribute__((aligned(1024))) char kb1[TB];
+  __shared__ __attribute__((aligned(1024))) char vb1[TB];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int G = lane >> 5, n = lane & 31;
+  int bid = blockIdx.x;
+  const int qblk = __builtin_amdgcn_readfirstlane(bid % p.nqblk);
+  bid /= p.nqblk;
+  const int kvh = __builtin_amdgcn_readfirstlane(bid % p.Hkv);
+  bid /= p.Hkv;
+  const int split = __builtin_amdgcn_readfirstlane(bid % p.splits);
+  const int b = __builtin_amdgcn_readfirstlane(bid / p.splits);
+
+  const int g = p.g, Sq = p.Sq, Hkv = p.Hkv, Hq = Hkv * g, nrows = p.nrows;
+  const int wg_row0 = qblk * kFastRowsPerWg;
+  const int wg_row1 = min(nrows, wg_row0 + kFastRowsPerWg);
+  const int row0 = wg_row0 + wave * kFastRowsPerWave;
+  const bool wave_active = row0 < nrows;
+  const int wave_t_lo = row0 / g;
+  const int wave_t_hi = (min(row0 + kFastRowsPerWave, nrows) - 1) / g;
+  const int wg_t_hi = (wg_row1 - 1) / g;
+  const int my_row = row0 + n;
+  const int my_t = my_row / g;
+  const float c = p.scale_log2;
+  RowOffsets<D> ro;
+  ro.init(n, G);
+  TrOffsets<D> to;
+  to.init(lane);
+
+  bf16x8 qf[NSTEP];
+  if (my_row < nrows) {
+    const __bf16 *rp = (const __bf16 *)p.q + (((int64_t)b * Sq + my_t) * Hq + kvh * g + (my_row - my_t * g)) * D;
+#pragma unroll
+    for (int st = 0; st < NSTEP; ++st) qf[st] = *reinterpret_cast<const bf16x8 *>(rp + st * 16 + G * 8);
+  } else {
+#pragma unroll
+    for (int st = 0; st < NSTEP; ++st) qf[st] = Mma<__bf16>::zero();
+  }
+
+  f32x16 oacc[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) oacc[dt] = zero16();
+  float m_run = -INFINITY, l_run = 0.0f;
+
+  const DevRow row = load_const(p.rows, b);
+  const int ptiles = row.prefix_tiles;
+  const int ntiles = ptiles + wg_t_hi / kKT + 1;
+  const int tb = (int)((int64_t)ntiles * split / p.splits);
+  const int te = (int)((int64_t)ntiles * (split + 1) / p.splits);
+  int seg = row.seg_begin;
+  const __bf16 *k_self = (const __bf16 *)p.k_self;
+  const __bf16 *v_self = (const __bf16 *)p.v_self;
+
+  auto issue = [&](const TileInfo &ti, char *kb, char *vb) {
+    dma_tile<D, kKT, kNW>(kb, [&](int r) { return ti.kp + r * ti.st; }, ti.nvalid, wave, lane);
+    dma_tile<D, kKT, kNW>(vb, [&](int r) { return ti.vp + r * ti.st; }, ti.nvalid, wave, lane);
+  };
+
+  auto compute = [&](const TileInfo &ti, const char *kb, const char *vb) {
+    if (!wave_active) return;
+    if (ti.self0 >= 0 && ti.self0 > wave_t_hi) return;
+    const bool need_mask = (ti.nvalid < kKT) || (ti.self0 >= 0 && ti.self0 + kKT - 1 > wave_t_lo);
+    f32x16 s0 = zero16(), s1 = zero16();
+#pragma unroll
+    for (int st = 0; st < NSTEP; ++st) {
+      const bf16x8 a0 = row_frag_at<D>(kb, ro, 0, st);
+      const bf16x8 a1 = row_frag_at<D>(kb, ro, 32, st);
+      s0 = Mma<__bf16>::run(a0, qf[st], s0);
+      s1 = Mma<__bf16>::run(a1, qf[st], s1);
+    }
+    if (need_mask) {
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int k0 = crow(j, G), k1 = 32 + crow(j, G);
+        const bool ok0 = k0 < ti.nvalid && (ti.self0 < 0 || ti.self0 + k0 <= my_t);
+        const bool ok1 = k1 < ti.nvalid && (ti.self0 < 0 || ti.self0 + k1 <= my_t);
+        s0[j] = ok0 ? s0[j] : -INFINITY;
+        s1[j] = ok1 ? s1[j] : -INFINITY;
+      }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) mx = fmaxf(mx, fmaxf(s0[j], s1[j]));
+    mx = fmaxf(mx, xor32(mx));
+    const float mt = mx * c;
+    // Rescale only when the running max grows by more than the slack; the
+    // unnormalised terms then stay below 2^slack, and O/l is unchanged.
+    if (wave_any(mt > m_run + kRescaleSlack)) {
+      const float m_new = fmaxf(m_run, mt);
+      const float alpha = (m_run == -INFINITY) ? 0.0f : fast_exp2(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+      m_run = m_new;
+    }
+    const float mu = (m_run == -INFINITY) ? 0.0f : m_run;
+    float ls = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      s0[j] = fast_exp2(fmaf(s0[j], c, -mu));
+      s1[j] = fast_exp2(fmaf(s1[j], c, -mu));
+      ls += s0[j] + s1[j];
+    }
+    l_run += ls;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const bf16x8 p0 = pack_bf16x8(s0, s), p1 = pack_bf16x8(s1, s);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        oacc[dt] = Mma<__bf16>::run(tr_frag_at<D>(vb, to, 16 * s, dt), p0, oacc[dt]);
+        oacc[dt] = Mma<__bf16>::run(tr_frag_at<D>(vb, to, 32 + 16 * s, dt), p1, oacc[dt]);
+      }
+    }
+  };
+
+  if (tb < te) {
+    TileInfo cur = key_tile(p.segs, seg, ptiles, tb, k_self, v_self, b, Sq, Hkv, kvh, D);
+    issue(cur, kb0, vb0);
+    __syncthreads();
+    for (int it = tb; it < te; it += 2) {
+      TileInfo nxt;
+      const bool has1 = it + 1 < te;
+      if (has1) {
+        nxt = key_tile(p.segs, seg, ptiles, it + 1, k_self, v_self, b, Sq, Hkv, kvh, D);
+        issue(nxt, kb1, vb1);
+      }
+      compute(cur, kb0, vb0);
+      __syncthreads();
+      if (!has1) break;
+      const bool has2 = it + 2 < te;
+      if (has2) {
+        cur = key_tile(p.segs, seg, ptiles, it + 2, k_self, v_self, b, Sq, Hkv, kvh, D);
+        issue(cur, kb0, vb0);
+      }
+      compute(nxt, kb1, vb1);
+      __syncthreads();
+    }
+  }
+
+  const float lt = l_run + xor32(l_run);
+  if (my_row >= nrows) return;
+  const int h = kvh * g + (my_row - my_t * g);
+  const float m_out = m_run;
+  if (p.splits == 1) {
+    const float inv = 1.0f / lt;
+    __bf16 *op = (__bf16 *)p.o + (((int64_t)b * Sq + my_t) * Hq + h) * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+        store4(op + dt * 32 + jj * 8 + G * 4, oacc[dt][jj * 4 + 0] * inv, oacc[dt][jj * 4 + 1] * inv,
+               oacc[dt][jj * 4 + 2] * inv, oacc[dt][jj * 4 + 3] * inv);
+    if (G == 0 && p.lse != nullptr) p.lse[((int64_t)b * Hq + h) * Sq + my_t] = (m_out + log2f(lt)) * kLn2;
+  } else {
+    const int64_t prow = (((int64_t)split * p.B + b) * Hkv + kvh) * nrows + my_row;
+    const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
+    float *op = p.part_o + prow * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+        store4(op + dt * 32 + jj * 8 + G * 4, oacc[dt][jj * 4 + 0] * inv, oacc[dt][jj * 4 + 1] * inv,
+               oacc[dt][jj * 4 + 2] * inv, oacc[dt][jj * 4 + 3] * inv);
+    if (G == 0) p.part_lse[prow] = lt > 0.0f ? (m_out + log2f(lt)) * kLn2 : -INFINITY;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dQ (query-stationary).
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
+  constexpr int NSTEP = D / 16;
+  constexpr int DT = D / 32;
+  constexpr int TB = kKT * D * 2;
+  __shared__ __attribute__((aligned(1024))) char kb0[TB];
+  __shared__ __attribute__((aligned(1024))) char vb0[TB];
+  __shared__ __attribute__((aligned(1024))) char kb1[TB];
+  __shared__ __attribute__((aligned(1024))) char vb1[TB];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int G = lane >> 5, n = lane & 31;
+  int bid = blockIdx.x;
+  const int qblk = __builtin_amdgcn_readfirstlane(bid % p.nqblk);
+  bid /= p.nqblk;
+  const int kvh = __builtin_amdgcn_readfirstlane(bid % p.Hkv);
+  bid /= p.Hkv;
+  const int split = __builtin_amdgcn_readfirstlane(bid % p.splits);
+  const int b = __builtin_amdgcn_readfirstlane(bid / p.splits);
+
+  const int g = p.g, Sq = p.Sq, Hkv = p.Hkv, Hq = Hkv * g, nrows = p.nrows;
+  const int wg_row0 = qblk * kFastRowsPerWg;
+  const int wg_row1 = min(nrows, wg_row0 + kFastRowsPerWg);
+  const int row0 = wg_row0 + wave * kFastRowsPerWave;
+  const bool wave_active = row0 < nrows;
+  const int wave_t_lo = row0 / g;
+  const int wave_t_hi = (min(row0 + kFastRowsPerWave, nrows) - 1) / g;
+  const int wg_t_hi = (wg_row1 - 1) / g;
+  const int my_row = row0 + n;
+  const int my_t = my_row / g;
+  const float c = p.scale_log2;
+  RowOffsets<D> ro;
+  ro.init(n, G);
+  TrOffsets<D> to;
+  to.init(lane);
+
+  bf16x8 qf[NSTEP], df[NSTEP];
+  float lse2r = INFINITY, dvr = 0.0f;
+  if (my_row < nrows) {
+    const int64_t off = (((int64_t)b * Sq + my_t) * Hq + kvh * g + (my_row - my_t * g)) * D;
+    const __bf16 *qp = (const __bf16 *)p.q + off;
+    const __bf16 *dp = (const __bf16 *)p.d_o + off;
+#pragma unroll
+    for (int st = 0; st < NSTEP; ++st) {
+      qf[st] = *reinterpret_cast<const bf16x8 *>(qp + st * 16 + G * 8);
+      df[st] = *reinterpret_cast<const bf16x8 *>(dp + st * 16 + G * 8);
+    }
+    const int64_t pk = ((int64_t)b * Hkv + kvh) * nrows + my_row;
+    lse2r = p.lse2[pk];
+    dvr = p.dvec[pk];
+  } else {
+#pragma unroll
+    for (int st = 0; st < NSTEP; ++st) {
+      qf[st] = Mma<__bf16>::zero();
+      df[st] = Mma<__bf16>::zero();
+    }
+  }
+  f32x16 acc[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) acc[dt] = zero16();
+
+  const DevRow row = load_const(p.rows, b);
+  const int ptiles = row.prefix_tiles;
+  const int ntiles = ptiles + wg_t_hi / kKT + 1;
+  const int tb = (int)((int64_t)ntiles * split / p.splits);
+  const int te = (int)((int64_t)ntiles * (split + 1) / p.splits);
+  int seg = row.seg_begin;
+  const __bf16 *k_self = (const __bf16 *)p.k_self;
+  const __bf16 *v_self = (const __bf16 *)p.v_self;
+
+  auto issue = [&](const TileInfo &ti, char *kb, char *vb) {
+    dma_tile<D, kKT, kNW>(kb, [&](int r) { return ti.kp + r * ti.st; }, ti.nvalid, wave, lane);
+    dma_tile<D, kKT, kNW>(vb, [&](int r) { return ti.vp + r * ti.st; }, ti.nvalid, wave, lane);
+  };
+
+  auto compute = [&](const TileInfo &ti, const char *kb, const char *vb) {
+    if (!wave_active) return;
+    if (ti.self0 >= 0 && ti.self0 > wave_t_hi) return;
+    const bool need_mask = (ti.nvalid < kKT) || (ti.self0 >= 0 && ti.self0 + kKT - 1 > wave_t_lo);
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      f32x16 sa = zero16(), dpa = zero16();
+#pragma unroll
+      for (int st = 0; st < NSTEP; ++st) {
+        sa = Mma<__bf16>::run(row_frag_at<D>(kb, ro, 32 * sub, st), qf[st], sa);
+        dpa = Mma<__bf16>::run(row_frag_at<D>(vb, ro, 32 * sub, st), df[st], dpa);
+      }
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        float pv = fast_exp2(fmaf(sa[j], c, -lse2r));
+        if (need_mask) {
+          const int key = 32 * sub + crow(j, G);
+          const bool ok = key < ti.nvalid && (ti.self0 < 0 || ti.self0 + key <= my_t);
+          pv = ok ? pv : 0.0f;
+        }
+        sa[j] = pv * (dpa[j] - dvr);
+      }
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const bf16x8 dsf = pack_bf16x8(sa, s);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          acc[dt] = Mma<__bf16>::run(tr_frag_at<D>(kb, to, 32 * sub + 16 * s, dt), dsf, acc[dt]);
+      }
+    }
+  };
+
+  if (tb < te) {
+    TileInfo cur = key_tile(p.segs, seg, ptiles, tb, k_self, v_self, b, Sq, Hkv, kvh, D);
+    issue(cur, kb0, vb0);
+    __syncthreads();
+    for (int it = tb; it < te; it += 2) {
+      TileInfo nxt;
+      const bool has1 = it + 1 < te;
+      if (has1) {
+        nxt = key_tile(p.segs, seg, ptiles, it + 1, k_self, v_self, b, Sq, Hkv, kvh, D);
+        issue(nxt, kb1, vb1);
+      }
+      compute(cur, kb0, vb0);
+      __syncthreads();
+      if (!has1) break;
+      const bool has2 = it + 2 < te;
+      if (has2) {
+        cur = key_tile(p.segs, seg, ptiles, it + 2, k_self, v_self, b, Sq, Hkv, kvh, D);
+        issue(cur, kb0, vb0);
+      }
+      compute(nxt, kb1, vb1);
+      __syncthreads();
+    }
+  }
+
+  if (my_row >= nrows) return;
+  const int h = kvh * g + (my_row - my_t * g);
+  if (p.splits == 1) {
+    const float sc = p.scale;
+    __bf16 *op = (__bf16 *)p.dq + (((int64_t)b * Sq + my_t) * Hq + h) * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+        store4(op + dt * 32 + jj * 8 + G * 4, acc[dt][jj * 4 + 0] * sc, acc[dt][jj * 4 + 1] * sc,
+               acc[dt][jj * 4 + 2] * sc, acc[dt][jj * 4 + 3] * sc);
+  } else {
+    const int64_t prow = (((int64_t)split * p.B + b) * Hkv + kvh) * nrows + my_row;
+    float *op = p.part_dq + prow * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+        store4(op + dt * 32 + jj * 8 + G * 4, acc[dt][jj * 4 + 0], acc[dt][jj * 4 + 1],
+               acc[dt][jj * 4 + 2], acc[dt][jj * 4 + 3]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dK / dV (key-stationary). 128 keys per workgroup, resident in LDS; wave w
+// owns keys 32*(w%4) .. +32 and query subtile w/4 of every 64-row block. The
+// two waves sharing keys add their sums through LDS at the end.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(kFastThreads) void dkdv_bf16_kernel(DkdvParams p) {
+  constexpr int NSTEP = D / 16;
+  constexpr int DT = D / 32;
+  constexpr int QB = 64;
+  constexpr int KTB = kDkdvKeyTile;            // 128
+  constexpr int KVB = KTB * D * 2;
+  constexpr int QBB = QB * D * 2;
+  __shared__ __attribute__((aligned(1024))) char ktile[KVB];
+  __shared__ __attribute__((aligned(1024))) char vtile[KVB];
+  __shared__ __attribute__((aligned(1024))) char qb0[QBB];
+  __shared__ __attribute__((aligned(1024))) char ob0[QBB];
+  __shared__ __attribute__((aligned(1024))) char qb1[QBB];
+  __shared__ __attribute__((aligned(1024))) char ob1[QBB];
+  __shared__ __attribute__((aligned(256))) float ls0[QB];
+  __shared__ __attribute__((aligned(256))) float dv0[QB];
+  __shared__ __attribute__((aligned(256))) float ls1[QB];
+  __shared__ __attribute__((aligned(256))) float dv1[QB];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int G = lane >> 5, n = lane & 31;
+  const int kq = wave & 3, qs = wave >> 2;     // key quarter, query subtile
+  const int tile = blockIdx.x, kvh = blockIdx.y;
+  const int g = p.g, Sq = p.Sq, Hkv = p.Hkv, Hq = Hkv * g, nrows = p.nrows;
+  const float c = p.scale_log2;
+
+  const __bf16 *kbase;
+  const __bf16 *vbase;
+  __bf16 *dkp;
+  __bf16 *dvp;
+  int64_t st;
+  int klen, key0, use_b = 0, use_e = 1;
+  const bool self = tile >= p.cart_tiles;
+  int self_b = 0;
+  if (!self) {
+    int lo = 0, hi = p.n_carts - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (load_const(p.carts, mid).tile_begin <= tile) lo = mid; else hi = mid - 1;
+    }
+    const DevCart cd = load_const(p.carts, lo);
+    key0 = (tile - cd.tile_begin) * KTB;
+    klen = cd.len;
+    kbase = (const __bf16 *)cd.k + kvh * cd.stride_head;
+    vbase = (const __bf16 *)cd.v + kvh * cd.stride_head;
+    dkp = cd.dk ? (__bf16 *)cd.dk + kvh * cd.stride_head : nullptr;
+    dvp = cd.dv ? (__bf16 *)cd.dv + kvh * cd.stride_head : nullptr;
+    st = cd.stride_tok;
+    use_b = cd.use_begin;
+    use_e = cd.use_end;
+  } else {
+    const int rel = tile - p.cart_tiles;
+    self_b = rel / p.self_tiles;
+    key0 = (rel % p.self_tiles) * KTB;
+    klen = Sq;
+    const int64_t base = ((int64_t)self_b * Sq * Hkv + kvh) * D;
+    kbase = (const __bf16 *)p.k_self + base;
+    vbase = (const __bf16 *)p.v_self + base;
+    dkp = p.dk_self ? (__bf16 *)p.dk_self + base : nullptr;
+    dvp = p.dv_self ? (__bf16 *)p.dv_self + base : nullptr;
+    st = (int64_t)Hkv * D;
+  }
+  const int nk = min(KTB, klen - key0);           // valid keys of this tile (>= 1)
+  const int wkey = kq * 32;                       // wave's first key within the tile
+  const int my_key = wkey + n;                    // lane's key within the tile
+  const bool key_ok = my_key < nk;
+  const bool wave_has_keys = wkey < nk;
+  const int abs_key = key0 + my_key;              // for the causal test on self keys
+  RowOffsets<D> ro;
+  ro.init(n, G);
+  TrOffsets<D> to;
+  to.init(lane);
+
+  // Stage this workgroup's K and V once.
+  dma_tile<D, KTB, kNW>(ktile, [&](int r) { return kbase + (int64_t)(key0 + r) * st; }, nk, wave, lane);
+  dma_tile<D, KTB, kNW>(vtile, [&](int r) { return vbase + (int64_t)(key0 + r) * st; }, nk, wave, lane);
+
+  f32x16 dk[DT], dv[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) {
+    dk[dt] = zero16();
+    dv[dt] = zero16();
+  }
+
+  const int nqb = (nrows + QB - 1) / QB;
+  const int qb_first = self ? (key0 * g) / QB : 0;
+  const int per_use = nqb - qb_first;
+  const int nblk = per_use * (use_e - use_b);
+
+  auto block_src = [&](int blk, int &b, int &qb) {
+    const int u = blk / per_use;
+    qb = qb_first + (blk - u * per_use);
+    b = self ? self_b : load_const(p.uses, __builtin_amdgcn_readfirstlane(use_b + u));
+  };
+  auto issue = [&](int blk, char *qb_l, char *ob_l, float *ls_l, float *dv_l) {
+    int b, qb;
+    block_src(blk, b, qb);
+    const int r0 = qb * QB;
+    const int nv = min(QB, nrows - r0);
+    const __bf16 *qbase = (const __bf16 *)p.q + ((int64_t)b * Sq * Hq + kvh * g) * D;
+    const __bf16 *obase = (const __bf16 *)p.d_o + ((int64_t)b * Sq * Hq + kvh * g) * D;
+    auto qrow = [&](int r) {
+      const int rr = r0 + r, t = rr / g;
+      return qbase + ((int64_t)t * Hq + (rr - t * g)) * D;
+    };
+    auto orow = [&](int r) {
+      const int rr = r0 + r, t = rr / g;
+      return obase + ((int64_t)t * Hq + (rr - t * g)) * D;
+    };
+    dma_tile<D, QB, kNW>(qb_l, qrow, nv, wave, lane);
+    dma_tile<D, QB, kNW>(ob_l, orow, nv, wave, lane);
+    if (wave == 0) {
+      // rows >= nrows read a clamped in-range row and are masked in compute
+      const int64_t base = ((int64_t)b * Hkv + kvh) * nrows + r0;
+      const int off = min(lane, nv - 1) - lane;
+      dma_f32x64(ls_l, p.lse2 + base + off, lane);
+      dma_f32x64(dv_l, p.dvec + base + off, lane);
+    }
+  };
+  auto compute = [&](int blk, const char *qb_l, const char *ob_l, const float *ls_l, const float *dv_l) {
+    if (!wave_has_keys) return;
+    int b, qb;
+    block_src(blk, b, qb);
+    (void)b;
+    const int r0 = qb * QB;
+    const int sub_r0 = r0 + 32 * qs;                 // first packed row of this wave's subtile
+    if (sub_r0 >= nrows) return;
+    const int t_hi = (min(sub_r0 + 32, nrows) - 1) / g;
+    if (self && key0 + wkey > t_hi) return;
+    const bool need_mask = (sub_r0 + 32 > nrows) || !key_ok || (self && key0 + wkey + 31 > sub_r0 / g);
+    f32x16 sa = zero16(), dpa = zero16();
+#pragma unroll
+    for (int s = 0; s < NSTEP; ++s) {
+      sa = Mma<__bf16>::run(row_frag_at<D>(qb_l, ro, 32 * qs, s), row_frag_at<D>(ktile, ro, wkey, s), sa);
+      dpa = Mma<__bf16>::run(row_frag_at<D>(ob_l, ro, 32 * qs, s), row_frag_at<D>(vtile, ro, wkey, s), dpa);
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int ql = 32 * qs + crow(j, G);           // query row within the block
+      float pv = fast_exp2(fmaf(sa[j], c, -ls_l[ql]));
+      if (need_mask) {
+        const int rr = r0 + ql;
+        bool ok = key_ok && rr < nrows;
+        if (self) ok = ok && abs_key <= rr / g;
+        pv = ok ? pv : 0.0f;
+      }
+      sa[j] = pv;
+      dpa[j] = pv * (dpa[j] - dv_l[ql]);
+    }
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const bf16x8 pf = pack_bf16x8(sa, s), dsf = pack_bf16x8(dpa, s);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        dv[dt] = Mma<__bf16>::run(tr_frag_at<D>(ob_l, to, 32 * qs + 16 * s, dt), pf, dv[dt]);
+        dk[dt] = Mma<__bf16>::run(tr_frag_at<D>(qb_l, to, 32 * qs + 16 * s, dt), dsf, dk[dt]);
+      }
+    }
+  };
+
+  if (nblk > 0) {
+    issue(0, qb0, ob0, ls0, dv0);
+    __syncthreads();
+    for (int blk = 0; blk < nblk; blk += 2) {
+      const bool has1 = blk + 1 < nblk;
+      if (has1) issue(blk + 1, qb1, ob1, ls1, dv1);
+      compute(blk, qb0, ob0, ls0, dv0);
+      __syncthreads();
+      if (!has1) break;
+      if (blk + 2 < nblk) issue(blk + 2, qb0, ob0, ls0, dv0);
+      compute(blk + 1, qb1, ob1, ls1, dv1);
+      __syncthreads();
+    }
+  } else {
+    __syncthreads();
+  }
+
+  // Pairwise reduction: waves 4..7 hand their sums to waves 0..3 through the
+  // K tile, which is no longer read: PD accumulators of 4 waves per pass.
+  constexpr int PD = KVB / (4 * 64 * 16 * 4);
+  static_assert(PD >= 1 && DT % PD == 0, "reduction pass size");
+  float *red = reinterpret_cast<float *>(ktile);
+#pragma unroll
+  for (int pass = 0; pass < 2 * (DT / PD); ++pass) {
+    f32x16 *acc = pass < DT / PD ? dk : dv;
+    const int d0 = (pass % (DT / PD)) * PD;
+    if (qs == 1) {
+#pragma unroll
+      for (int i = 0; i < PD; ++i)
+        *reinterpret_cast<f32x16 *>(red + ((kq * PD + i) * 64 + lane) * 16) = acc[d0 + i];
+    }
+    __syncthreads();
+    if (qs == 0) {
+#pragma unroll
+      for (int i = 0; i < PD; ++i)
+        acc[d0 + i] += *reinterpret_cast<const f32x16 *>(red + ((kq * PD + i) * 64 + lane) * 16);
+    }
+    __syncthreads();
+  }
+  if (qs != 0 || !key_ok) return;
+  const float sc = p.scale;
+  const int64_t krow = (int64_t)(key0 + my_key) * st;
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const int d0 = dt * 32 + jj * 8 + G * 4;
+      if (dkp)
+        store4(dkp + krow + d0, dk[dt][jj * 4 + 0] * sc, dk[dt][jj * 4 + 1] * sc, dk[dt][jj * 4 + 2] * sc,
+               dk[dt][jj * 4 + 3] * sc);
+      if (dvp)
+        store4(dvp + krow + d0, dv[dt][jj * 4 + 0], dv[dt][jj * 4 + 1], dv[dt][jj * 4 + 2], dv[dt][jj * 4 + 3]);
+    }
+}
+
+hipError_t launch_fwd_bf16(const FwdParams &p, int D, hipStream_t s) {
+  const int64_t grid = (int64_t)p.nqblk * p.Hkv * p.splits * p.B;
+  if (D == 64)
+    hipLaunchKernelGGL(fwd_bf16_kernel<64>, dim3((unsigned)grid), dim3(kFastThreads), 0, s, p);
+  else
+    hipLaunchKernelGGL(fwd_bf16_kernel<128>, dim3((unsigned)grid), dim3(kFastThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_dq_bf16(const DqParams &p, int D, hipStream_t s) {
+  const int64_t grid = (int64_t)p.nqblk * p.Hkv * p.splits * p.B;
+  if (D == 64)
+    hipLaunchKernelGGL(dq_bf16_kernel<64>, dim3((unsigned)grid), dim3(kFastThreads), 0, s, p);
+  else
+    hipLaunchKernelGGL(dq_bf16_kernel<128>, dim3((unsigned)grid), dim3(kFastThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_dkdv_bf16(const DkdvParams &p, int D, int gx, hipStream_t s) {
+  if (D == 64)
+    hipLaunchKernelGGL(dkdv_bf16_kernel<64>, dim3((unsigned)gx, (unsigned)p.Hkv), dim3(kFastThreads), 0, s, p);
+  else
+    hipLaunchKernelGGL(dkdv_bf16_kernel<128>, dim3((unsigned)gx, (unsigned)p.Hkv), dim3(kFastThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+}  // namespace cas

@@ -476,7 +476,7 @@ static hipError_t launch_dkdv_t(const DkdvParams &p, int gx, hipStream_t s) {
 }
 
 hipError_t launch_dkdv(const DkdvParams &p, DType dt, int D, int gx, hipStream_t s) {
-  if (dt == kBF16) return D == 64 ? launch_dkdv_t<__bf16, 64>(p, gx, s) : launch_dkdv_t<__bf16, 128>(p, gx, s);
+  if (dt == kBF16) return launch_dkdv_bf16(p, D, gx, s);
   return D == 64 ? launch_dkdv_t<float, 64>(p, gx, s) : launch_dkdv_t<float, 128>(p, gx, s);
 }
 
@@ -488,7 +488,7 @@ static hipError_t launch_dq_t(const DqParams &p, hipStream_t s) {
 }
 
 hipError_t launch_dq(const DqParams &p, DType dt, int D, hipStream_t s) {
-  if (dt == kBF16) return D == 64 ? launch_dq_t<__bf16, 64>(p, s) : launch_dq_t<__bf16, 128>(p, s);
+  if (dt == kBF16) return launch_dq_bf16(p, D, s);
   return D == 64 ? launch_dq_t<float, 64>(p, s) : launch_dq_t<float, 128>(p, s);
 }
 

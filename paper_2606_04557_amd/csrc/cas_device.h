@@ -223,3 +223,141 @@ __device__ __forceinline__ float to_f32(T x) {
 }
 
 }  // namespace cas
+
+namespace cas {
+
+// ---------------------------------------------------------------------------
+// Swizzled bf16 row tiles for the gfx950 fast path.
+//
+// A tile of R rows x D bf16 columns is stored with no padding; row r's
+// 16-byte chunk c sits at chunk position c ^ swz(r). For D = 128 the swizzle
+// swz(r) = 4*(r%4) + (r/4)%4 makes both access patterns conflict-free:
+//   * row fragments (lane m reads row m, one chunk): 16 consecutive rows hit
+//     16 different bank groups;
+//   * transposed fragments (ds_read_b64_tr_b16, 8 rows x 64 bytes): each
+//     group of 4 rows covers all 16 bank groups.
+// Tiles are filled with direct global->LDS copies (global_load_lds_dwordx4),
+// so a wave's 64 lanes write 1 KiB in lane order and the swizzle is applied
+// on the global side (lane at chunk position p of row r loads chunk p^swz(r)).
+// ---------------------------------------------------------------------------
+
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4_t;
+
+template <int D>
+__device__ __forceinline__ constexpr int swz(int r) {
+  if constexpr (D == 128) {
+    return ((r & 3) << 2) | ((r >> 2) & 3);
+  } else {
+    return (r >> 1) & 7;
+  }
+}
+
+template <int D>
+__device__ __forceinline__ int swz_off(int r, int c) {
+  return r * (D * 2) + ((c ^ swz<D>(r)) << 4);
+}
+
+// Asynchronous copy of R rows into a swizzled tile, shared by NW waves. Rows
+// at or beyond nvalid (>= 1) re-read row nvalid-1, which is finite; callers
+// mask those rows. Completion: s_waitcnt vmcnt(0) + barrier (__syncthreads).
+template <int D, int R, int NW, typename RowPtr>
+__device__ __forceinline__ void dma_tile(char *tile, RowPtr rowptr, int nvalid, int wave, int lane) {
+  constexpr int CPR = D / 8;
+  constexpr int NI = R * CPR / 64;   // 1 KiB wave instructions per tile
+  for (int inst = wave; inst < NI; inst += NW) {
+    const int pos = inst * 64 + lane;
+    const int r = pos / CPR;
+    const int c = (pos % CPR) ^ swz<D>(r);
+    const __bf16 *src = rowptr(r < nvalid ? r : nvalid - 1) + c * 8;
+    __builtin_amdgcn_global_load_lds((const void *)src, (lds_void_t *)(tile + inst * 1024), 16, 0, 0);
+  }
+}
+
+// Asynchronous copy of 64 consecutive floats (one wave instruction).
+__device__ __forceinline__ void dma_f32x64(float *dst, const float *src, int lane) {
+  __builtin_amdgcn_global_load_lds((const void *)(src + lane), (lds_void_t *)dst, 4, 0, 0);
+}
+
+// Per-lane byte offsets into swizzled tiles. swz(r) is unchanged when r moves
+// by a multiple of 16, so fragments of rows r + 16k are the same offsets plus
+// a constant: each lane keeps D/16 row-fragment and D/16 transposed-fragment
+// offsets and every tile/subtile/buffer is reached by an immediate offset.
+//
+// Row fragment: lane (G, m) reads row m, chunk 2*st + G (channels 16st+8G..).
+template <int D>
+struct RowOffsets {
+  int off[D / 16];
+  __device__ __forceinline__ void init(int m, int G) {
+#pragma unroll
+    for (int st = 0; st < D / 16; ++st) off[st] = m * (D * 2) + (((2 * st + G) ^ swz<D>(m)) << 4);
+  }
+};
+
+// Transposed A fragment of a 32x32x16 MFMA from a row tile: lane (G, m)
+// receives column dt*32 + m of rows row0 + 4G + {0..3} (slots 0..3) and
+// row0 + 8 + 4G + {0..3} (slots 4..7) -- the reduction indices that C
+// registers 8s..8s+7 of group G stand for when row0 = 32*sub + 16*s.
+// ds_read_b64_tr_b16: within each 16-lane block, output lane 4a+c receives
+// element c of the 8 bytes addressed by source lanes a, a+4, a+8, a+12; so
+// source lane 16b + j addresses row row0 + 8h + 4(b/2) + j/4 at columns
+// dt*32 + 16(b%2) + 4(j%4) .. +3.
+template <int D>
+struct TrOffsets {
+  int off[D / 32][2];
+  __device__ __forceinline__ void init(int lane) {
+    const int b = lane >> 4, j = lane & 15;
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int row = 8 * h + 4 * (b >> 1) + (j >> 2);
+        const int col = dt * 32 + 16 * (b & 1) + 4 * (j & 3);
+        off[dt][h] = row * (D * 2) + (((col >> 3) ^ swz<D>(row)) << 4) + ((col >> 2) & 1) * 8;
+      }
+  }
+};
+
+template <int D>
+__device__ __forceinline__ bf16x8 row_frag_at(const char *tile, const RowOffsets<D> &ro, int row0, int st) {
+  return *reinterpret_cast<const bf16x8 *>(tile + row0 * (D * 2) + ro.off[st]);
+}
+
+template <int D>
+__device__ __forceinline__ bf16x8 tr_frag_at(const char *tile, const TrOffsets<D> &to, int row0, int dt) {
+  const char *base = tile + row0 * (D * 2);
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t *)(base + to.off[dt][0]));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t *)(base + to.off[dt][1]));
+  typedef short i16x8 __attribute__((ext_vector_type(8)));
+  const i16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+__device__ __forceinline__ bf16x8 pack_bf16x8(const f32x16 &x, int s) {
+  bf16x8 r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = (__bf16)x[8 * s + e];
+  return r;
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ bool wave_any(bool p) { return __ballot(p) != 0; }
+
+// Launch tables (segment descriptors, use lists) are written before a kernel
+// starts and never during it; reading them through the constant address space
+// lets uniform reads become scalar loads.
+template <typename T>
+__device__ __forceinline__ T load_const(const T *base, int i) {
+  static_assert(sizeof(T) % 4 == 0, "4-byte words");
+  typedef const __attribute__((address_space(4))) uint32_t cword_t;
+  cword_t *w = (cword_t *)(base + i);
+  T r;
+  uint32_t *rw = reinterpret_cast<uint32_t *>(&r);
+#pragma unroll
+  for (int k = 0; k < (int)(sizeof(T) / 4); ++k) rw[k] = w[k];
+  return r;
+}
+
+}  // namespace cas

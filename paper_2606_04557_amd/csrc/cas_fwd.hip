@@ -282,7 +282,7 @@ static hipError_t launch_fwd_t(const FwdParams &p, hipStream_t s) {
 }
 
 hipError_t launch_fwd(const FwdParams &p, DType dt, int D, hipStream_t s) {
-  if (dt == kBF16) return D == 64 ? launch_fwd_t<__bf16, 64>(p, s) : launch_fwd_t<__bf16, 128>(p, s);
+  if (dt == kBF16) return launch_fwd_bf16(p, D, s);
   return D == 64 ? launch_fwd_t<float, 64>(p, s) : launch_fwd_t<float, 128>(p, s);
 }
 

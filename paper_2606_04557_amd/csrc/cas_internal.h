@@ -136,5 +136,10 @@ hipError_t launch_bwd_pre(const PreParams &p, DType dt, int D, hipStream_t s);
 hipError_t launch_dq(const DqParams &p, DType dt, int D, hipStream_t s);
 hipError_t launch_dq_reduce(const DqReduceParams &p, DType dt, int D, hipStream_t s);
 hipError_t launch_dkdv(const DkdvParams &p, DType dt, int D, int grid_x, hipStream_t s);
+// bf16 fast path (8-wave workgroups; forward and dQ take 256 packed rows per workgroup).
+constexpr int kBf16RowsPerWg = 256;
+hipError_t launch_fwd_bf16(const FwdParams &p, int D, hipStream_t s);
+hipError_t launch_dq_bf16(const DqParams &p, int D, hipStream_t s);
+hipError_t launch_dkdv_bf16(const DkdvParams &p, int D, int grid_x, hipStream_t s);
 
 }  // namespace cas
