@@ -189,7 +189,12 @@ def cartridge_stage(copies: Sequence[Tuple[object, object]], side_stream, done_e
         arr[i].host_src, arr[i].dev_dst, arr[i].bytes = h.data_ptr(), d.data_ptr(), nb
     ev = None
     if done_event is not None:
-        ev = done_event.cuda_event if hasattr(done_event, "cuda_event") else int(done_event)
+        if hasattr(done_event, "cuda_event"):
+            if not done_event.cuda_event:
+                done_event.record(side_stream)   # torch creates its event lazily
+            ev = done_event.cuda_event
+        else:
+            ev = int(done_event)
     _check(load().cas_cartridge_stage(ctypes.cast(arr, ctypes.POINTER(_lib.StageCopy)), len(copies),
                                       side_stream.cuda_stream, ev))
 

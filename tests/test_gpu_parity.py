@@ -177,3 +177,69 @@ def test_c2_full_size_sampled():
     targets = {3: [(0, [0, 511, 1023]), (13, [5, 1000]), (-1, [0, 1023]), (-4, [512])]}
     o, lse, grads = _sampled_check(case, key_targets=targets)
     _gradient_sums(case, grads)
+
+
+def test_c3_full_size_sampled():
+    """The headline 16 x 2048-cartridge configuration in the launch plan the bench times."""
+    case = GpuCase(casgen.config(3))
+    targets = {5: [(0, [0, 2047]), (17, [1000]), (-1, [0, 2047]), (-2, [1024])]}
+    o, lse, grads = _sampled_check(case, n_rows=32, key_targets=targets, seed=3)
+    _gradient_sums(case, grads)
+
+
+def test_c4_full_size_sampled():
+    """64 cartridges of U[256, 4096] tokens in separate allocations with padded and
+    head-major layouts; B = 1 forces key-axis splits in the forward and dQ."""
+    import paper_2606_04557_amd as cas
+    wl = casgen.config(4)
+    case = GpuCase(wl)
+    prob = cas.Problem.from_tensors(case.q, case.rows, wl.num_kv_heads, wl.group_size, float(wl.scale))
+    info = cas.plan_info(prob)
+    assert info["fwd_splits"] > 1 and info["dq_splits"] > 1
+    last = len(wl.cart_lens) - 1
+    targets = {2: [(0, [0, wl.cart_lens[0] - 1]), (37, [wl.cart_lens[37] // 2]),
+                   (last, [wl.cart_lens[last] - 1]), (-1, [0, 511])]}
+    o, lse, grads = _sampled_check(case, n_rows=32, key_targets=targets, seed=4)
+    _gradient_sums(case, grads)
+
+
+def test_c5_forward_with_staging():
+    """Retrieval-style inference mix: 64 requests each over 4 cartridges of a
+    256-cartridge pool; the pool's second half is staged host -> HBM with
+    cas_cartridge_stage on a side stream, and the forward waits on its events."""
+    import torch
+    import paper_2606_04557_amd as cas
+    wl = casgen.config(5)
+    used = sorted({c for r in wl.rows for c in r})
+    T = casgen.make_tensors(wl, carts=used)
+    case = GpuCase(wl, tensors=T, grads=False)
+    # Re-stage the second half from pinned host memory into the same device buffers.
+    for c in used:
+        if c >= 128:
+            case.k[c].fill_(float("nan"))
+            case.v[c].fill_(float("nan"))
+    side = torch.cuda.Stream()
+    events = []
+    staged = [c for c in used if c >= 128]
+    hosts = []
+    for i in range(0, len(staged), 16):
+        chunk = staged[i:i + 16]
+        copies = []
+        for c in chunk:
+            for src, dst in ((T["cart_k"][c], case.k[c]), (T["cart_v"][c], case.v[c])):
+                h = torch.from_numpy(src.view(np.int16)).view(torch.bfloat16).pin_memory()
+                hosts.append(h)
+                copies.append((h, dst))
+        ev = torch.cuda.Event()
+        torch.cuda.synchronize()
+        cas.cartridge_stage(copies, side, ev)
+        events.append(ev)
+    for ev in events:
+        torch.cuda.current_stream().wait_event(ev)
+    _sampled_check(case, n_rows=40, forward_only=True, seed=5)
+    # A pageable source is refused before anything is enqueued.
+    src = torch.zeros(1024, dtype=torch.bfloat16)
+    dst = torch.zeros(1024, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(cas.CasError) as ei:
+        cas.cartridge_stage([(src, dst)], side)
+    assert "CAS_ERR_NOT_PINNED" in str(ei.value)
