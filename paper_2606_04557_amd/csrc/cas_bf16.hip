@@ -6,6 +6,8 @@
 // (the copy of tile i+1 is in flight while tile i is computed; one barrier per
 // tile), and ds_read_b64_tr_b16 for every operand that is reduced along its
 // row axis (V in the forward, K in dQ, Q and dO in dK/dV).
+#include <type_traits>
+
 #include "cas_device.h"
 
 namespace cas {
@@ -22,10 +24,65 @@ constexpr float kRescaleSlack = 8.0f;  // lazy softmax rescale threshold (log2 u
 struct TileInfo {
   const __bf16 *kp;
   const __bf16 *vp;
-  int64_t st;
+  int st;      // token stride in elements (the host keeps 128 rows within 32-bit offsets)
   int nvalid;
   int self0;   // first self key of the tile, or -1 for a cartridge tile
 };
+
+// Scheduling groups: the next n MFMAs / LDS reads of the region, in order.
+template <int N>
+__device__ __forceinline__ void sched_mfma() { __builtin_amdgcn_sched_group_barrier(0x008, N, 0); }
+template <int N>
+__device__ __forceinline__ void sched_ds_read() { __builtin_amdgcn_sched_group_barrier(0x100, N, 0); }
+
+struct TileMask {
+  int nvalid;
+  int self0;
+};
+
+// Per-lane share of the direct-to-LDS copies of an R-row tile: the tile row
+// and element offset (swizzle applied) of each 16-byte chunk this lane moves
+// are fixed for the whole kernel, so a tile copy costs one multiply-add and
+// one copy instruction per chunk.
+template <int D, int R, int NW>
+struct CopyLanes {
+  static constexpr int CPR = D / 8;
+  static constexpr int NI = R * CPR / 64;             // 1 KiB wave instructions per tile
+  static constexpr int PER = (NI + NW - 1) / NW;      // instructions per wave
+  int row[PER];
+  int coff[PER];
+  __device__ __forceinline__ void init(int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int pos = (wave + i * NW) * 64 + lane;
+      const int r = pos / CPR;
+      row[i] = r;
+      coff[i] = ((pos % CPR) ^ swz<D>(r)) * 8;
+    }
+  }
+  // Rows at or beyond nvalid (>= 1) re-read row nvalid-1 (finite; masked
+  // later). The copies go through a buffer resource spanning exactly the
+  // tile's rows (an out-of-range offset would read zeros, not fault), and
+  // as MUBUF LDS loads they are counted on vmcnt alone.
+  __device__ __forceinline__ void issue(char *tile, const __bf16 *base, int st, int nvalid, int wave) const {
+    const BufRsrc rs = make_rsrc(base, ((nvalid - 1) * st + D) * 2);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int inst = wave + i * NW;
+      if (NI % NW == 0 || inst < NI) dma16(rs, (min(row[i], nvalid - 1) * st + coff[i]) * 2, tile + inst * 1024);
+    }
+  }
+};
+
+// Workgroup barrier that orders LDS use: this wave's LDS reads have returned,
+// and the compiler moves no memory access across it. Outstanding direct
+// global->LDS copies are not waited for (wait_vmcnt does that).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0); vmcnt, expcnt untouched
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 // Key tile `tile` of batch row b: prefix tiles walk the segment table (seg is
 // the walk position, advanced monotonically), then causal self tiles.
@@ -46,7 +103,7 @@ __device__ __forceinline__ TileInfo key_tile(const DevSeg *segs, int &seg, int p
     const int64_t off = kvh * sd.stride_head + (int64_t)key0 * sd.stride_tok;
     ti.kp = (const __bf16 *)sd.k + off;
     ti.vp = (const __bf16 *)sd.v + off;
-    ti.st = sd.stride_tok;
+    ti.st = (int)sd.stride_tok;
     ti.nvalid = min(kKT, sd.len - key0);
     ti.self0 = -1;
   } else {
@@ -54,7 +111,7 @@ __device__ __forceinline__ TileInfo key_tile(const DevSeg *segs, int &seg, int p
     const int64_t off = (((int64_t)b * Sq + s0) * Hkv + kvh) * D;
     ti.kp = k_self + off;
     ti.vp = v_self + off;
-    ti.st = (int64_t)Hkv * D;
+    ti.st = Hkv * D;
     ti.nvalid = min(kKT, Sq - s0);
     ti.self0 = s0;
   }
@@ -64,19 +121,32 @@ __device__ __forceinline__ TileInfo key_tile(const DevSeg *segs, int &seg, int p
 }  // namespace
 
 // ---------------------------------------------------------------------------
-// Forward.
+// Forward: ping-pong between the two waves of each SIMD.
+//
+// Waves 0-3 (group A) and 4-7 (group B) occupy one slot on each of the four
+// SIMDs. Per key tile i a wave runs a matrix phase G_i (O += V_{i-1}^T P_{i-1},
+// then S_i = K_i Q^T: 32 MFMAs) and a softmax phase X_i (mask, running max,
+// exp2, row sums, bf16 packing of P_i: VALU only). Group B runs one phase
+// behind group A and every phase ends in a workgroup barrier, so on each SIMD
+// one wave's MFMA stream always runs beside the other wave's softmax.
+//
+// LDS: two K and two V tile buffers. At the start of phase 2i every wave
+// issues its share of the copies of K_{i+1} and V_i (into the buffers K_{i-1}
+// and V_{i-2} left free after phase 2i-1); they are waited for at the end of
+// phase 2i+1, before group A's G_{i+1} reads them.
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(kFastThreads) void fwd_bf16_kernel(FwdParams p) {
+__global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void fwd_bf16_kernel(FwdParams p) {
   constexpr int NSTEP = D / 16;
   constexpr int DT = D / 32;
   constexpr int TB = kKT * D * 2;
   __shared__ __attribute__((aligned(1024))) char kb0[TB];
-  __shared__ __attribute__((aligned(1024))) char vb0[TB];
   __shared__ __attribute__((aligned(1024))) char kb1[TB];
+  __shared__ __attribute__((aligned(1024))) char vb0[TB];
   __shared__ __attribute__((aligned(1024))) char vb1[TB];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2;
   const int G = lane >> 5, n = lane & 31;
   int bid = blockIdx.x;
   const int qblk = __builtin_amdgcn_readfirstlane(bid % p.nqblk);
@@ -102,6 +172,16 @@ __global__ __launch_bounds__(kFastThreads) void fwd_bf16_kernel(FwdParams p) {
   TrOffsets<D> to;
   to.init(lane);
 
+  // Wave-uniform tile range of this split (readfirstlane keeps it, and every
+  // segment-table read that depends on it, in scalar registers).
+  const DevRow row = load_const(p.rows, b);
+  const int ptiles = __builtin_amdgcn_readfirstlane(row.prefix_tiles);
+  const int ntiles = ptiles + wg_t_hi / kKT + 1;
+  const int tb = __builtin_amdgcn_readfirstlane((int)((int64_t)ntiles * split / p.splits));
+  const int te = __builtin_amdgcn_readfirstlane((int)((int64_t)ntiles * (split + 1) / p.splits));
+  const int nt = te - tb;
+  int seg = __builtin_amdgcn_readfirstlane(row.seg_begin);
+
   bf16x8 qf[NSTEP];
   if (my_row < nrows) {
     const __bf16 *rp = (const __bf16 *)p.q + (((int64_t)b * Sq + my_t) * Hq + kvh * g + (my_row - my_t * g)) * D;
@@ -117,49 +197,96 @@ __global__ __launch_bounds__(kFastThreads) void fwd_bf16_kernel(FwdParams p) {
   for (int dt = 0; dt < DT; ++dt) oacc[dt] = zero16();
   float m_run = -INFINITY, l_run = 0.0f;
 
-  const DevRow row = load_const(p.rows, b);
-  const int ptiles = row.prefix_tiles;
-  const int ntiles = ptiles + wg_t_hi / kKT + 1;
-  const int tb = (int)((int64_t)ntiles * split / p.splits);
-  const int te = (int)((int64_t)ntiles * (split + 1) / p.splits);
-  int seg = row.seg_begin;
   const __bf16 *k_self = (const __bf16 *)p.k_self;
   const __bf16 *v_self = (const __bf16 *)p.v_self;
 
-  auto issue = [&](const TileInfo &ti, char *kb, char *vb) {
-    dma_tile<D, kKT, kNW>(kb, [&](int r) { return ti.kp + r * ti.st; }, ti.nvalid, wave, lane);
-    dma_tile<D, kKT, kNW>(vb, [&](int r) { return ti.vp + r * ti.st; }, ti.nvalid, wave, lane);
+  CopyLanes<D, kKT, kNW> cl;
+  cl.init(wave, lane);
+
+  // Scores of the tile between its G and X phases; P of the tile between its
+  // X phase and the next G phase.
+  f32x16 s0 = zero16(), s1 = zero16();
+  bf16x8 pf[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int s = 0; s < 2; ++s) pf[a][s] = Mma<__bf16>::zero();
+
+  // Whether this wave has any visible key in a tile (self tiles past the
+  // wave's last query position are skipped), and whether it needs the mask.
+  auto live = [&](const TileMask &tm) __attribute__((always_inline)) { return wave_active && !(tm.self0 >= 0 && tm.self0 > wave_t_hi); };
+  auto needs_mask = [&](const TileMask &tm) __attribute__((always_inline)) {
+    return (tm.nvalid < kKT) || (tm.self0 >= 0 && tm.self0 + kKT - 1 > wave_t_lo);
   };
 
-  auto compute = [&](const TileInfo &ti, const char *kb, const char *vb) {
-    if (!wave_active) return;
-    if (ti.self0 >= 0 && ti.self0 > wave_t_hi) return;
-    const bool need_mask = (ti.nvalid < kKT) || (ti.self0 >= 0 && ti.self0 + kKT - 1 > wave_t_lo);
-    f32x16 s0 = zero16(), s1 = zero16();
+  // The matrix phases read every LDS fragment into registers a few MFMAs
+  // ahead of its use (the scheduling groups pin that order), so the LDS
+  // latency hides behind the MFMA pipe instead of stalling it.
+  auto scores = [&](const char *kb) __attribute__((always_inline)) {
+    constexpr int LEAD = 4;
+    bf16x8 fr[2 * NSTEP];
 #pragma unroll
     for (int st = 0; st < NSTEP; ++st) {
-      const bf16x8 a0 = row_frag_at<D>(kb, ro, 0, st);
-      const bf16x8 a1 = row_frag_at<D>(kb, ro, 32, st);
-      s0 = Mma<__bf16>::run(a0, qf[st], s0);
-      s1 = Mma<__bf16>::run(a1, qf[st], s1);
+      fr[2 * st] = row_frag_at<D>(kb, ro, 0, st);
+      fr[2 * st + 1] = row_frag_at<D>(kb, ro, 32, st);
     }
-    if (need_mask) {
+    s0 = zero16();
+    s1 = zero16();
+#pragma unroll
+    for (int st = 0; st < NSTEP; ++st) {
+      s0 = Mma<__bf16>::run(fr[2 * st], qf[st], s0);
+      s1 = Mma<__bf16>::run(fr[2 * st + 1], qf[st], s1);
+    }
+    sched_ds_read<LEAD>();
+#pragma unroll
+    for (int k = 0; k < 2 * NSTEP - LEAD; ++k) {
+      sched_mfma<1>();
+      sched_ds_read<1>();
+    }
+    sched_mfma<LEAD>();
+  };
+  auto pv = [&](const char *vb) __attribute__((always_inline)) {
+    constexpr int LEAD = 4;
+    bf16x8 fr[4 * DT];
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        fr[(s * DT + dt) * 2] = tr_frag_at<D>(vb, to, 16 * s, dt);
+        fr[(s * DT + dt) * 2 + 1] = tr_frag_at<D>(vb, to, 32 + 16 * s, dt);
+      }
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        oacc[dt] = Mma<__bf16>::run(fr[(s * DT + dt) * 2], pf[0][s], oacc[dt]);
+        oacc[dt] = Mma<__bf16>::run(fr[(s * DT + dt) * 2 + 1], pf[1][s], oacc[dt]);
+      }
+    sched_ds_read<2 * LEAD>();
+#pragma unroll
+    for (int k = 0; k < 4 * DT - LEAD; ++k) {
+      sched_mfma<1>();
+      sched_ds_read<2>();
+    }
+    sched_mfma<LEAD>();
+  };
+  auto softmax = [&](auto MASK, const TileMask &tm) __attribute__((always_inline)) {
+    if constexpr (decltype(MASK)::value) {
+      const int lim = tm.self0 < 0 ? tm.nvalid - 1 : min(tm.nvalid - 1, my_t - tm.self0);
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const int k0 = crow(j, G), k1 = 32 + crow(j, G);
-        const bool ok0 = k0 < ti.nvalid && (ti.self0 < 0 || ti.self0 + k0 <= my_t);
-        const bool ok1 = k1 < ti.nvalid && (ti.self0 < 0 || ti.self0 + k1 <= my_t);
-        s0[j] = ok0 ? s0[j] : -INFINITY;
-        s1[j] = ok1 ? s1[j] : -INFINITY;
+        // Last visible key of this lane's query: lim (keys beyond it masked).
+        s0[j] = k0 <= lim ? s0[j] : -INFINITY;
+        s1[j] = k1 <= lim ? s1[j] : -INFINITY;
       }
     }
     float mx = -INFINITY;
 #pragma unroll
     for (int j = 0; j < 16; ++j) mx = fmaxf(mx, fmaxf(s0[j], s1[j]));
-    mx = fmaxf(mx, xor32(mx));
-    const float mt = mx * c;
-    // Rescale only when the running max grows by more than the slack; the
-    // unnormalised terms then stay below 2^slack, and O/l is unchanged.
+    const float mt = fmaxf(mx, xor32(mx)) * c;
+    // Lazy rescale: only when the running max grows by more than the slack
+    // (the unnormalised terms then stay below 2^slack; O/l is unchanged).
     if (wave_any(mt > m_run + kRescaleSlack)) {
       const float m_new = fmaxf(m_run, mt);
       const float alpha = (m_run == -INFINITY) ? 0.0f : fast_exp2(m_run - m_new);
@@ -179,37 +306,81 @@ __global__ __launch_bounds__(kFastThreads) void fwd_bf16_kernel(FwdParams p) {
     l_run += ls;
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
-      const bf16x8 p0 = pack_bf16x8(s0, s), p1 = pack_bf16x8(s1, s);
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        oacc[dt] = Mma<__bf16>::run(tr_frag_at<D>(vb, to, 16 * s, dt), p0, oacc[dt]);
-        oacc[dt] = Mma<__bf16>::run(tr_frag_at<D>(vb, to, 32 + 16 * s, dt), p1, oacc[dt]);
-      }
+      pf[0][s] = pack_bf16x8(s0, s);
+      pf[1][s] = pack_bf16x8(s1, s);
     }
   };
 
-  if (tb < te) {
-    TileInfo cur = key_tile(p.segs, seg, ptiles, tb, k_self, v_self, b, Sq, Hkv, kvh, D);
-    issue(cur, kb0, vb0);
-    __syncthreads();
-    for (int it = tb; it < te; it += 2) {
-      TileInfo nxt;
-      const bool has1 = it + 1 < te;
-      if (has1) {
-        nxt = key_tile(p.segs, seg, ptiles, it + 1, k_self, v_self, b, Sq, Hkv, kvh, D);
-        issue(nxt, kb1, vb1);
-      }
-      compute(cur, kb0, vb0);
-      __syncthreads();
-      if (!has1) break;
-      const bool has2 = it + 2 < te;
-      if (has2) {
-        cur = key_tile(p.segs, seg, ptiles, it + 2, k_self, v_self, b, Sq, Hkv, kvh, D);
-        issue(cur, kb0, vb0);
-      }
-      compute(nxt, kb1, vb1);
-      __syncthreads();
+  // Tile bookkeeping (wave-uniform): the copy source of the last K tile
+  // issued, and the mask data of tiles with even / odd local index.
+  TileInfo tk;
+  int nv0 = kKT, sf0 = -1, nv1 = kKT, sf1 = -1;
+  auto tmask = [&](int j) __attribute__((always_inline)) {
+    return (j & 1) ? TileMask{nv1, sf1} : TileMask{nv0, sf0};
+  };
+
+  // Matrix phase G_j of this wave: O += V_{j-1}^T P_{j-1}, then S_j.
+  // (The scheduling barrier keeps the two halves' LDS fragments from being
+  // in flight together, which would not fit the register budget.)
+  auto gphase = [&](int j, const char *kb, const char *vbp) __attribute__((always_inline)) {
+    if (j >= 1 && j - 1 < nt && live(tmask(j - 1))) pv(vbp);
+    __builtin_amdgcn_sched_barrier(0);
+    if (j < nt && live(tmask(j))) scores(kb);
+  };
+  auto xphase = [&](int j) __attribute__((always_inline)) {
+    if (j < 0 || j >= nt) return;
+    const TileMask tm = tmask(j);
+    if (!live(tm)) return;
+    if (needs_mask(tm)) softmax(std::true_type{}, tm);
+    else softmax(std::false_type{}, tm);
+  };
+  // Copies issued at the start of phase 2i: K_{i+1} and V_i.
+  auto issue = [&](int i, char *kbn, char *vbi) __attribute__((always_inline)) {
+    if (i >= nt) return;
+    const TileInfo tv = tk;
+    if (i & 1) {
+      nv1 = tv.nvalid;
+      sf1 = tv.self0;
+    } else {
+      nv0 = tv.nvalid;
+      sf0 = tv.self0;
     }
+    if (i + 1 < nt) {
+      tk = key_tile(p.segs, seg, ptiles, tb + i + 1, k_self, v_self, b, Sq, Hkv, kvh, D);
+      cl.issue(kbn, tk.kp, tk.st, tk.nvalid, wave);
+    }
+    cl.issue(vbi, tv.vp, tv.st, tv.nvalid, wave);
+  };
+
+  if (nt > 0) {
+    tk = key_tile(p.segs, seg, ptiles, tb, k_self, v_self, b, Sq, Hkv, kvh, D);
+    cl.issue(kb0, tk.kp, tk.st, tk.nvalid, wave);
+    wait_vmcnt<0>();
+    lds_barrier();
+    // Four phases per iteration (two tiles), so every buffer is a fixed LDS
+    // address: phases 2i, 2i+1 use K_i in kb0 and V_{i-1} in vb1; phases
+    // 2i+2, 2i+3 use K_{i+1} in kb1 and V_i in vb0. Each group runs its own
+    // copy of the loop (straight-line phases); s_barrier pairs them up.
+    auto run = [&](auto GROUP_A) __attribute__((always_inline)) {
+      constexpr bool A = decltype(GROUP_A)::value;
+      for (int i = 0; i <= nt; i += 2) {
+        issue(i, kb1, vb0);
+        if constexpr (A) gphase(i, kb0, vb1); else xphase(i - 1);
+        lds_barrier();
+        if constexpr (A) xphase(i); else gphase(i, kb0, vb1);
+        wait_vmcnt<0>();
+        lds_barrier();
+        if (i + 1 > nt) break;
+        issue(i + 1, kb0, vb1);
+        if constexpr (A) gphase(i + 1, kb1, vb0); else xphase(i);
+        lds_barrier();
+        if constexpr (A) xphase(i + 1); else gphase(i + 1, kb1, vb0);
+        wait_vmcnt<0>();
+        lds_barrier();
+      }
+    };
+    if (grp == 0) run(std::true_type{});
+    else run(std::false_type{});
   }
 
   const float lt = l_run + xor32(l_run);
@@ -313,12 +484,12 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
   const __bf16 *k_self = (const __bf16 *)p.k_self;
   const __bf16 *v_self = (const __bf16 *)p.v_self;
 
-  auto issue = [&](const TileInfo &ti, char *kb, char *vb) {
-    dma_tile<D, kKT, kNW>(kb, [&](int r) { return ti.kp + r * ti.st; }, ti.nvalid, wave, lane);
-    dma_tile<D, kKT, kNW>(vb, [&](int r) { return ti.vp + r * ti.st; }, ti.nvalid, wave, lane);
+  auto issue = [&](const TileInfo &ti, char *kb, char *vb) __attribute__((always_inline)) {
+    dma_tile<D, kKT, kNW>(kb, ti.kp, [&](int r) { return r * ti.st; }, ti.nvalid, wave, lane);
+    dma_tile<D, kKT, kNW>(vb, ti.vp, [&](int r) { return r * ti.st; }, ti.nvalid, wave, lane);
   };
 
-  auto compute = [&](const TileInfo &ti, const char *kb, const char *vb) {
+  auto compute = [&](const TileInfo &ti, const char *kb, const char *vb) __attribute__((always_inline)) {
     if (!wave_active) return;
     if (ti.self0 >= 0 && ti.self0 > wave_t_hi) return;
     const bool need_mask = (ti.nvalid < kKT) || (ti.self0 >= 0 && ti.self0 + kKT - 1 > wave_t_lo);
@@ -476,8 +647,11 @@ __global__ __launch_bounds__(kFastThreads) void dkdv_bf16_kernel(DkdvParams p) {
   to.init(lane);
 
   // Stage this workgroup's K and V once.
-  dma_tile<D, KTB, kNW>(ktile, [&](int r) { return kbase + (int64_t)(key0 + r) * st; }, nk, wave, lane);
-  dma_tile<D, KTB, kNW>(vtile, [&](int r) { return vbase + (int64_t)(key0 + r) * st; }, nk, wave, lane);
+  {
+    const int sti = (int)st;
+    dma_tile<D, KTB, kNW>(ktile, kbase + (int64_t)key0 * st, [&](int r) { return r * sti; }, nk, wave, lane);
+    dma_tile<D, KTB, kNW>(vtile, vbase + (int64_t)key0 * st, [&](int r) { return r * sti; }, nk, wave, lane);
+  }
 
   f32x16 dk[DT], dv[DT];
 #pragma unroll
@@ -491,37 +665,34 @@ __global__ __launch_bounds__(kFastThreads) void dkdv_bf16_kernel(DkdvParams p) {
   const int per_use = nqb - qb_first;
   const int nblk = per_use * (use_e - use_b);
 
-  auto block_src = [&](int blk, int &b, int &qb) {
+  auto block_src = [&](int blk, int &b, int &qb) __attribute__((always_inline)) {
     const int u = blk / per_use;
     qb = qb_first + (blk - u * per_use);
     b = self ? self_b : load_const(p.uses, __builtin_amdgcn_readfirstlane(use_b + u));
   };
-  auto issue = [&](int blk, char *qb_l, char *ob_l, float *ls_l, float *dv_l) {
+  auto issue = [&](int blk, char *qb_l, char *ob_l, float *ls_l, float *dv_l) __attribute__((always_inline)) {
     int b, qb;
     block_src(blk, b, qb);
     const int r0 = qb * QB;
     const int nv = min(QB, nrows - r0);
-    const __bf16 *qbase = (const __bf16 *)p.q + ((int64_t)b * Sq * Hq + kvh * g) * D;
-    const __bf16 *obase = (const __bf16 *)p.d_o + ((int64_t)b * Sq * Hq + kvh * g) * D;
-    auto qrow = [&](int r) {
+    // Packed row r0 + r is query position t = (r0+r)/g, head (r0+r)%g of the
+    // group; offsets are taken from the block's first position.
+    const int t0 = r0 / g;
+    const int64_t head0 = (((int64_t)b * Sq + t0) * Hq + kvh * g) * D;
+    auto rowoff = [&](int r) __attribute__((always_inline)) {
       const int rr = r0 + r, t = rr / g;
-      return qbase + ((int64_t)t * Hq + (rr - t * g)) * D;
+      return ((t - t0) * Hq + (rr - t * g)) * D;
     };
-    auto orow = [&](int r) {
-      const int rr = r0 + r, t = rr / g;
-      return obase + ((int64_t)t * Hq + (rr - t * g)) * D;
-    };
-    dma_tile<D, QB, kNW>(qb_l, qrow, nv, wave, lane);
-    dma_tile<D, QB, kNW>(ob_l, orow, nv, wave, lane);
+    dma_tile<D, QB, kNW>(qb_l, (const __bf16 *)p.q + head0, rowoff, nv, wave, lane);
+    dma_tile<D, QB, kNW>(ob_l, (const __bf16 *)p.d_o + head0, rowoff, nv, wave, lane);
     if (wave == 0) {
       // rows >= nrows read a clamped in-range row and are masked in compute
       const int64_t base = ((int64_t)b * Hkv + kvh) * nrows + r0;
-      const int off = min(lane, nv - 1) - lane;
-      dma_f32x64(ls_l, p.lse2 + base + off, lane);
-      dma_f32x64(dv_l, p.dvec + base + off, lane);
+      dma_f32x64(ls_l, p.lse2 + base, nv, lane);
+      dma_f32x64(dv_l, p.dvec + base, nv, lane);
     }
   };
-  auto compute = [&](int blk, const char *qb_l, const char *ob_l, const float *ls_l, const float *dv_l) {
+  auto compute = [&](int blk, const char *qb_l, const char *ob_l, const float *ls_l, const float *dv_l) __attribute__((always_inline)) {
     if (!wave_has_keys) return;
     int b, qb;
     block_src(blk, b, qb);

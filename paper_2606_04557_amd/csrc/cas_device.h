@@ -236,7 +236,7 @@ namespace cas {
 //     16 different bank groups;
 //   * transposed fragments (ds_read_b64_tr_b16, 8 rows x 64 bytes): each
 //     group of 4 rows covers all 16 bank groups.
-// Tiles are filled with direct global->LDS copies (global_load_lds_dwordx4),
+// Tiles are filled with direct buffer->LDS copies (buffer_load_dwordx4 ... lds),
 // so a wave's 64 lanes write 1 KiB in lane order and the swizzle is applied
 // on the global side (lane at chunk position p of row r loads chunk p^swz(r)).
 // ---------------------------------------------------------------------------
@@ -259,25 +259,44 @@ __device__ __forceinline__ int swz_off(int r, int c) {
   return r * (D * 2) + ((c ^ swz<D>(r)) << 4);
 }
 
-// Asynchronous copy of R rows into a swizzled tile, shared by NW waves. Rows
-// at or beyond nvalid (>= 1) re-read row nvalid-1, which is finite; callers
-// mask those rows. Completion: s_waitcnt vmcnt(0) + barrier (__syncthreads).
-template <int D, int R, int NW, typename RowPtr>
-__device__ __forceinline__ void dma_tile(char *tile, RowPtr rowptr, int nvalid, int wave, int lane) {
+// Buffer resource over `bytes` bytes from base (raw addressing, no stride);
+// loads at offsets beyond it return zero. Direct buffer->LDS copies of 16
+// bytes per lane: a wave writes 1 KiB in lane order at lds. Unlike the FLAT
+// form, a MUBUF LDS load is tracked on vmcnt alone, so LDS reads issued while
+// copies are in flight keep exact lgkmcnt waits.
+typedef __amdgpu_buffer_rsrc_t BufRsrc;
+
+__device__ __forceinline__ BufRsrc make_rsrc(const void *base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, bytes, 0x00020000);
+}
+
+__device__ __forceinline__ void dma16(BufRsrc rs, int byte_off, char *lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t *)lds, 16, byte_off, 0, 0, 0);
+}
+
+// Asynchronous copy of R rows into a swizzled tile, shared by NW waves: row r
+// starts rowoff(r) elements after base (rowoff increases with r and stays in
+// 32 bits). Rows at or beyond nvalid (>= 1) re-read row nvalid-1, which is
+// finite; callers mask those rows. Completion: s_waitcnt vmcnt + barrier.
+template <int D, int R, int NW, typename RowOff>
+__device__ __forceinline__ void dma_tile(char *tile, const __bf16 *base, RowOff rowoff, int nvalid, int wave,
+                                         int lane) {
   constexpr int CPR = D / 8;
   constexpr int NI = R * CPR / 64;   // 1 KiB wave instructions per tile
+  const BufRsrc rs = make_rsrc(base, (rowoff(nvalid - 1) + D) * 2);
   for (int inst = wave; inst < NI; inst += NW) {
     const int pos = inst * 64 + lane;
     const int r = pos / CPR;
     const int c = (pos % CPR) ^ swz<D>(r);
-    const __bf16 *src = rowptr(r < nvalid ? r : nvalid - 1) + c * 8;
-    __builtin_amdgcn_global_load_lds((const void *)src, (lds_void_t *)(tile + inst * 1024), 16, 0, 0);
+    dma16(rs, (rowoff(r < nvalid ? r : nvalid - 1) + c * 8) * 2, tile + inst * 1024);
   }
 }
 
-// Asynchronous copy of 64 consecutive floats (one wave instruction).
-__device__ __forceinline__ void dma_f32x64(float *dst, const float *src, int lane) {
-  __builtin_amdgcn_global_load_lds((const void *)(src + lane), (lds_void_t *)dst, 4, 0, 0);
+// Asynchronous copy of 64 consecutive floats (one wave instruction); lanes at
+// or beyond n (>= 1) re-read element n-1.
+__device__ __forceinline__ void dma_f32x64(float *dst, const float *src, int n, int lane) {
+  const BufRsrc rs = make_rsrc(src, n * 4);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t *)dst, 4, min(lane, n - 1) * 4, 0, 0, 0);
 }
 
 // Per-lane byte offsets into swizzled tiles. swz(r) is unchanged when r moves
@@ -344,6 +363,16 @@ __device__ __forceinline__ bf16x8 pack_bf16x8(const f32x16 &x, int s) {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ __forceinline__ bool wave_any(bool p) { return __ballot(p) != 0; }
+
+// s_waitcnt for "at most n vector-memory operations of this wave outstanding",
+// leaving the export and LDS/scalar counters alone (gfx9 encoding: vmcnt in
+// bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8). Direct global->LDS copies
+// complete in issue order, so this waits for all but the newest n copies.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
 
 // Launch tables (segment descriptors, use lists) are written before a kernel
 // starts and never during it; reading them through the constant address space
