@@ -85,6 +85,7 @@ struct Plan {
   float scale;
   std::vector<DevSeg> segs;
   std::vector<DevRow> rows;
+  std::vector<DevTile> tiles;
   std::vector<DevCart> carts;
   std::vector<int32_t> uses;
   int64_t max_prefix = 0;
@@ -93,8 +94,8 @@ struct Plan {
   int cart_tiles = 0, self_tiles = 0;
   bool want_self_grad = false;
   // workspace layout
-  size_t off_segs = 0, off_rows = 0, off_carts = 0, off_uses = 0, table_bytes = 0;
-  size_t off_part_o = 0, off_part_lse = 0, ws_fwd = 0;
+  size_t off_segs = 0, off_rows = 0, off_tiles = 0, off_carts = 0, off_uses = 0, table_bytes = 0;
+  size_t off_part_o = 0, off_part_lse = 0, off_ovf = 0, off_row_max = 0, ws_fwd = 0;
   size_t off_dvec = 0, off_lse2 = 0, off_part_dq = 0, ws_bwd = 0;
 };
 
@@ -123,6 +124,8 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
   const int64_t nrows = (int64_t)p->group_size * p->q_len;
   if (Hq > (1 << 16) || nrows > (1 << 28))
     return fail(CAS_ERR_UNSUPPORTED, "num_kv_heads*group_size or group_size*q_len too large");
+  if ((int64_t)p->num_kv_heads * p->head_dim > (1 << 22))
+    return fail(CAS_ERR_UNSUPPORTED, "num_kv_heads*head_dim above 2^22 (self-token stride)");
   if ((int64_t)p->batch * p->q_len * Hq * p->head_dim > (int64_t)1 << 40)
     return fail(CAS_ERR_UNSUPPORTED, "query tensor too large");
   if (!p->seg_offsets) return fail(CAS_ERR_INVALID_ARGUMENT, "seg_offsets is NULL");
@@ -151,6 +154,7 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
   for (int b = 0; b < pl.B; ++b) {
     DevRow r{};
     r.seg_begin = (int32_t)pl.segs.size();
+    r.tile_begin = (int32_t)pl.tiles.size();
     int64_t tiles = 0, plen = 0;
     for (int i = p->seg_offsets[b]; i < p->seg_offsets[b + 1]; ++i) {
       const cas_segment_t &s = p->segments[i];
@@ -164,6 +168,9 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
         return fail(CAS_ERR_ALIGNMENT, "segment " + std::to_string(i) +
                                            ": pointers and strides must be multiples of 16 bytes");
       if (s.len > (1 << 30)) return fail(CAS_ERR_UNSUPPORTED, "segment longer than 2^30 tokens");
+      // Tile copies address up to 128 tokens with 32-bit byte offsets.
+      if (s.stride_tok > (1 << 22))
+        return fail(CAS_ERR_UNSUPPORTED, "segment " + std::to_string(i) + ": token stride above 2^22 elements");
       DevSeg d{};
       d.k = s.k;
       d.v = s.v;
@@ -171,6 +178,15 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
       d.stride_head = s.stride_head;
       d.len = (int32_t)s.len;
       d.tile_begin = (int32_t)tiles;
+      for (int64_t key0 = 0; key0 < s.len; key0 += kKeyTile) {
+        DevTile t{};
+        t.k = (const char *)s.k + key0 * s.stride_tok * es;
+        t.v = (const char *)s.v + key0 * s.stride_tok * es;
+        t.stride_head = s.stride_head;
+        t.stride_tok = (int32_t)s.stride_tok;
+        t.nvalid = (int32_t)std::min<int64_t>(kKeyTile, s.len - key0);
+        pl.tiles.push_back(t);
+      }
       tiles += ceil_div(s.len, kKeyTile);
       plen += s.len;
       pl.segs.push_back(d);
@@ -179,6 +195,18 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
       return fail(CAS_ERR_UNSUPPORTED, "row " + std::to_string(b) + ": prefix longer than 2^30 tokens");
     r.seg_end = (int32_t)pl.segs.size();
     r.prefix_tiles = (int32_t)tiles;
+    // The row's causal self tiles follow its prefix tiles; k/v hold byte
+    // offsets from k_self/v_self until bind_self_tiles adds the base.
+    for (int64_t s0 = 0; s0 < p->q_len; s0 += kKeyTile) {
+      DevTile t{};
+      const int64_t off = (((int64_t)b * p->q_len + s0) * Hkv) * D * es;
+      t.k = (const void *)(uintptr_t)off;
+      t.v = (const void *)(uintptr_t)off;
+      t.stride_head = D;
+      t.stride_tok = Hkv * D;
+      t.nvalid = (int32_t)std::min<int64_t>(kKeyTile, p->q_len - s0);
+      pl.tiles.push_back(t);
+    }
     pl.rows[b] = r;
     pl.max_prefix = std::max(pl.max_prefix, plen);
     min_row_tiles = std::min(min_row_tiles, tiles + 1);
@@ -261,6 +289,8 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
   off = align_up(off + pl.segs.size() * sizeof(DevSeg), 256);
   pl.off_rows = off;
   off = align_up(off + pl.rows.size() * sizeof(DevRow), 256);
+  pl.off_tiles = off;
+  off = align_up(off + pl.tiles.size() * sizeof(DevTile), 256);
   if (bwd) {
     pl.off_carts = off;
     off = align_up(off + pl.carts.size() * sizeof(DevCart), 256);
@@ -276,6 +306,13 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
       pl.off_part_lse = off;
       off = align_up(off + (size_t)pl.fwd_splits * plane * 4, 256);
     }
+    if (pl.dt == kBF16) {
+      // Per-workgroup flags and per-row maxima of the exact-maximum pass.
+      pl.off_ovf = off;
+      off = align_up(off + (size_t)pl.B * Hkv * pl.nqblk_fwd * pl.fwd_splits * 4, 256);
+      pl.off_row_max = off;
+      off = align_up(off + (size_t)pl.fwd_splits * plane * 4, 256);
+    }
     pl.ws_fwd = off;
   } else {
     pl.off_dvec = off;
@@ -289,6 +326,19 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
     pl.ws_bwd = off;
   }
   return CAS_OK;
+}
+
+// Turns the self-tile offsets of the tile table into pointers.
+void bind_self_tiles(Plan &pl, const void *k_self, const void *v_self) {
+  for (int b = 0; b < pl.B; ++b) {
+    const DevRow &r = pl.rows[b];
+    const int n = (int)ceil_div(pl.Sq, kKeyTile);
+    for (int i = 0; i < n; ++i) {
+      DevTile &t = pl.tiles[r.tile_begin + r.prefix_tiles + i];
+      t.k = (const char *)k_self + (uintptr_t)t.k;
+      t.v = (const char *)v_self + (uintptr_t)t.v;
+    }
+  }
 }
 
 void add_segment_intervals(const Plan &pl, const cas_problem_t *p, bool with_grads,
@@ -311,11 +361,12 @@ void add_segment_intervals(const Plan &pl, const cas_problem_t *p, bool with_gra
 // ---------------------------------------------------------------------------
 // Pinned staging ring for segment tables (host -> workspace copies).
 // ---------------------------------------------------------------------------
-constexpr size_t kSlotBytes = 1 << 20;
+constexpr size_t kMinSlotBytes = 1 << 20;
 constexpr int kSlots = 8;
 
 struct Ring {
   char *host = nullptr;
+  size_t slot_bytes = 0;
   hipEvent_t ev[kSlots] = {};
   bool used[kSlots] = {};
   int next = 0;
@@ -325,23 +376,36 @@ std::mutex g_ring_mu;
 std::map<int, Ring> g_rings;
 
 cas_status_t upload_tables(const Plan &pl, bool bwd, void *ws, hipStream_t stream) {
-  if (pl.table_bytes > kSlotBytes)
-    return fail(CAS_ERR_UNSUPPORTED, "segment table larger than " + std::to_string(kSlotBytes) + " bytes");
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
   std::lock_guard<std::mutex> lk(g_ring_mu);
   Ring &r = g_rings[dev];
-  if (!r.host) {
-    e = hipHostMalloc((void **)&r.host, kSlotBytes * kSlots, hipHostMallocDefault);
-    if (e != hipSuccess) {
-      r.host = nullptr;
-      return fail(CAS_ERR_HIP, std::string("hipHostMalloc: ") + hipGetErrorString(e));
-    }
+  if (!r.ev[0]) {
     for (int i = 0; i < kSlots; ++i) {
       e = hipEventCreateWithFlags(&r.ev[i], hipEventDisableTiming);
       if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipEventCreate: ") + hipGetErrorString(e));
     }
+  }
+  if (!r.host || pl.table_bytes > r.slot_bytes) {
+    // (Re)allocate the pinned ring once every earlier upload from it is done.
+    for (int i = 0; i < kSlots; ++i) {
+      if (!r.used[i]) continue;
+      e = hipEventSynchronize(r.ev[i]);
+      if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipEventSynchronize: ") + hipGetErrorString(e));
+      r.used[i] = false;
+    }
+    if (r.host) hipHostFree(r.host);
+    r.host = nullptr;
+    size_t sb = kMinSlotBytes;
+    while (sb < pl.table_bytes) sb *= 2;
+    e = hipHostMalloc((void **)&r.host, sb * kSlots, hipHostMallocDefault);
+    if (e != hipSuccess) {
+      r.host = nullptr;
+      r.slot_bytes = 0;
+      return fail(CAS_ERR_HIP, std::string("hipHostMalloc: ") + hipGetErrorString(e));
+    }
+    r.slot_bytes = sb;
   }
   const int slot = r.next;
   r.next = (r.next + 1) % kSlots;
@@ -349,10 +413,11 @@ cas_status_t upload_tables(const Plan &pl, bool bwd, void *ws, hipStream_t strea
     e = hipEventSynchronize(r.ev[slot]);
     if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipEventSynchronize: ") + hipGetErrorString(e));
   }
-  char *h = r.host + (size_t)slot * kSlotBytes;
+  char *h = r.host + (size_t)slot * r.slot_bytes;
   std::memset(h, 0, pl.table_bytes);
   if (!pl.segs.empty()) std::memcpy(h + pl.off_segs, pl.segs.data(), pl.segs.size() * sizeof(DevSeg));
   std::memcpy(h + pl.off_rows, pl.rows.data(), pl.rows.size() * sizeof(DevRow));
+  if (!pl.tiles.empty()) std::memcpy(h + pl.off_tiles, pl.tiles.data(), pl.tiles.size() * sizeof(DevTile));
   if (bwd) {
     if (!pl.carts.empty()) std::memcpy(h + pl.off_carts, pl.carts.data(), pl.carts.size() * sizeof(DevCart));
     if (!pl.uses.empty()) std::memcpy(h + pl.off_uses, pl.uses.data(), pl.uses.size() * sizeof(int32_t));
@@ -518,6 +583,7 @@ cas_status_t cas_prefix_attn_fwd(const cas_problem_t *p, const void *q, const vo
   if (s != CAS_OK) return s;
 
   hipStream_t stream = (hipStream_t)hip_stream;
+  bind_self_tiles(pl, k_self, v_self);
   s = upload_tables(pl, false, workspace, stream);
   if (s != CAS_OK) return s;
   char *ws = (char *)workspace;
@@ -531,6 +597,9 @@ cas_status_t cas_prefix_attn_fwd(const cas_problem_t *p, const void *q, const vo
   fp.part_lse = pl.fwd_splits > 1 ? (float *)(ws + pl.off_part_lse) : nullptr;
   fp.segs = (const DevSeg *)(ws + pl.off_segs);
   fp.rows = (const DevRow *)(ws + pl.off_rows);
+  fp.tiles = (const DevTile *)(ws + pl.off_tiles);
+  fp.ovf_flag = pl.dt == kBF16 ? (int32_t *)(ws + pl.off_ovf) : nullptr;
+  fp.row_max = pl.dt == kBF16 ? (float *)(ws + pl.off_row_max) : nullptr;
   fp.B = pl.B;
   fp.Sq = pl.Sq;
   fp.Hkv = pl.Hkv;
@@ -590,6 +659,7 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
   if (s != CAS_OK) return s;
 
   hipStream_t stream = (hipStream_t)hip_stream;
+  bind_self_tiles(pl, k_self, v_self);
   s = upload_tables(pl, true, workspace, stream);
   if (s != CAS_OK) return s;
   char *ws = (char *)workspace;
@@ -650,6 +720,7 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
     dp.dq = dq;
     dp.part_dq = pl.dq_splits > 1 ? (float *)(ws + pl.off_part_dq) : nullptr;
     dp.segs = (const DevSeg *)(ws + pl.off_segs);
+    dp.tiles = (const DevTile *)(ws + pl.off_tiles);
     dp.rows = (const DevRow *)(ws + pl.off_rows);
     dp.B = pl.B;
     dp.Sq = pl.Sq;

@@ -19,7 +19,7 @@ constexpr int kFastThreads = kNW * 64;
 constexpr int kKT = 64;                // keys per tile (forward, dQ)
 constexpr int kFastRowsPerWave = 32;
 constexpr int kFastRowsPerWg = kNW * kFastRowsPerWave;   // 256
-constexpr float kRescaleSlack = 8.0f;  // lazy softmax rescale threshold (log2 units)
+constexpr float kRefMargin = 64.0f;    // forward: largest score above the row's fixed offset (log2 units)
 
 struct TileInfo {
   const __bf16 *kp;
@@ -84,39 +84,33 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// Key tile `tile` of batch row b: prefix tiles walk the segment table (seg is
-// the walk position, advanced monotonically), then causal self tiles.
-__device__ __forceinline__ TileInfo key_tile(const DevSeg *segs, int &seg, int ptiles, int tile,
-                                             const __bf16 *k_self, const __bf16 *v_self, int b,
-                                             int Sq, int Hkv, int kvh, int D) {
-  TileInfo ti;
-  if (tile < ptiles) {
-    // seg is wave-uniform: readfirstlane keeps the descriptor loads scalar
-    // (s_load), off the vector-memory counter the tile copies use.
-    for (;;) {
-      const DevSeg sd = load_const(segs, __builtin_amdgcn_readfirstlane(seg));
-      if (tile < sd.tile_begin + (sd.len + kKT - 1) / kKT) break;
-      ++seg;
-    }
-    const DevSeg sd = load_const(segs, __builtin_amdgcn_readfirstlane(seg));
-    const int key0 = (tile - sd.tile_begin) * kKT;
-    const int64_t off = kvh * sd.stride_head + (int64_t)key0 * sd.stride_tok;
-    ti.kp = (const __bf16 *)sd.k + off;
-    ti.vp = (const __bf16 *)sd.v + off;
-    ti.st = (int)sd.stride_tok;
-    ti.nvalid = min(kKT, sd.len - key0);
-    ti.self0 = -1;
-  } else {
-    const int s0 = (tile - ptiles) * kKT;
-    const int64_t off = (((int64_t)b * Sq + s0) * Hkv + kvh) * D;
-    ti.kp = k_self + off;
-    ti.vp = v_self + off;
-    ti.st = Hkv * D;
-    ti.nvalid = min(kKT, Sq - s0);
-    ti.self0 = s0;
+// Key tiles of one batch row at one KV head, from the row's slice of the
+// host-built tile table (one scalar load per tile): the prefix tiles in
+// segment order, then the causal self tiles.
+struct TileTable {
+  const DevTile *tiles;
+  int tile_begin;   // row's first table entry
+  int ptiles;       // prefix tiles of the row
+  int kvh;
+
+  __device__ __forceinline__ void init(const DevTile *t, const DevRow &row, int kvh_) {
+    tiles = t;
+    tile_begin = __builtin_amdgcn_readfirstlane(row.tile_begin);
+    ptiles = __builtin_amdgcn_readfirstlane(row.prefix_tiles);
+    kvh = kvh_;
   }
-  return ti;
-}
+  __device__ __forceinline__ TileInfo at(int tile) const {
+    const DevTile t = load_const(tiles, __builtin_amdgcn_readfirstlane(tile_begin + tile));
+    const int64_t hoff = kvh * t.stride_head;
+    TileInfo ti;
+    ti.kp = (const __bf16 *)t.k + hoff;
+    ti.vp = (const __bf16 *)t.v + hoff;
+    ti.st = t.stride_tok;
+    ti.nvalid = t.nvalid;
+    ti.self0 = tile < ptiles ? -1 : (tile - ptiles) * kKT;
+    return ti;
+  }
+};
 
 }  // namespace
 
@@ -125,18 +119,27 @@ __device__ __forceinline__ TileInfo key_tile(const DevSeg *segs, int &seg, int p
 //
 // Waves 0-3 (group A) and 4-7 (group B) occupy one slot on each of the four
 // SIMDs. Per key tile i a wave runs a matrix phase G_i (O += V_{i-1}^T P_{i-1},
-// then S_i = K_i Q^T: 32 MFMAs) and a softmax phase X_i (mask, running max,
-// exp2, row sums, bf16 packing of P_i: VALU only). Group B runs one phase
+// then S_i = K_i Q^T: 32 MFMAs) and a softmax phase X_i (mask, row max, exp2,
+// bf16 packing of P_i and its row sums: VALU only). Group B runs one phase
 // behind group A and every phase ends in a workgroup barrier, so on each SIMD
-// one wave's MFMA stream always runs beside the other wave's softmax.
+// one wave's MFMA stream runs beside the other wave's softmax.
 //
 // LDS: two K and two V tile buffers. At the start of phase 2i every wave
 // issues its share of the copies of K_{i+1} and V_i (into the buffers K_{i-1}
 // and V_{i-2} left free after phase 2i-1); they are waited for at the end of
 // phase 2i+1, before group A's G_{i+1} reads them.
+//
+// Softmax reference: a row's exponent offset m is fixed by the first tile in
+// which it sees a key, and never moved, so O is never rescaled in the loop.
+// Later scores may exceed m by up to kRefMargin (log2 units) -- P stays below
+// 2^kRefMargin, far inside fp32 and bf16 range. A row that goes beyond the
+// margin flags the workgroup; it records every row's exact maximum, and a
+// second launch (FIXUP) recomputes only the flagged workgroups with m set to
+// that maximum. Unflagged workgroups of the second launch exit at once.
 // ---------------------------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void fwd_bf16_kernel(FwdParams p) {
+template <int D, bool FIXUP>
+__global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void fwd_bf16_kernel(FwdParams p) {
   constexpr int NSTEP = D / 16;
   constexpr int DT = D / 32;
   constexpr int TB = kKT * D * 2;
@@ -155,6 +158,9 @@ __global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2,
   bid /= p.Hkv;
   const int split = __builtin_amdgcn_readfirstlane(bid % p.splits);
   const int b = __builtin_amdgcn_readfirstlane(bid / p.splits);
+  if constexpr (FIXUP) {
+    if (load_const(p.ovf_flag, (int)blockIdx.x) == 0) return;
+  }
 
   const int g = p.g, Sq = p.Sq, Hkv = p.Hkv, Hq = Hkv * g, nrows = p.nrows;
   const int wg_row0 = qblk * kFastRowsPerWg;
@@ -167,10 +173,8 @@ __global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2,
   const int my_row = row0 + n;
   const int my_t = my_row / g;
   const float c = p.scale_log2;
-  RowOffsets<D> ro;
-  ro.init(n, G);
-  TrOffsets<D> to;
-  to.init(lane);
+  // This row's slot in the per-split row-maximum buffer.
+  const int64_t mrow = (((int64_t)split * p.B + b) * Hkv + kvh) * nrows + min(my_row, nrows - 1);
 
   // Wave-uniform tile range of this split (readfirstlane keeps it, and every
   // segment-table read that depends on it, in scalar registers).
@@ -180,7 +184,13 @@ __global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2,
   const int tb = __builtin_amdgcn_readfirstlane((int)((int64_t)ntiles * split / p.splits));
   const int te = __builtin_amdgcn_readfirstlane((int)((int64_t)ntiles * (split + 1) / p.splits));
   const int nt = te - tb;
-  int seg = __builtin_amdgcn_readfirstlane(row.seg_begin);
+  TileTable tt;
+  tt.init(p.tiles, row, kvh);
+
+  RowOffsets<D> ro;
+  ro.init(n, G);
+  TrOffsets<D> to;
+  to.init(lane);
 
   bf16x8 qf[NSTEP];
   if (my_row < nrows) {
@@ -191,14 +201,19 @@ __global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2,
 #pragma unroll
     for (int st = 0; st < NSTEP; ++st) qf[st] = Mma<__bf16>::zero();
   }
+  // The tile copies below are not ordered with these loads by the compiler's
+  // counters' bookkeeping alone; wait for Q before the first copy is issued.
+  wait_vmcnt<0>();
 
   f32x16 oacc[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) oacc[dt] = zero16();
-  float m_run = -INFINITY, l_run = 0.0f;
-
-  const __bf16 *k_self = (const __bf16 *)p.k_self;
-  const __bf16 *v_self = (const __bf16 *)p.v_self;
+  // Exponent offset of this lane's row: fixed by its first visible tile, or
+  // (FIXUP) the exact row maximum the first launch recorded.
+  float m_run = FIXUP ? p.row_max[mrow] : -INFINITY;
+  float m_max = -INFINITY;    // exact running row max
+  float l_run = 0.0f;
+  bool beyond = false;        // a score exceeded m_run + kRefMargin
 
   CopyLanes<D, kKT, kNW> cl;
   cl.init(wave, lane);
@@ -214,7 +229,9 @@ __global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2,
 
   // Whether this wave has any visible key in a tile (self tiles past the
   // wave's last query position are skipped), and whether it needs the mask.
-  auto live = [&](const TileMask &tm) __attribute__((always_inline)) { return wave_active && !(tm.self0 >= 0 && tm.self0 > wave_t_hi); };
+  auto live = [&](const TileMask &tm) __attribute__((always_inline)) {
+    return wave_active && !(tm.self0 >= 0 && tm.self0 > wave_t_hi);
+  };
   auto needs_mask = [&](const TileMask &tm) __attribute__((always_inline)) {
     return (tm.nvalid < kKT) || (tm.self0 >= 0 && tm.self0 + kKT - 1 > wave_t_lo);
   };
@@ -272,43 +289,45 @@ __global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2,
   };
   auto softmax = [&](auto MASK, const TileMask &tm) __attribute__((always_inline)) {
     if constexpr (decltype(MASK)::value) {
+      // lim: last visible key of this lane's query within the tile. Register
+      // j of group G holds key crow(j, G) = crow(j, 0) + 4G, so comparing
+      // lim - 4G against compile-time constants needs no index registers.
       const int lim = tm.self0 < 0 ? tm.nvalid - 1 : min(tm.nvalid - 1, my_t - tm.self0);
+      const int limg = lim - 4 * G;
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
-        const int k0 = crow(j, G), k1 = 32 + crow(j, G);
-        // Last visible key of this lane's query: lim (keys beyond it masked).
-        s0[j] = k0 <= lim ? s0[j] : -INFINITY;
-        s1[j] = k1 <= lim ? s1[j] : -INFINITY;
+        s0[j] = crow(j, 0) <= limg ? s0[j] : -INFINITY;
+        s1[j] = 32 + crow(j, 0) <= limg ? s1[j] : -INFINITY;
       }
     }
     float mx = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) mx = fmaxf(mx, fmaxf(s0[j], s1[j]));
+    for (int j = 0; j < 16; j += 2) mx = fmaxf(fmaxf(mx, fmaxf(s0[j], s1[j])), fmaxf(s0[j + 1], s1[j + 1]));
     const float mt = fmaxf(mx, xor32(mx)) * c;
-    // Lazy rescale: only when the running max grows by more than the slack
-    // (the unnormalised terms then stay below 2^slack; O/l is unchanged).
-    if (wave_any(mt > m_run + kRescaleSlack)) {
-      const float m_new = fmaxf(m_run, mt);
-      const float alpha = (m_run == -INFINITY) ? 0.0f : fast_exp2(m_run - m_new);
-      l_run *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
-      m_run = m_new;
+    if constexpr (!FIXUP) {
+      m_run = (m_run == -INFINITY) ? mt : m_run;
+      beyond = beyond || (mt > m_run + kRefMargin);
+      m_max = fmaxf(m_max, mt);
     }
     const float mu = (m_run == -INFINITY) ? 0.0f : m_run;
-    float ls = 0.0f;
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       s0[j] = fast_exp2(fmaf(s0[j], c, -mu));
       s1[j] = fast_exp2(fmaf(s1[j], c, -mu));
-      ls += s0[j] + s1[j];
     }
-    l_run += ls;
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       pf[0][s] = pack_bf16x8(s0, s);
       pf[1][s] = pack_bf16x8(s1, s);
     }
+    // Row sums in fp32 (the LSE needs them to better than bf16 rounding).
+    float la = 0.0f, lb = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      la += s0[j];
+      lb += s1[j];
+    }
+    l_run += la + lb;
   };
 
   // Tile bookkeeping (wave-uniform): the copy source of the last K tile
@@ -320,11 +339,8 @@ __global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2,
   };
 
   // Matrix phase G_j of this wave: O += V_{j-1}^T P_{j-1}, then S_j.
-  // (The scheduling barrier keeps the two halves' LDS fragments from being
-  // in flight together, which would not fit the register budget.)
   auto gphase = [&](int j, const char *kb, const char *vbp) __attribute__((always_inline)) {
     if (j >= 1 && j - 1 < nt && live(tmask(j - 1))) pv(vbp);
-    __builtin_amdgcn_sched_barrier(0);
     if (j < nt && live(tmask(j))) scores(kb);
   };
   auto xphase = [&](int j) __attribute__((always_inline)) {
@@ -346,41 +362,50 @@ __global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2,
       sf0 = tv.self0;
     }
     if (i + 1 < nt) {
-      tk = key_tile(p.segs, seg, ptiles, tb + i + 1, k_self, v_self, b, Sq, Hkv, kvh, D);
+      tk = tt.at(tb + i + 1);
       cl.issue(kbn, tk.kp, tk.st, tk.nvalid, wave);
     }
     cl.issue(vbi, tv.vp, tv.st, tv.nvalid, wave);
   };
 
-  if (nt > 0) {
-    tk = key_tile(p.segs, seg, ptiles, tb, k_self, v_self, b, Sq, Hkv, kvh, D);
-    cl.issue(kb0, tk.kp, tk.st, tk.nvalid, wave);
-    wait_vmcnt<0>();
-    lds_barrier();
-    // Four phases per iteration (two tiles), so every buffer is a fixed LDS
-    // address: phases 2i, 2i+1 use K_i in kb0 and V_{i-1} in vb1; phases
-    // 2i+2, 2i+3 use K_{i+1} in kb1 and V_i in vb0. Each group runs its own
-    // copy of the loop (straight-line phases); s_barrier pairs them up.
-    auto run = [&](auto GROUP_A) __attribute__((always_inline)) {
-      constexpr bool A = decltype(GROUP_A)::value;
-      for (int i = 0; i <= nt; i += 2) {
-        issue(i, kb1, vb0);
-        if constexpr (A) gphase(i, kb0, vb1); else xphase(i - 1);
-        lds_barrier();
-        if constexpr (A) xphase(i); else gphase(i, kb0, vb1);
-        wait_vmcnt<0>();
-        lds_barrier();
-        if (i + 1 > nt) break;
-        issue(i + 1, kb0, vb1);
-        if constexpr (A) gphase(i + 1, kb1, vb0); else xphase(i);
-        lds_barrier();
-        if constexpr (A) xphase(i + 1); else gphase(i + 1, kb1, vb0);
-        wait_vmcnt<0>();
-        lds_barrier();
-      }
-    };
-    if (grp == 0) run(std::true_type{});
-    else run(std::false_type{});
+  {
+    if (nt > 0) {
+      tk = tt.at(tb);
+      cl.issue(kb0, tk.kp, tk.st, tk.nvalid, wave);
+      wait_vmcnt<0>();
+      lds_barrier();
+      // Four phases per iteration (two tiles), so every buffer is a fixed LDS
+      // address: phases 2i, 2i+1 use K_i in kb0 and V_{i-1} in vb1; phases
+      // 2i+2, 2i+3 use K_{i+1} in kb1 and V_i in vb0. Each group runs its own
+      // copy of the loop (straight-line phases); s_barrier pairs them up.
+      auto run = [&](auto GROUP_A) __attribute__((always_inline)) {
+        constexpr bool A = decltype(GROUP_A)::value;
+        for (int i = 0; i <= nt; i += 2) {
+          issue(i, kb1, vb0);
+          if constexpr (A) gphase(i, kb0, vb1); else xphase(i - 1);
+          lds_barrier();
+          if constexpr (A) xphase(i); else gphase(i, kb0, vb1);
+          wait_vmcnt<0>();
+          lds_barrier();
+          if (i + 1 > nt) break;
+          issue(i + 1, kb0, vb1);
+          if constexpr (A) gphase(i + 1, kb1, vb0); else xphase(i);
+          lds_barrier();
+          if constexpr (A) xphase(i + 1); else gphase(i + 1, kb1, vb0);
+          wait_vmcnt<0>();
+          lds_barrier();
+        }
+      };
+      if (grp == 0) run(std::true_type{});
+      else run(std::false_type{});
+    }
+  }
+  if constexpr (!FIXUP) {
+    // Every wave reaches this point: flag the workgroup and keep the exact
+    // row maxima if any row went beyond the margin.
+    const int any = __syncthreads_or(beyond ? 1 : 0);
+    if (tid == 0) p.ovf_flag[blockIdx.x] = any;
+    if (any && my_row < nrows && G == 0) p.row_max[mrow] = m_max;
   }
 
   const float lt = l_run + xor32(l_run);
@@ -476,13 +501,12 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
   for (int dt = 0; dt < DT; ++dt) acc[dt] = zero16();
 
   const DevRow row = load_const(p.rows, b);
-  const int ptiles = row.prefix_tiles;
+  const int ptiles = __builtin_amdgcn_readfirstlane(row.prefix_tiles);
   const int ntiles = ptiles + wg_t_hi / kKT + 1;
-  const int tb = (int)((int64_t)ntiles * split / p.splits);
-  const int te = (int)((int64_t)ntiles * (split + 1) / p.splits);
-  int seg = row.seg_begin;
-  const __bf16 *k_self = (const __bf16 *)p.k_self;
-  const __bf16 *v_self = (const __bf16 *)p.v_self;
+  const int tb = __builtin_amdgcn_readfirstlane((int)((int64_t)ntiles * split / p.splits));
+  const int te = __builtin_amdgcn_readfirstlane((int)((int64_t)ntiles * (split + 1) / p.splits));
+  TileTable tt;
+  tt.init(p.tiles, row, kvh);
 
   auto issue = [&](const TileInfo &ti, char *kb, char *vb) __attribute__((always_inline)) {
     dma_tile<D, kKT, kNW>(kb, ti.kp, [&](int r) { return r * ti.st; }, ti.nvalid, wave, lane);
@@ -522,14 +546,14 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
   };
 
   if (tb < te) {
-    TileInfo cur = key_tile(p.segs, seg, ptiles, tb, k_self, v_self, b, Sq, Hkv, kvh, D);
+    TileInfo cur = tt.at(tb);
     issue(cur, kb0, vb0);
     __syncthreads();
     for (int it = tb; it < te; it += 2) {
       TileInfo nxt;
       const bool has1 = it + 1 < te;
       if (has1) {
-        nxt = key_tile(p.segs, seg, ptiles, it + 1, k_self, v_self, b, Sq, Hkv, kvh, D);
+        nxt = tt.at(it + 1);
         issue(nxt, kb1, vb1);
       }
       compute(cur, kb0, vb0);
@@ -537,7 +561,7 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
       if (!has1) break;
       const bool has2 = it + 2 < te;
       if (has2) {
-        cur = key_tile(p.segs, seg, ptiles, it + 2, k_self, v_self, b, Sq, Hkv, kvh, D);
+        cur = tt.at(it + 2);
         issue(cur, kb0, vb0);
       }
       compute(nxt, kb1, vb1);
@@ -790,10 +814,13 @@ __global__ __launch_bounds__(kFastThreads) void dkdv_bf16_kernel(DkdvParams p) {
 
 hipError_t launch_fwd_bf16(const FwdParams &p, int D, hipStream_t s) {
   const int64_t grid = (int64_t)p.nqblk * p.Hkv * p.splits * p.B;
-  if (D == 64)
-    hipLaunchKernelGGL(fwd_bf16_kernel<64>, dim3((unsigned)grid), dim3(kFastThreads), 0, s, p);
-  else
-    hipLaunchKernelGGL(fwd_bf16_kernel<128>, dim3((unsigned)grid), dim3(kFastThreads), 0, s, p);
+  if (D == 64) {
+    hipLaunchKernelGGL((fwd_bf16_kernel<64, false>), dim3((unsigned)grid), dim3(kFastThreads), 0, s, p);
+    hipLaunchKernelGGL((fwd_bf16_kernel<64, true>), dim3((unsigned)grid), dim3(kFastThreads), 0, s, p);
+  } else {
+    hipLaunchKernelGGL((fwd_bf16_kernel<128, false>), dim3((unsigned)grid), dim3(kFastThreads), 0, s, p);
+    hipLaunchKernelGGL((fwd_bf16_kernel<128, true>), dim3((unsigned)grid), dim3(kFastThreads), 0, s, p);
+  }
   return hipGetLastError();
 }
 

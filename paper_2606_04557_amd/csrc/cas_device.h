@@ -362,6 +362,7 @@ __device__ __forceinline__ bf16x8 pack_bf16x8(const f32x16 &x, int s) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+
 __device__ __forceinline__ bool wave_any(bool p) { return __ballot(p) != 0; }
 
 // s_waitcnt for "at most n vector-memory operations of this wave outstanding",

@@ -37,7 +37,17 @@ struct DevRow {
   int32_t seg_begin;
   int32_t seg_end;
   int32_t prefix_tiles;  // kKeyTile tiles over the row's whole prefix
-  int32_t pad;
+  int32_t tile_begin;    // the row's first entry in the DevTile table
+};
+
+// One kKeyTile-key tile of a row's prefix (bf16 forward and dQ): its first key
+// at KV head 0 and the strides to reach the other heads and keys.
+struct DevTile {
+  const void *k;
+  const void *v;
+  int64_t stride_head;
+  int32_t stride_tok;
+  int32_t nvalid;        // keys in the tile, 1 .. kKeyTile
 };
 
 // Distinct cartridge after alias folding (dK/dV pass).
@@ -66,6 +76,9 @@ struct FwdParams {
   float *part_lse;    // [splits][B][Hkv][nrows]
   const DevSeg *segs;
   const DevRow *rows;
+  const DevTile *tiles;
+  int32_t *ovf_flag;  // [grid] bf16: workgroup needs the exact-maximum pass
+  float *row_max;     // [splits][B][Hkv][nrows] bf16: exact row maxima (log2 units)
   int32_t B, Sq, Hkv, g, nrows, nqblk, splits;
   float scale_log2;   // softmax_scale * log2(e)
 };
@@ -98,6 +111,7 @@ struct DqParams {
   float *part_dq;   // [splits][B][Hkv][nrows][D] when splits > 1
   const DevSeg *segs;
   const DevRow *rows;
+  const DevTile *tiles;
   int32_t B, Sq, Hkv, g, nrows, nqblk, splits;
   float scale_log2;
   float scale;
