@@ -7,6 +7,7 @@
 // tile), and ds_read_b64_tr_b16 for every operand that is reduced along its
 // row axis (V in the forward, K in dQ, Q and dO in dK/dV).
 #include <type_traits>
+#include <utility>
 
 #include "cas_device.h"
 
@@ -28,6 +29,16 @@ struct TileInfo {
   int nvalid;
   int self0;   // first self key of the tile, or -1 for a cartridge tile
 };
+
+// f(integral_constant<int, 0>) ... f(integral_constant<int, N-1>), unrolled.
+template <typename F, int... Ks>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, Ks...>) {
+  (f(std::integral_constant<int, Ks>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 // Scheduling groups: the next n MFMAs / LDS reads of the region, in order.
 template <int N>
@@ -99,6 +110,9 @@ struct TileTable {
     ptiles = __builtin_amdgcn_readfirstlane(row.prefix_tiles);
     kvh = kvh_;
   }
+  __device__ __forceinline__ int nvalid(int tile) const {
+    return load_const(&tiles[__builtin_amdgcn_readfirstlane(tile_begin + tile)].nvalid, 0);
+  }
   __device__ __forceinline__ TileInfo at(int tile) const {
     const DevTile t = load_const(tiles, __builtin_amdgcn_readfirstlane(tile_begin + tile));
     const int64_t hoff = kvh * t.stride_head;
@@ -118,22 +132,23 @@ struct TileTable {
 // Forward: ping-pong between the two waves of each SIMD.
 //
 // Waves 0-3 (group A) and 4-7 (group B) occupy one slot on each of the four
-// SIMDs. Per key tile i a wave runs a matrix phase G_i (O += V_{i-1}^T P_{i-1},
-// then S_i = K_i Q^T: 32 MFMAs) and a softmax phase X_i (mask, row max, exp2,
-// bf16 packing of P_i and its row sums: VALU only). Group B runs one phase
-// behind group A and every phase ends in a workgroup barrier, so on each SIMD
-// one wave's MFMA stream runs beside the other wave's softmax.
+// SIMDs. Per key tile i a wave runs a matrix phase G_i (O += V_{i-1}^T P_{i-1}
+// and S_i = K_i Q^T: 32 MFMAs in one scheduling region) and a softmax phase
+// X_i (mask, row max, exp2, row sums, bf16 packing of P_i: VALU only). Group B
+// runs one phase behind group A and every phase ends in a workgroup barrier,
+// so on each SIMD one wave's MFMA stream runs beside the other wave's softmax.
 //
-// LDS: two K and two V tile buffers. At the start of phase 2i every wave
-// issues its share of the copies of K_{i+1} and V_i (into the buffers K_{i-1}
-// and V_{i-2} left free after phase 2i-1); they are waited for at the end of
-// phase 2i+1, before group A's G_{i+1} reads them.
+// LDS: three K and three V tile buffers. Only group B copies: at the start of
+// phase 2i (while it runs a softmax phase) it issues K_{i+2} and V_{i+1} into
+// the buffers that K_{i-1} and V_{i-2} left free after phase 2i-1, and at the
+// end of phase 2i it waits for the copies it issued at phase 2i-2, which
+// group A's G_{i+1} reads at phase 2i+2.
 //
 // Softmax reference: a row's exponent offset m is fixed by the first tile in
 // which it sees a key, and never moved, so O is never rescaled in the loop.
 // Later scores may exceed m by up to kRefMargin (log2 units) -- P stays below
 // 2^kRefMargin, far inside fp32 and bf16 range. A row that goes beyond the
-// margin flags the workgroup; it records every row's exact maximum, and a
+// margin flags its workgroup; it records every row's exact maximum, and a
 // second launch (FIXUP) recomputes only the flagged workgroups with m set to
 // that maximum. Unflagged workgroups of the second launch exit at once.
 // ---------------------------------------------------------------------------
@@ -145,8 +160,10 @@ void fwd_bf16_kernel(FwdParams p) {
   constexpr int TB = kKT * D * 2;
   __shared__ __attribute__((aligned(1024))) char kb0[TB];
   __shared__ __attribute__((aligned(1024))) char kb1[TB];
+  __shared__ __attribute__((aligned(1024))) char kb2[TB];
   __shared__ __attribute__((aligned(1024))) char vb0[TB];
   __shared__ __attribute__((aligned(1024))) char vb1[TB];
+  __shared__ __attribute__((aligned(1024))) char vb2[TB];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2;
@@ -177,7 +194,7 @@ void fwd_bf16_kernel(FwdParams p) {
   const int64_t mrow = (((int64_t)split * p.B + b) * Hkv + kvh) * nrows + min(my_row, nrows - 1);
 
   // Wave-uniform tile range of this split (readfirstlane keeps it, and every
-  // segment-table read that depends on it, in scalar registers).
+  // tile-table read that depends on it, in scalar registers).
   const DevRow row = load_const(p.rows, b);
   const int ptiles = __builtin_amdgcn_readfirstlane(row.prefix_tiles);
   const int ntiles = ptiles + wg_t_hi / kKT + 1;
@@ -201,8 +218,8 @@ void fwd_bf16_kernel(FwdParams p) {
 #pragma unroll
     for (int st = 0; st < NSTEP; ++st) qf[st] = Mma<__bf16>::zero();
   }
-  // The tile copies below are not ordered with these loads by the compiler's
-  // counters' bookkeeping alone; wait for Q before the first copy is issued.
+  // Tile copies are waited for with partial vmcnt counts, which must not
+  // include these loads.
   wait_vmcnt<0>();
 
   f32x16 oacc[DT];
@@ -215,8 +232,10 @@ void fwd_bf16_kernel(FwdParams p) {
   float l_run = 0.0f;
   bool beyond = false;        // a score exceeded m_run + kRefMargin
 
-  CopyLanes<D, kKT, kNW> cl;
-  cl.init(wave, lane);
+  // Group B's share of every tile copy (4 waves).
+  CopyLanes<D, kKT, 4> cl;
+  cl.init(wave & 3, lane);
+  constexpr int kCopyInst = CopyLanes<D, kKT, 4>::PER;   // per wave per K or V tile
 
   // Scores of the tile between its G and X phases; P of the tile between its
   // X phase and the next G phase.
@@ -227,72 +246,81 @@ void fwd_bf16_kernel(FwdParams p) {
 #pragma unroll
     for (int s = 0; s < 2; ++s) pf[a][s] = Mma<__bf16>::zero();
 
-  // Whether this wave has any visible key in a tile (self tiles past the
-  // wave's last query position are skipped), and whether it needs the mask.
-  auto live = [&](const TileMask &tm) __attribute__((always_inline)) {
-    return wave_active && !(tm.self0 >= 0 && tm.self0 > wave_t_hi);
+  // Local tile j: whether this wave sees any key of it (self tiles past the
+  // wave's last query position are skipped), and its mask data.
+  auto self0_of = [&](int j) __attribute__((always_inline)) {
+    return tb + j < ptiles ? -1 : (tb + j - ptiles) * kKT;
   };
-  auto needs_mask = [&](const TileMask &tm) __attribute__((always_inline)) {
-    return (tm.nvalid < kKT) || (tm.self0 >= 0 && tm.self0 + kKT - 1 > wave_t_lo);
+  auto live = [&](int j) __attribute__((always_inline)) {
+    const int s0_ = self0_of(j);
+    return wave_active && !(s0_ >= 0 && s0_ > wave_t_hi);
   };
 
-  // The matrix phases read every LDS fragment into registers a few MFMAs
-  // ahead of its use (the scheduling groups pin that order), so the LDS
-  // latency hides behind the MFMA pipe instead of stalling it.
-  auto scores = [&](const char *kb) __attribute__((always_inline)) {
-    constexpr int LEAD = 4;
-    bf16x8 fr[2 * NSTEP];
-#pragma unroll
-    for (int st = 0; st < NSTEP; ++st) {
-      fr[2 * st] = row_frag_at<D>(kb, ro, 0, st);
-      fr[2 * st + 1] = row_frag_at<D>(kb, ro, 32, st);
-    }
-    s0 = zero16();
-    s1 = zero16();
-#pragma unroll
-    for (int st = 0; st < NSTEP; ++st) {
-      s0 = Mma<__bf16>::run(fr[2 * st], qf[st], s0);
-      s1 = Mma<__bf16>::run(fr[2 * st + 1], qf[st], s1);
-    }
-    sched_ds_read<LEAD>();
-#pragma unroll
-    for (int k = 0; k < 2 * NSTEP - LEAD; ++k) {
-      sched_mfma<1>();
-      sched_ds_read<1>();
-    }
-    sched_mfma<LEAD>();
-  };
-  auto pv = [&](const char *vb) __attribute__((always_inline)) {
-    constexpr int LEAD = 4;
-    bf16x8 fr[4 * DT];
-#pragma unroll
-    for (int s = 0; s < 2; ++s)
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        fr[(s * DT + dt) * 2] = tr_frag_at<D>(vb, to, 16 * s, dt);
-        fr[(s * DT + dt) * 2 + 1] = tr_frag_at<D>(vb, to, 32 + 16 * s, dt);
+  // Matrix phase as one software-pipelined sequence of MFMAs: the PV product
+  // of the previous tile (16 MFMAs, two transposed LDS reads per fragment),
+  // then the scores of this one (16 MFMAs, one LDS read per fragment). The
+  // fragment of MFMA k+LEAD is read while MFMA k runs, into a ring of LEAD+1
+  // registers, and the scheduling groups pin exactly that order, so the LDS
+  // latency hides behind the MFMA pipe across the PV -> S boundary too.
+  auto matrix = [&](auto DO_PV, auto DO_S, const char *kb, const char *vb) __attribute__((always_inline)) {
+    constexpr bool PV = decltype(DO_PV)::value, S = decltype(DO_S)::value;
+    constexpr int NPV = PV ? 4 * DT : 0;          // PV MFMAs
+    constexpr int N = NPV + (S ? 2 * NSTEP : 0);  // all MFMAs
+    constexpr int LEAD = 4, R = LEAD + 1;
+    // MFMA k < NPV: s = k / (2*DT), dt = (k / 2) % DT, key half hh = k % 2.
+    // MFMA k >= NPV: st = (k - NPV) / 2, score half hh = (k - NPV) % 2.
+    auto load = [&](auto K) __attribute__((always_inline)) {
+      constexpr int k = decltype(K)::value;
+      if constexpr (k < NPV) {
+        constexpr int s = k / (2 * DT), dt = (k / 2) % DT, hh = k % 2;
+        return tr_frag_at<D>(vb, to, 32 * hh + 16 * s, dt);
+      } else {
+        constexpr int st = (k - NPV) / 2, hh = (k - NPV) % 2;
+        return row_frag_at<D>(kb, ro, 32 * hh, st);
       }
-#pragma unroll
-    for (int s = 0; s < 2; ++s)
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        oacc[dt] = Mma<__bf16>::run(fr[(s * DT + dt) * 2], pf[0][s], oacc[dt]);
-        oacc[dt] = Mma<__bf16>::run(fr[(s * DT + dt) * 2 + 1], pf[1][s], oacc[dt]);
+    };
+    auto mma = [&](auto K, const bf16x8 &f) __attribute__((always_inline)) {
+      constexpr int k = decltype(K)::value;
+      if constexpr (k < NPV) {
+        constexpr int s = k / (2 * DT), dt = (k / 2) % DT, hh = k % 2;
+        oacc[dt] = Mma<__bf16>::run(f, pf[hh][s], oacc[dt]);
+      } else {
+        constexpr int st = (k - NPV) / 2, hh = (k - NPV) % 2;
+        if constexpr (hh == 0) s0 = Mma<__bf16>::run(f, qf[st], s0);
+        else s1 = Mma<__bf16>::run(f, qf[st], s1);
       }
-    sched_ds_read<2 * LEAD>();
-#pragma unroll
-    for (int k = 0; k < 4 * DT - LEAD; ++k) {
-      sched_mfma<1>();
-      sched_ds_read<2>();
+    };
+    if constexpr (S) {
+      s0 = zero16();
+      s1 = zero16();
     }
-    sched_mfma<LEAD>();
+    bf16x8 ring[R];
+    static_for<LEAD>([&](auto K) __attribute__((always_inline)) {
+      constexpr int k = decltype(K)::value;
+      if constexpr (k < N) ring[k % R] = load(K);
+    });
+    static_for<N>([&](auto K) __attribute__((always_inline)) {
+      constexpr int k = decltype(K)::value;
+      if constexpr (k + LEAD < N) ring[(k + LEAD) % R] = load(std::integral_constant<int, k + LEAD>{});
+      mma(K, ring[k % R]);
+    });
+    // Scheduling groups: the LEAD first fragments, then per MFMA k the reads
+    // of fragment k+LEAD.
+    static_for<LEAD>([&](auto K) __attribute__((always_inline)) {
+      constexpr int k = decltype(K)::value;
+      if constexpr (k < N) sched_ds_read<(k < NPV ? 2 : 1)>();
+    });
+    static_for<N>([&](auto K) __attribute__((always_inline)) {
+      constexpr int k = decltype(K)::value;
+      sched_mfma<1>();
+      if constexpr (k + LEAD < N) sched_ds_read<(k + LEAD < NPV ? 2 : 1)>();
+    });
   };
-  auto softmax = [&](auto MASK, const TileMask &tm) __attribute__((always_inline)) {
+  auto softmax = [&](auto MASK, int lim) __attribute__((always_inline)) {
     if constexpr (decltype(MASK)::value) {
       // lim: last visible key of this lane's query within the tile. Register
       // j of group G holds key crow(j, G) = crow(j, 0) + 4G, so comparing
       // lim - 4G against compile-time constants needs no index registers.
-      const int lim = tm.self0 < 0 ? tm.nvalid - 1 : min(tm.nvalid - 1, my_t - tm.self0);
       const int limg = lim - 4 * G;
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
@@ -330,75 +358,99 @@ void fwd_bf16_kernel(FwdParams p) {
     l_run += la + lb;
   };
 
-  // Tile bookkeeping (wave-uniform): the copy source of the last K tile
-  // issued, and the mask data of tiles with even / odd local index.
-  TileInfo tk;
-  int nv0 = kKT, sf0 = -1, nv1 = kKT, sf1 = -1;
-  auto tmask = [&](int j) __attribute__((always_inline)) {
-    return (j & 1) ? TileMask{nv1, sf1} : TileMask{nv0, sf0};
-  };
-
-  // Matrix phase G_j of this wave: O += V_{j-1}^T P_{j-1}, then S_j.
+  // G_j: PV of tile j-1 (V_{j-1} in vbp) and scores of tile j (K_j in kb),
+  // always both: P is zero where there is no previous tile or it was not
+  // visible, and scores of a tile past the end or not visible are never
+  // read. (Conditionally skipping either half would make the register
+  // allocator copy the accumulators around every such branch.)
   auto gphase = [&](int j, const char *kb, const char *vbp) __attribute__((always_inline)) {
-    if (j >= 1 && j - 1 < nt && live(tmask(j - 1))) pv(vbp);
-    if (j < nt && live(tmask(j))) scores(kb);
+    if (j <= nt && wave_active) matrix(std::true_type{}, std::true_type{}, kb, vbp);
   };
   auto xphase = [&](int j) __attribute__((always_inline)) {
     if (j < 0 || j >= nt) return;
-    const TileMask tm = tmask(j);
-    if (!live(tm)) return;
-    if (needs_mask(tm)) softmax(std::true_type{}, tm);
-    else softmax(std::false_type{}, tm);
-  };
-  // Copies issued at the start of phase 2i: K_{i+1} and V_i.
-  auto issue = [&](int i, char *kbn, char *vbi) __attribute__((always_inline)) {
-    if (i >= nt) return;
-    const TileInfo tv = tk;
-    if (i & 1) {
-      nv1 = tv.nvalid;
-      sf1 = tv.self0;
+    if (!live(j)) {
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int s = 0; s < 2; ++s) pf[a][s] = Mma<__bf16>::zero();
+      return;
+    }
+    const int self0 = self0_of(j);
+    const int nvalid = __builtin_amdgcn_readfirstlane(tt.nvalid(tb + j));
+    if (nvalid < kKT || (self0 >= 0 && self0 + kKT - 1 > wave_t_lo)) {
+      const int lim = self0 < 0 ? nvalid - 1 : min(nvalid - 1, my_t - self0);
+      softmax(std::true_type{}, lim);
     } else {
-      nv0 = tv.nvalid;
-      sf0 = tv.self0;
+      softmax(std::false_type{}, kKT - 1);
     }
-    if (i + 1 < nt) {
-      tk = tt.at(tb + i + 1);
-      cl.issue(kbn, tk.kp, tk.st, tk.nvalid, wave);
-    }
-    cl.issue(vbi, tv.vp, tv.st, tv.nvalid, wave);
   };
 
-  {
-    if (nt > 0) {
-      tk = tt.at(tb);
-      cl.issue(kb0, tk.kp, tk.st, tk.nvalid, wave);
+  // Group B's copies. tk: the K tile issued last (tile i+1 when phase 2i
+  // starts), whose V is issued next.
+  TileInfo tk;
+  auto copy_k = [&](char *kbn, int j) __attribute__((always_inline)) {
+    tk = tt.at(tb + j);
+    cl.issue(kbn, tk.kp, tk.st, tk.nvalid, wave & 3);
+  };
+  // Phase 2i: K_{i+2} and V_{i+1}; then the copies of phase 2i-2 are waited for.
+  auto issue = [&](int i, char *kbn, char *vbn) __attribute__((always_inline)) {
+    if (i + 1 < nt) cl.issue(vbn, tk.vp, tk.st, tk.nvalid, wave & 3);
+    if (i + 2 < nt) copy_k(kbn, i + 2);
+  };
+  auto wait_older = [&](int i) __attribute__((always_inline)) {
+    // The newest batch (issued this phase) may still be in flight.
+    if (i + 2 < nt) wait_vmcnt<2 * kCopyInst>();
+    else if (i + 1 < nt) wait_vmcnt<kCopyInst>();
+    else wait_vmcnt<0>();
+  };
+
+  if (nt > 0) {
+    // G_0 multiplies V buffer 2 by P = 0: clear it so no stale bit pattern
+    // (a NaN) can reach O.
+    for (int i = tid; i < TB / 16; i += kFastThreads) reinterpret_cast<uint4 *>(vb2)[i] = uint4{0, 0, 0, 0};
+    // Prologue (group B): K_0, then K_1 and V_0.
+    if (grp == 1) {
+      copy_k(kb0, 0);
       wait_vmcnt<0>();
-      lds_barrier();
-      // Four phases per iteration (two tiles), so every buffer is a fixed LDS
-      // address: phases 2i, 2i+1 use K_i in kb0 and V_{i-1} in vb1; phases
-      // 2i+2, 2i+3 use K_{i+1} in kb1 and V_i in vb0. Each group runs its own
-      // copy of the loop (straight-line phases); s_barrier pairs them up.
-      auto run = [&](auto GROUP_A) __attribute__((always_inline)) {
-        constexpr bool A = decltype(GROUP_A)::value;
-        for (int i = 0; i <= nt; i += 2) {
-          issue(i, kb1, vb0);
-          if constexpr (A) gphase(i, kb0, vb1); else xphase(i - 1);
-          lds_barrier();
-          if constexpr (A) xphase(i); else gphase(i, kb0, vb1);
-          wait_vmcnt<0>();
-          lds_barrier();
-          if (i + 1 > nt) break;
-          issue(i + 1, kb0, vb1);
-          if constexpr (A) gphase(i + 1, kb1, vb0); else xphase(i);
-          lds_barrier();
-          if constexpr (A) xphase(i + 1); else gphase(i + 1, kb1, vb0);
-          wait_vmcnt<0>();
-          lds_barrier();
-        }
-      };
-      if (grp == 0) run(std::true_type{});
-      else run(std::false_type{});
+      const TileInfo t0 = tk;
+      cl.issue(vb0, t0.vp, t0.st, t0.nvalid, wave & 3);
+      if (nt > 1) copy_k(kb1, 1);
     }
+    lds_barrier();
+    // Six phases per iteration (three tiles), so every buffer is a fixed LDS
+    // address: G_i reads K_i from kb[i%3] and V_{i-1} from vb[(i-1)%3]; the
+    // copies of phase 2i go to kb[(i+2)%3] and vb[(i+1)%3]. Each group runs
+    // its own copy of the loop (straight-line phases); s_barrier pairs them.
+    auto run = [&](auto GROUP_A) __attribute__((always_inline)) {
+      constexpr bool A = decltype(GROUP_A)::value;
+      auto even = [&](int i, const char *kbi, const char *vbp, char *kbn, char *vbn) __attribute__((always_inline)) {
+        if constexpr (A) {
+          gphase(i, kbi, vbp);
+        } else {
+          issue(i, kbn, vbn);
+          xphase(i - 1);
+          wait_older(i);
+        }
+        lds_barrier();
+      };
+      auto odd = [&](int i, const char *kbi, const char *vbp) __attribute__((always_inline)) {
+        if constexpr (A) xphase(i);
+        else gphase(i, kbi, vbp);
+        lds_barrier();
+      };
+      for (int i = 0; i <= nt; i += 3) {
+        even(i, kb0, vb2, kb2, vb1);
+        odd(i, kb0, vb2);
+        if (i + 1 > nt) break;
+        even(i + 1, kb1, vb0, kb0, vb2);
+        odd(i + 1, kb1, vb0);
+        if (i + 2 > nt) break;
+        even(i + 2, kb2, vb1, kb1, vb0);
+        odd(i + 2, kb2, vb1);
+      }
+    };
+    if (grp == 0) run(std::true_type{});
+    else run(std::false_type{});
   }
   if constexpr (!FIXUP) {
     // Every wave reaches this point: flag the workgroup and keep the exact
