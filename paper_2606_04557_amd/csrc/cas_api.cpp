@@ -96,7 +96,7 @@ struct Plan {
   // workspace layout
   size_t off_segs = 0, off_rows = 0, off_tiles = 0, off_carts = 0, off_uses = 0, table_bytes = 0;
   size_t off_part_o = 0, off_part_lse = 0, off_ovf = 0, off_row_max = 0, ws_fwd = 0;
-  size_t off_dvec = 0, off_lse2 = 0, off_part_dq = 0, ws_bwd = 0;
+  size_t off_dvec = 0, off_lse2 = 0, off_part_dq = 0, off_qT = 0, off_doT = 0, ws_bwd = 0;
 };
 
 constexpr int kTargetWgs = 512;   // two workgroups per CU on a 256-CU MI355X
@@ -319,6 +319,14 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
     off = align_up(off + plane * 4, 256);
     pl.off_lse2 = off;
     off = align_up(off + plane * 4, 256);
+    if (pl.dt == kBF16) {
+      // Transposed Q and dO of every 64-row block (dK/dV operands).
+      const size_t tblk = (size_t)pl.B * Hkv * ceil_div(pl.nrows, 64) * 64 * D * 2;
+      pl.off_qT = off;
+      off = align_up(off + tblk, 256);
+      pl.off_doT = off;
+      off = align_up(off + tblk, 256);
+    }
     if (pl.dq_splits > 1) {
       pl.off_part_dq = off;
       off = align_up(off + (size_t)pl.dq_splits * plane * D * 4, 256);
@@ -678,6 +686,10 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
   pp.Hkv = pl.Hkv;
   pp.g = pl.g;
   pp.nrows = pl.nrows;
+  pp.q = q;
+  pp.qT = pl.dt == kBF16 ? ws + pl.off_qT : nullptr;
+  pp.doT = pl.dt == kBF16 ? ws + pl.off_doT : nullptr;
+  pp.nqb = (int)ceil_div(pl.nrows, 64);
   hipError_t e = timed("bwd_pre", stream, [&] { return launch_bwd_pre(pp, pl.dt, pl.D, stream); });
   if (e != hipSuccess) return hip_fail("bwd_pre launch", e);
 
@@ -691,6 +703,8 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
     kp.d_o = d_o;
     kp.dvec = dvec;
     kp.lse2 = lse2;
+    kp.qT = pp.qT;
+    kp.doT = pp.doT;
     kp.dk_self = dk_self;
     kp.dv_self = dv_self;
     kp.carts = (const DevCart *)(ws + pl.off_carts);
@@ -705,6 +719,10 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
     kp.nrows = pl.nrows;
     kp.scale_log2 = scale_log2;
     kp.scale = pl.scale;
+    if (pl.dt == kBF16) {
+      e = timed("bwd_transpose", stream, [&] { return launch_bwd_transpose_bf16(pp, pl.D, stream); });
+      if (e != hipSuccess) return hip_fail("bwd_transpose launch", e);
+    }
     e = timed("dkdv", stream, [&] { return launch_dkdv(kp, pl.dt, pl.D, gx, stream); });
     if (e != hipSuccess) return hip_fail("dkdv launch", e);
   }

@@ -20,6 +20,10 @@ constexpr int kFastThreads = kNW * 64;
 constexpr int kKT = 64;                // keys per tile (forward, dQ)
 constexpr int kFastRowsPerWave = 32;
 constexpr int kFastRowsPerWg = kNW * kFastRowsPerWave;   // 256
+#ifndef CAS_DKDV_LEAD
+#define CAS_DKDV_LEAD 4
+#endif
+constexpr int kDkdvLead = CAS_DKDV_LEAD;  // dK/dV: LDS fragments in flight ahead of their MFMA
 constexpr float kRefMargin = 64.0f;    // forward: largest score above the row's fixed offset (log2 units)
 
 struct TileInfo {
@@ -645,32 +649,111 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// dK / dV (key-stationary). 128 keys per workgroup, resident in LDS; wave w
-// owns keys 32*(w%4) .. +32 and query subtile w/4 of every 64-row block. The
-// two waves sharing keys add their sums through LDS at the end.
+// Backward prologue for the bf16 dK/dV kernel: Q and dO of every 64-row
+// query block of each (batch row, KV head), transposed to [channel][64 rows],
+// zero beyond nrows. Within each 16-row group the rows are stored in the
+// order 0-3, 8-11, 4-7, 12-15, so the 8 rows that one lane group of a 32x32
+// MFMA fragment needs (4G..4G+3 and 8+4G..8+4G+3) are one 16-byte chunk.
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(kFastThreads) void dkdv_bf16_kernel(DkdvParams p) {
+__global__ __launch_bounds__(256) void bwd_transpose_bf16_kernel(PreParams p) {
+  __shared__ __attribute__((aligned(16))) __bf16 tile[64][D + 8];
+  const int tid = threadIdx.x;
+  const int qb = blockIdx.x % p.nqb;
+  const int bk = blockIdx.x / p.nqb;
+  const int kvh = bk % p.Hkv, b = bk / p.Hkv;
+  const int g = p.g, Hq = p.Hkv * g;
+  for (int which = 0; which < 2; ++which) {
+    const __bf16 *src = (const __bf16 *)(which ? p.d_o : p.q);
+    __bf16 *dst = (__bf16 *)(which ? p.doT : p.qT) + (int64_t)blockIdx.x * D * 64;
+    for (int i = tid; i < 64 * D / 8; i += 256) {
+      const int r = i / (D / 8), c8 = i % (D / 8);
+      const int rr = qb * 64 + r;
+      uint4 v = uint4{0, 0, 0, 0};
+      if (rr < p.nrows) {
+        const int t = rr / g, h = kvh * g + (rr - t * g);
+        v = *reinterpret_cast<const uint4 *>(src + (((int64_t)b * p.Sq + t) * Hq + h) * D + c8 * 8);
+      }
+      *reinterpret_cast<uint4 *>(&tile[r][c8 * 8]) = v;
+    }
+    __syncthreads();
+    for (int i = tid; i < D * 8; i += 256) {
+      const int d = i / 8, pg = i % 8;
+      bf16x8 out;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int pos = pg * 8 + e, w = pos & 15, quad = w >> 2;
+        const int sq = quad == 1 ? 2 : (quad == 2 ? 1 : quad);
+        out[e] = tile[(pos & ~15) + sq * 4 + (w & 3)][d];
+      }
+      *reinterpret_cast<bf16x8 *>(dst + d * 64 + pg * 8) = out;
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dK / dV (key-stationary): S and dP on the two waves of each SIMD.
+//
+// 128 keys per workgroup of eight waves. Waves w and w+4 share SIMD w and
+// keys 32w .. 32w+31. Wave w (the P wave) holds their K fragments and computes
+// S = Q K^T, P = exp2(S c - LSE2) and dV^T += dO^T P; wave w+4 (the dS wave)
+// holds their V fragments and computes dP = dO V^T, dS = P (dP - D) and
+// dK^T += Q^T dS, taking P from the P wave through LDS. Each wave so keeps one
+// 32 x D accumulator and one operand set in registers (two waves per SIMD
+// fit), and per 64-row query block runs 32 MFMAs (D = 128) and one VALU pass.
+// Block i is two phases, each ending in a workgroup barrier:
+//   A_i: P waves:  S_{i+1}, dV += dO_i^T P_i       (MFMA)
+//        dS waves: dS_i = P_i (dP_i - D_i)          (VALU)
+//   B_i: dS waves: dK += Q_i^T dS_i, dP_{i+1}       (MFMA)
+//        P waves:  P_{i+1} = exp2(S_{i+1} c - LSE2)  (VALU)
+// so on every SIMD one wave's MFMA stream runs beside the other's VALU work.
+// Every operand read is a 16-byte row read: Q and dO rows for S and dP, and
+// the transposed blocks Q^T and dO^T (written by the backward prologue) for
+// the dK and dV products.
+//
+// Copies (LDS double buffers), one instruction per four MFMAs of the issuing
+// wave's matrix phase: P waves issue dO rows of block i+2, Q^T_{i+1} and LSE2
+// of i+2 during A_i; dS waves issue Q rows of block i+3, dO^T_{i+2} and D of
+// i+2 during B_i. A wave waits for a batch at the end of its next matrix
+// phase. Copies for blocks past the end use an empty buffer resource (they
+// write zeros that nothing reads), so every batch has the same size.
+//
+// P needs no mask for keys beyond the tile (their dK / dV columns are never
+// stored) or rows beyond nrows (Q, dO, Q^T, dO^T, LSE2 and D all read as
+// zero there: P = 1 and dS = 0 add nothing). On self keys P = 0 for rows
+// before the key's position.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void dkdv_bf16_kernel(DkdvParams p) {
   constexpr int NSTEP = D / 16;
   constexpr int DT = D / 32;
-  constexpr int QB = 64;
-  constexpr int KTB = kDkdvKeyTile;            // 128
-  constexpr int KVB = KTB * D * 2;
-  constexpr int QBB = QB * D * 2;
-  __shared__ __attribute__((aligned(1024))) char ktile[KVB];
-  __shared__ __attribute__((aligned(1024))) char vtile[KVB];
-  __shared__ __attribute__((aligned(1024))) char qb0[QBB];
-  __shared__ __attribute__((aligned(1024))) char ob0[QBB];
-  __shared__ __attribute__((aligned(1024))) char qb1[QBB];
-  __shared__ __attribute__((aligned(1024))) char ob1[QBB];
-  __shared__ __attribute__((aligned(256))) float ls0[QB];
-  __shared__ __attribute__((aligned(256))) float dv0[QB];
-  __shared__ __attribute__((aligned(256))) float ls1[QB];
-  __shared__ __attribute__((aligned(256))) float dv1[QB];
+  constexpr int QB = kDkdvQBlock;              // 64 query rows per block
+  constexpr int KTB = kDkdvKeyTile;            // 128 keys
+  constexpr int RB = QB * D * 2;               // bytes of one 64 x D block
+  constexpr int NMF = 4 * NSTEP;               // MFMAs of a wave's matrix phase
+  constexpr int LEAD = kDkdvLead, RING = LEAD + 1;
+  // One LDS arena. The P waves' matrix operands (Q rows, dO^T) fill the first
+  // 4 RB bytes and the dS waves' (dO rows, Q^T) the next 4 RB, so each wave
+  // reaches all of its fragments from one set of lane offsets plus 16-bit
+  // immediates.
+  constexpr int XCH = 8 * RB;                  // P of each SIMD's 32 keys x 64 rows, 4 KiB per SIMD
+  constexpr int STATS = XCH + 16384;           // LSE2 x2, D x2
+  __shared__ __attribute__((aligned(1024))) char smem[STATS + 4 * QB * 4];
+  char *const qr0 = smem, *const qr1 = smem + RB, *const ot0 = smem + 2 * RB, *const ot1 = smem + 3 * RB;
+  char *const or0 = smem + 4 * RB, *const or1 = smem + 5 * RB, *const qt0 = smem + 6 * RB,
+              *const qt1 = smem + 7 * RB;
+  char *const xch = smem + XCH;
+  float *const ls0 = reinterpret_cast<float *>(smem + STATS);
+  float *const ls1 = ls0 + QB;
+  float *const dv0 = ls0 + 2 * QB;
+  float *const dv1 = ls0 + 3 * QB;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = lane >> 5, n = lane & 31;
-  const int kq = wave & 3, qs = wave >> 2;     // key quarter, query subtile
+  const int q = wave & 3;                      // SIMD, key quarter, index within the wave's group
+  const bool pwave = wave < 4;
   const int tile = blockIdx.x, kvh = blockIdx.y;
   const int g = p.g, Sq = p.Sq, Hkv = p.Hkv, Hq = Hkv * g, nrows = p.nrows;
   const float c = p.scale_log2;
@@ -711,157 +794,384 @@ __global__ __launch_bounds__(kFastThreads) void dkdv_bf16_kernel(DkdvParams p) {
     dvp = p.dv_self ? (__bf16 *)p.dv_self + base : nullptr;
     st = (int64_t)Hkv * D;
   }
-  const int nk = min(KTB, klen - key0);           // valid keys of this tile (>= 1)
-  const int wkey = kq * 32;                       // wave's first key within the tile
-  const int my_key = wkey + n;                    // lane's key within the tile
+  const int nk = __builtin_amdgcn_readfirstlane(min(KTB, klen - key0));   // valid keys (>= 1)
+  const int my_key = 32 * q + n;               // lane's key within the tile
   const bool key_ok = my_key < nk;
-  const bool wave_has_keys = wkey < nk;
-  const int abs_key = key0 + my_key;              // for the causal test on self keys
-  RowOffsets<D> ro;
-  ro.init(n, G);
-  TrOffsets<D> to;
-  to.init(lane);
+  const int abs_key = key0 + my_key;           // for the causal test on self keys
+  RowOffsets<D> ro0;
+  ro0.init(n, G);
+  RowOffsets<64> rt0;                          // transposed blocks: rows of 64 query slots
+  rt0.init(n, G);
 
-  // Stage this workgroup's K and V once.
+  // K and V of the workgroup's 128 keys, staged through the row buffers (64
+  // keys per buffer), then held in registers as B fragments: K on P waves,
+  // V on dS waves. Halves without keys are zero-filled.
   {
     const int sti = (int)st;
-    dma_tile<D, KTB, kNW>(ktile, kbase + (int64_t)key0 * st, [&](int r) { return r * sti; }, nk, wave, lane);
-    dma_tile<D, KTB, kNW>(vtile, vbase + (int64_t)key0 * st, [&](int r) { return r * sti; }, nk, wave, lane);
-  }
-
-  f32x16 dk[DT], dv[DT];
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt) {
-    dk[dt] = zero16();
-    dv[dt] = zero16();
+    for (int h = 0; h < 2; ++h) {
+      const int nv = min(nk - 64 * h, 64);
+      char *kd = h ? qr1 : qr0;
+      char *vd = h ? or1 : or0;
+      if (nv > 0) {
+        const __bf16 *kb = kbase + (int64_t)(key0 + 64 * h) * st;
+        const __bf16 *vb = vbase + (int64_t)(key0 + 64 * h) * st;
+        dma_tile<D, 64, kNW>(kd, kb, [&](int r) { return r * sti; }, nv, wave, lane);
+        dma_tile<D, 64, kNW>(vd, vb, [&](int r) { return r * sti; }, nv, wave, lane);
+      } else {
+        for (int i = tid; i < RB / 16; i += kFastThreads) {
+          reinterpret_cast<u32x4 *>(kd)[i] = u32x4{0, 0, 0, 0};
+          reinterpret_cast<u32x4 *>(vd)[i] = u32x4{0, 0, 0, 0};
+        }
+      }
+    }
+    wait_vmcnt<0>();
+    lds_barrier();
   }
 
   const int nqb = (nrows + QB - 1) / QB;
   const int qb_first = self ? (key0 * g) / QB : 0;
   const int per_use = nqb - qb_first;
-  const int nblk = per_use * (use_e - use_b);
+  const int nblk = __builtin_amdgcn_readfirstlane(per_use * (use_e - use_b));
 
   auto block_src = [&](int blk, int &b, int &qb) __attribute__((always_inline)) {
     const int u = blk / per_use;
     qb = qb_first + (blk - u * per_use);
     b = self ? self_b : load_const(p.uses, __builtin_amdgcn_readfirstlane(use_b + u));
   };
-  auto issue = [&](int blk, char *qb_l, char *ob_l, float *ls_l, float *dv_l) __attribute__((always_inline)) {
+
+  // --- copies of one block, by the four waves of one group ----------------
+  // Packed row r0 + r of a block is query position (r0+r)/g, head (r0+r)%g of
+  // the group. When g divides 64 every block starts on a position boundary
+  // and a lane's element offset within the block is fixed.
+  const bool g_fast = (QB % g) == 0;
+  constexpr int CPI = D / 8;                   // 16-byte chunks per row
+  constexpr int RPER = QB * CPI / 64 / 4;      // row-block copy instructions per wave
+  int qfix[RPER];
+#pragma unroll
+  for (int i = 0; i < RPER; ++i) {
+    const int pos = (q + 4 * i) * 64 + lane;
+    const int r = pos / CPI;
+    qfix[i] = ((r / g) * Hq + r % g) * D + ((pos % CPI) ^ swz<D>(r)) * 8;
+  }
+  CopyLanes<64, D, 4> ct;                      // transposed blocks: D rows of 64
+  ct.init(q, lane);
+  constexpr int TPER = CopyLanes<64, D, 4>::PER;
+  static_assert(RPER + TPER == NMF / 4, "one copy instruction per four MFMAs");
+  int tvoff[TPER];
+#pragma unroll
+  for (int i = 0; i < TPER; ++i) tvoff[i] = (ct.row[i] * 64 + ct.coff[i]) * 2;
+
+  struct RowJob {
+    BufRsrc rs;
+    int voff[RPER];
+  };
+  // Rows of block blk of Q or dO (blocks past the end: empty resource).
+  auto prep_rows = [&](const void *src, int blk) __attribute__((always_inline)) {
+    RowJob jb;
+    const bool live = blk < nblk;
     int b, qb;
-    block_src(blk, b, qb);
+    block_src(live ? blk : nblk - 1, b, qb);
     const int r0 = qb * QB;
     const int nv = min(QB, nrows - r0);
-    // Packed row r0 + r is query position t = (r0+r)/g, head (r0+r)%g of the
-    // group; offsets are taken from the block's first position.
     const int t0 = r0 / g;
     const int64_t head0 = (((int64_t)b * Sq + t0) * Hq + kvh * g) * D;
+    // Packed row r is at element ((t - t0) Hq + h) D; rows at or beyond nv lie
+    // outside the resource and read as zero.
     auto rowoff = [&](int r) __attribute__((always_inline)) {
       const int rr = r0 + r, t = rr / g;
       return ((t - t0) * Hq + (rr - t * g)) * D;
     };
-    dma_tile<D, QB, kNW>(qb_l, (const __bf16 *)p.q + head0, rowoff, nv, wave, lane);
-    dma_tile<D, QB, kNW>(ob_l, (const __bf16 *)p.d_o + head0, rowoff, nv, wave, lane);
-    if (wave == 0) {
-      // rows >= nrows read a clamped in-range row and are masked in compute
-      const int64_t base = ((int64_t)b * Hkv + kvh) * nrows + r0;
-      dma_f32x64(ls_l, p.lse2 + base, nv, lane);
-      dma_f32x64(dv_l, p.dvec + base, nv, lane);
+    const int last = rowoff(nv - 1) + D;
+    jb.rs = make_rsrc((const __bf16 *)src + head0, live ? last * 2 : 0);
+#pragma unroll
+    for (int i = 0; i < RPER; ++i) {
+      if (g_fast) {
+        jb.voff[i] = qfix[i] * 2;
+      } else {
+        const int pos = (q + 4 * i) * 64 + lane;
+        const int r = pos / CPI;
+        jb.voff[i] = (rowoff(r) + ((pos % CPI) ^ swz<D>(r)) * 8) * 2;
+      }
     }
+    return jb;
   };
-  auto compute = [&](int blk, const char *qb_l, const char *ob_l, const float *ls_l, const float *dv_l) __attribute__((always_inline)) {
-    if (!wave_has_keys) return;
+  auto issue_rows = [&](const RowJob &jb, int i, char *dst) __attribute__((always_inline)) {
+    dma16(jb.rs, jb.voff[i], dst + (q + 4 * i) * 1024);
+  };
+  // Transposed block blk of Q or dO.
+  auto prep_t = [&](const void *src, int blk) __attribute__((always_inline)) {
+    const bool live = blk < nblk;
     int b, qb;
-    block_src(blk, b, qb);
-    (void)b;
+    block_src(live ? blk : nblk - 1, b, qb);
+    const int64_t tb = (((int64_t)b * Hkv + kvh) * nqb + qb) * D * 64;
+    return make_rsrc((const __bf16 *)src + tb, live ? D * 128 : 0);
+  };
+  auto issue_t = [&](BufRsrc rs, int i, char *dst) __attribute__((always_inline)) {
+    dma16(rs, tvoff[i], dst + (q + 4 * i) * 1024);
+  };
+  // LSE2 or D of block blk (64 floats; lanes at or beyond nrows read zero).
+  auto prep_stat = [&](const float *src, int blk) __attribute__((always_inline)) {
+    const bool live = blk < nblk;
+    int b, qb;
+    block_src(live ? blk : nblk - 1, b, qb);
     const int r0 = qb * QB;
-    const int sub_r0 = r0 + 32 * qs;                 // first packed row of this wave's subtile
-    if (sub_r0 >= nrows) return;
-    const int t_hi = (min(sub_r0 + 32, nrows) - 1) / g;
-    if (self && key0 + wkey > t_hi) return;
-    const bool need_mask = (sub_r0 + 32 > nrows) || !key_ok || (self && key0 + wkey + 31 > sub_r0 / g);
-    f32x16 sa = zero16(), dpa = zero16();
+    const int64_t base = ((int64_t)b * Hkv + kvh) * nrows + r0;
+    return make_rsrc(src + base, live ? min(QB, nrows - r0) * 4 : 0);
+  };
+  auto issue_stat = [&](BufRsrc rs, float *dst) __attribute__((always_inline)) {
+    if (q == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t *)dst, 4, lane * 4, 0, 0, 0);
+  };
+  // Waits for all of this wave's copies but the batch issued in the current
+  // matrix phase.
+  auto wait_prev_batch = [&]() __attribute__((always_inline)) {
+    if (q == 0) wait_vmcnt<RPER + TPER + 1>();
+    else wait_vmcnt<RPER + TPER>();
+  };
+
+  // The two roles run separate code (PW: P wave); barriers pair up one to one.
+  auto body = [&](auto PW) __attribute__((always_inline)) {
+    constexpr bool pwave = decltype(PW)::value;
+    // Lane offsets from this role's region (opaque to the compiler, so it
+    // keeps one register per offset and folds each buffer into the immediate).
+    constexpr int RBASE = pwave ? 0 : 4 * RB;
+    RowOffsets<D> ro;
+    RowOffsets<64> rt;
 #pragma unroll
     for (int s = 0; s < NSTEP; ++s) {
-      sa = Mma<__bf16>::run(row_frag_at<D>(qb_l, ro, 32 * qs, s), row_frag_at<D>(ktile, ro, wkey, s), sa);
-      dpa = Mma<__bf16>::run(row_frag_at<D>(ob_l, ro, 32 * qs, s), row_frag_at<D>(vtile, ro, wkey, s), dpa);
+      ro.off[s] = ro0.off[s] + RBASE;
+      asm volatile("" : "+v"(ro.off[s]));
     }
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int ql = 32 * qs + crow(j, G);           // query row within the block
-      float pv = fast_exp2(fmaf(sa[j], c, -ls_l[ql]));
-      if (need_mask) {
-        const int rr = r0 + ql;
-        bool ok = key_ok && rr < nrows;
-        if (self) ok = ok && abs_key <= rr / g;
-        pv = ok ? pv : 0.0f;
+    for (int s = 0; s < 4; ++s) {
+      rt.off[s] = rt0.off[s] + RBASE;
+      asm volatile("" : "+v"(rt.off[s]));
+    }
+    auto rel = [&](const char *buf) __attribute__((always_inline)) { return buf - RBASE; };
+    bf16x8 kv[NSTEP];
+    {
+      const char *src = pwave ? ((q >> 1) ? qr1 : qr0) : ((q >> 1) ? or1 : or0);
+#pragma unroll
+      for (int s = 0; s < NSTEP; ++s) kv[s] = row_frag_at<D>(rel(src), ro, 32 * (q & 1), s);
+      lds_barrier();
+    }
+    f32x16 acc[DT];                              // dV^T (P waves) or dK^T (dS waves): [channel][key]
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) acc[dt] = zero16();
+    f32x16 sp[2];                                // S (P waves) or dP (dS waves) of both 32-row subtiles
+    bf16x8 pk[4];                                // P (P waves) or dS (dS waves), k-step 2 sub + h
+
+    // Matrix phase: 2 NSTEP MFMAs on row fragments of `rows` (S or dP of the
+    // next block) and 2 NSTEP on transposed fragments of `tr` times pk (dV or
+    // dK of this block); TR_FIRST puts the transposed product first. One LDS
+    // fragment per MFMA, LEAD fragments ahead; copy piece k/4 after MFMA k
+    // when k % 4 == 3.
+    auto matrix = [&](auto TR_FIRST, const char *rows, const char *tr, auto &&piece) __attribute__((always_inline)) {
+      constexpr bool TF = decltype(TR_FIRST)::value;
+      constexpr int H = 2 * NSTEP;
+      auto frag = [&](auto K) __attribute__((always_inline)) {
+        constexpr int k = decltype(K)::value;
+        constexpr bool is_tr = TF ? (k < H) : (k >= H);
+        constexpr int kk = TF ? (k < H ? k : k - H) : (k < H ? k : k - H);
+        if constexpr (is_tr) return row_frag_at<64>(tr, rt, 32 * (kk / 4), kk % 4);
+        else return row_frag_at<D>(rows, ro, 32 * (kk / NSTEP), kk % NSTEP);
+      };
+      sp[0] = zero16();
+      sp[1] = zero16();
+      bf16x8 ring[RING];
+      static_for<LEAD>([&](auto K) __attribute__((always_inline)) { ring[decltype(K)::value] = frag(K); });
+      static_for<NMF>([&](auto K) __attribute__((always_inline)) {
+        constexpr int k = decltype(K)::value;
+        constexpr bool is_tr = TF ? (k < H) : (k >= H);
+        constexpr int kk = k < H ? k : k - H;
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (k + LEAD < NMF) ring[(k + LEAD) % RING] = frag(std::integral_constant<int, k + LEAD>{});
+        if constexpr (is_tr) acc[kk / 4] = Mma<__bf16>::run(ring[k % RING], pk[kk % 4], acc[kk / 4]);
+        else sp[kk / NSTEP] = Mma<__bf16>::run(ring[k % RING], kv[kk % NSTEP], sp[kk / NSTEP]);
+        if constexpr ((k & 3) == 3) piece(k >> 2);
+      });
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    // S or dP of block 0 alone (prologue).
+    auto first_rows = [&](const char *rows) __attribute__((always_inline)) {
+      sp[0] = zero16();
+      sp[1] = zero16();
+#pragma unroll
+      for (int s = 0; s < NSTEP; ++s) {
+        sp[0] = Mma<__bf16>::run(row_frag_at<D>(rows, ro, 0, s), kv[s], sp[0]);
+        sp[1] = Mma<__bf16>::run(row_frag_at<D>(rows, ro, 32, s), kv[s], sp[1]);
       }
-      sa[j] = pv;
-      dpa[j] = pv * (dpa[j] - dv_l[ql]);
-    }
+    };
+    char *const xme = xch + q * 4096 + lane * 16;   // this lane's P slots (4 x 16 bytes, 1 KiB apart)
+
+    // P wave VALU phase: P of block blk from sp (S) and its LSE2 in lsb; packed
+    // into pk and published to the SIMD's dS wave.
+    auto p_valu = [&](auto CAUSAL, int blk, const float *lsb) __attribute__((always_inline)) {
+      constexpr bool CA = decltype(CAUSAL)::value;
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      const bf16x8 pf = pack_bf16x8(sa, s), dsf = pack_bf16x8(dpa, s);
+      for (int sub = 0; sub < 2; ++sub) {
+        int lo = 0;
+        if constexpr (CA) {
+          int b, qb;
+          block_src(blk, b, qb);
+          (void)b;
+          lo = abs_key * g - (qb * QB + 32 * sub) - 4 * G;   // rows at or after the key's position
+        }
+        f32x4 lsv[4];
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        dv[dt] = Mma<__bf16>::run(tr_frag_at<D>(ob_l, to, 32 * qs + 16 * s, dt), pf, dv[dt]);
-        dk[dt] = Mma<__bf16>::run(tr_frag_at<D>(qb_l, to, 32 * qs + 16 * s, dt), dsf, dk[dt]);
+        for (int k = 0; k < 4; ++k) lsv[k] = *reinterpret_cast<const f32x4 *>(lsb + 32 * sub + 8 * k + 4 * G);
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          float pv = fast_exp2(fmaf(sp[sub][j], c, -lsv[j >> 2][j & 3]));
+          if constexpr (CA) pv = crow(j, 0) >= lo ? pv : 0.0f;
+          sp[sub][j] = pv;
+        }
+        pk[2 * sub] = pack_bf16x8(sp[sub], 0);
+        pk[2 * sub + 1] = pack_bf16x8(sp[sub], 1);
       }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) *reinterpret_cast<bf16x8 *>(xme + t * 1024) = pk[t];
+    };
+    // dS wave VALU phase: dS of a block from the published P, sp (dP) and D in dvb.
+    auto ds_valu = [&](const float *dvb) __attribute__((always_inline)) {
+      bf16x8 pv[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) pv[t] = *reinterpret_cast<const bf16x8 *>(xme + t * 1024);
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub) {
+        f32x4 dvv[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) dvv[k] = *reinterpret_cast<const f32x4 *>(dvb + 32 * sub + 8 * k + 4 * G);
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          sp[sub][j] = (float)pv[2 * sub + (j >> 3)][j & 7] * (sp[sub][j] - dvv[j >> 2][j & 3]);
+        pk[2 * sub] = pack_bf16x8(sp[sub], 0);
+        pk[2 * sub + 1] = pack_bf16x8(sp[sub], 1);
+      }
+    };
+
+    // P wave, block i (A_i then B_i). Buffers: rows of i+1 (qrn), dO^T_i (ot);
+    // copies into orw (dO rows of i+2), qtw (Q^T_{i+1}), lsw (LSE2 of i+2);
+    // LSE2 of i+1 in lsn.
+    auto p_step = [&](auto CAUSAL, int i, const char *qrn, const char *ot, char *orw, char *qtw, float *lsw,
+                      const float *lsn) __attribute__((always_inline)) {
+      const RowJob rj = prep_rows(p.d_o, i + 2);
+      const BufRsrc tj = prep_t(p.qT, i + 1);
+      const BufRsrc sj = prep_stat(p.lse2, i + 2);
+      __builtin_amdgcn_s_waitcnt(0xC07F);   // scalar loads done: exact LDS counts below
+      matrix(std::false_type{}, rel(qrn), rel(ot), [&](int k) __attribute__((always_inline)) {
+        if (k < RPER) issue_rows(rj, k, orw);
+        else issue_t(tj, k - RPER, qtw);
+        if (k == 0) issue_stat(sj, lsw);
+      });
+      wait_prev_batch();
+      lds_barrier();
+      p_valu(CAUSAL, i + 1, lsn);
+      lds_barrier();
+    };
+    // dS wave, block i (A_i then B_i). Buffers: D_i (dvb), Q^T_i (qt), dO rows
+    // of i+1 (orn); copies into qrw (Q rows of i+3), otw (dO^T_{i+2}), dvw (D
+    // of i+2).
+    auto ds_step = [&](int i, const float *dvb, const char *qt, const char *orn, char *qrw, char *otw,
+                       float *dvw) __attribute__((always_inline)) {
+      ds_valu(dvb);
+      lds_barrier();
+      const RowJob rj = prep_rows(p.q, i + 3);
+      const BufRsrc tj = prep_t(p.doT, i + 2);
+      const BufRsrc sj = prep_stat(p.dvec, i + 2);
+      __builtin_amdgcn_s_waitcnt(0xC07F);
+      matrix(std::true_type{}, rel(orn), rel(qt), [&](int k) __attribute__((always_inline)) {
+        if (k < RPER) issue_rows(rj, k, qrw);
+        else issue_t(tj, k - RPER, otw);
+        if (k == 0) issue_stat(sj, dvw);
+      });
+      wait_prev_batch();
+      lds_barrier();
+    };
+
+    if (nblk > 0) {
+      // Blocks 0 and 1: rows of 0 and 1, Q^T_0 / dO^T_0, LSE2 of 0 and 1, D_0.
+      if constexpr (pwave) {
+        RowJob rj = prep_rows(p.q, 0);
+#pragma unroll
+        for (int k = 0; k < RPER; ++k) issue_rows(rj, k, qr0);
+        rj = prep_rows(p.q, 1);
+#pragma unroll
+        for (int k = 0; k < RPER; ++k) issue_rows(rj, k, qr1);
+        const BufRsrc tj = prep_t(p.qT, 0);
+#pragma unroll
+        for (int k = 0; k < TPER; ++k) issue_t(tj, k, qt0);
+        issue_stat(prep_stat(p.lse2, 0), ls0);
+        issue_stat(prep_stat(p.lse2, 1), ls1);
+      } else {
+        RowJob rj = prep_rows(p.d_o, 0);
+#pragma unroll
+        for (int k = 0; k < RPER; ++k) issue_rows(rj, k, or0);
+        rj = prep_rows(p.d_o, 1);
+#pragma unroll
+        for (int k = 0; k < RPER; ++k) issue_rows(rj, k, or1);
+        const BufRsrc tj = prep_t(p.doT, 0);
+#pragma unroll
+        for (int k = 0; k < TPER; ++k) issue_t(tj, k, ot0);
+        issue_stat(prep_stat(p.dvec, 0), dv0);
+      }
+      wait_vmcnt<0>();
+      lds_barrier();
+      if constexpr (pwave) {
+        auto run = [&](auto CAUSAL) __attribute__((always_inline)) {
+          // Distinct markers keep the compiler from hoisting the two variants'
+          // common first loads above the branch (they would stay live across
+          // the other variant's loop).
+          if constexpr (decltype(CAUSAL)::value) asm volatile("; causal tiles" ::: "memory");
+          else asm volatile("; prefix tiles" ::: "memory");
+          first_rows(rel(qr0));
+          p_valu(CAUSAL, 0, ls0);
+          lds_barrier();
+          for (int i = 0; i < nblk; i += 2) {
+            p_step(CAUSAL, i, qr1, ot0, or0, qt1, ls0, ls1);
+            if (i + 1 >= nblk) break;
+            p_step(CAUSAL, i + 1, qr0, ot1, or1, qt0, ls1, ls0);
+          }
+        };
+        if (self) run(std::true_type{});
+        else run(std::false_type{});
+      } else {
+        first_rows(rel(or0));
+        lds_barrier();
+        // Copies that a B_{-1} phase would have issued: Q rows of 2, dO^T_1, D_1.
+        {
+          const RowJob rj = prep_rows(p.q, 2);
+#pragma unroll
+          for (int k = 0; k < RPER; ++k) issue_rows(rj, k, qr0);
+          const BufRsrc tj = prep_t(p.doT, 1);
+#pragma unroll
+          for (int k = 0; k < TPER; ++k) issue_t(tj, k, ot1);
+          issue_stat(prep_stat(p.dvec, 1), dv1);
+        }
+        for (int i = 0; i < nblk; i += 2) {
+          ds_step(i, dv0, qt0, or1, qr1, ot0, dv0);
+          if (i + 1 >= nblk) break;
+          ds_step(i + 1, dv1, qt1, or0, qr0, ot1, dv1);
+        }
+      }
+      wait_vmcnt<0>();
     }
+
+    if (!key_ok) return;
+    __bf16 *dst = pwave ? dvp : dkp;
+    if (!dst) return;
+    const float sc = pwave ? 1.0f : p.scale;
+    const int64_t krow = (int64_t)(key0 + my_key) * st;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+        store4(dst + krow + dt * 32 + jj * 8 + G * 4, acc[dt][jj * 4 + 0] * sc, acc[dt][jj * 4 + 1] * sc,
+               acc[dt][jj * 4 + 2] * sc, acc[dt][jj * 4 + 3] * sc);
+
   };
-
-  if (nblk > 0) {
-    issue(0, qb0, ob0, ls0, dv0);
-    __syncthreads();
-    for (int blk = 0; blk < nblk; blk += 2) {
-      const bool has1 = blk + 1 < nblk;
-      if (has1) issue(blk + 1, qb1, ob1, ls1, dv1);
-      compute(blk, qb0, ob0, ls0, dv0);
-      __syncthreads();
-      if (!has1) break;
-      if (blk + 2 < nblk) issue(blk + 2, qb0, ob0, ls0, dv0);
-      compute(blk + 1, qb1, ob1, ls1, dv1);
-      __syncthreads();
-    }
-  } else {
-    __syncthreads();
-  }
-
-  // Pairwise reduction: waves 4..7 hand their sums to waves 0..3 through the
-  // K tile, which is no longer read: PD accumulators of 4 waves per pass.
-  constexpr int PD = KVB / (4 * 64 * 16 * 4);
-  static_assert(PD >= 1 && DT % PD == 0, "reduction pass size");
-  float *red = reinterpret_cast<float *>(ktile);
-#pragma unroll
-  for (int pass = 0; pass < 2 * (DT / PD); ++pass) {
-    f32x16 *acc = pass < DT / PD ? dk : dv;
-    const int d0 = (pass % (DT / PD)) * PD;
-    if (qs == 1) {
-#pragma unroll
-      for (int i = 0; i < PD; ++i)
-        *reinterpret_cast<f32x16 *>(red + ((kq * PD + i) * 64 + lane) * 16) = acc[d0 + i];
-    }
-    __syncthreads();
-    if (qs == 0) {
-#pragma unroll
-      for (int i = 0; i < PD; ++i)
-        acc[d0 + i] += *reinterpret_cast<const f32x16 *>(red + ((kq * PD + i) * 64 + lane) * 16);
-    }
-    __syncthreads();
-  }
-  if (qs != 0 || !key_ok) return;
-  const float sc = p.scale;
-  const int64_t krow = (int64_t)(key0 + my_key) * st;
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      const int d0 = dt * 32 + jj * 8 + G * 4;
-      if (dkp)
-        store4(dkp + krow + d0, dk[dt][jj * 4 + 0] * sc, dk[dt][jj * 4 + 1] * sc, dk[dt][jj * 4 + 2] * sc,
-               dk[dt][jj * 4 + 3] * sc);
-      if (dvp)
-        store4(dvp + krow + d0, dv[dt][jj * 4 + 0], dv[dt][jj * 4 + 1], dv[dt][jj * 4 + 2], dv[dt][jj * 4 + 3]);
-    }
+  if (pwave) body(std::true_type{});
+  else body(std::false_type{});
 }
 
 hipError_t launch_fwd_bf16(const FwdParams &p, int D, hipStream_t s) {
@@ -890,6 +1200,15 @@ hipError_t launch_dkdv_bf16(const DkdvParams &p, int D, int gx, hipStream_t s) {
     hipLaunchKernelGGL(dkdv_bf16_kernel<64>, dim3((unsigned)gx, (unsigned)p.Hkv), dim3(kFastThreads), 0, s, p);
   else
     hipLaunchKernelGGL(dkdv_bf16_kernel<128>, dim3((unsigned)gx, (unsigned)p.Hkv), dim3(kFastThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_transpose_bf16(const PreParams &p, int D, hipStream_t s) {
+  const int64_t grid = (int64_t)p.B * p.Hkv * p.nqb;
+  if (D == 64)
+    hipLaunchKernelGGL(bwd_transpose_bf16_kernel<64>, dim3((unsigned)grid), dim3(256), 0, s, p);
+  else
+    hipLaunchKernelGGL(bwd_transpose_bf16_kernel<128>, dim3((unsigned)grid), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

@@ -275,9 +275,10 @@ __device__ __forceinline__ void dma16(BufRsrc rs, int byte_off, char *lds) {
 }
 
 // Asynchronous copy of R rows into a swizzled tile, shared by NW waves: row r
-// starts rowoff(r) elements after base (rowoff increases with r and stays in
-// 32 bits). Rows at or beyond nvalid (>= 1) re-read row nvalid-1, which is
-// finite; callers mask those rows. Completion: s_waitcnt vmcnt + barrier.
+// starts rowoff(r) elements after base (rowoff increases by at least D per
+// row and stays in 32 bits). The buffer resource ends after row nvalid-1
+// (>= 1), so rows at or beyond nvalid read as zero. Completion: s_waitcnt
+// vmcnt + barrier.
 template <int D, int R, int NW, typename RowOff>
 __device__ __forceinline__ void dma_tile(char *tile, const __bf16 *base, RowOff rowoff, int nvalid, int wave,
                                          int lane) {
@@ -288,15 +289,15 @@ __device__ __forceinline__ void dma_tile(char *tile, const __bf16 *base, RowOff 
     const int pos = inst * 64 + lane;
     const int r = pos / CPR;
     const int c = (pos % CPR) ^ swz<D>(r);
-    dma16(rs, (rowoff(r < nvalid ? r : nvalid - 1) + c * 8) * 2, tile + inst * 1024);
+    dma16(rs, (rowoff(r) + c * 8) * 2, tile + inst * 1024);
   }
 }
 
 // Asynchronous copy of 64 consecutive floats (one wave instruction); lanes at
-// or beyond n (>= 1) re-read element n-1.
-__device__ __forceinline__ void dma_f32x64(float *dst, const float *src, int n, int lane) {
+// or beyond n read zero.
+__device__ __forceinline__ void dma_f32x64_zero(float *dst, const float *src, int n, int lane) {
   const BufRsrc rs = make_rsrc(src, n * 4);
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t *)dst, 4, min(lane, n - 1) * 4, 0, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t *)dst, 4, lane * 4, 0, 0, 0);
 }
 
 // Per-lane byte offsets into swizzled tiles. swz(r) is unchanged when r moves

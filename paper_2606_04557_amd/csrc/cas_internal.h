@@ -97,7 +97,10 @@ struct PreParams {
   const float *lse;
   float *dvec;   // [B][Hkv][nrows]  rowsum(dO * O)
   float *lse2;   // [B][Hkv][nrows]  LSE * log2(e)
-  int32_t B, Sq, Hkv, g, nrows;
+  const void *q;
+  void *qT;      // bf16: [B][Hkv][nqb][D][64] Q of each 64-row block, transposed
+  void *doT;     // bf16: same for dO
+  int32_t B, Sq, Hkv, g, nrows, nqb;
 };
 
 struct DqParams {
@@ -131,6 +134,8 @@ struct DkdvParams {
   const void *d_o;
   const float *dvec;
   const float *lse2;
+  const void *qT;           // bf16: transposed Q / dO blocks (see PreParams)
+  const void *doT;
   void *dk_self;
   void *dv_self;
   const DevCart *carts;
@@ -155,5 +160,6 @@ constexpr int kBf16RowsPerWg = 256;
 hipError_t launch_fwd_bf16(const FwdParams &p, int D, hipStream_t s);
 hipError_t launch_dq_bf16(const DqParams &p, int D, hipStream_t s);
 hipError_t launch_dkdv_bf16(const DkdvParams &p, int D, int grid_x, hipStream_t s);
+hipError_t launch_bwd_transpose_bf16(const PreParams &p, int D, hipStream_t s);
 
 }  // namespace cas
