@@ -23,7 +23,10 @@ constexpr int kFastRowsPerWg = kNW * kFastRowsPerWave;   // 256
 #ifndef CAS_DKDV_LEAD
 #define CAS_DKDV_LEAD 4
 #endif
-constexpr int kDkdvLead = CAS_DKDV_LEAD;  // dK/dV: LDS fragments in flight ahead of their MFMA
+constexpr int kDkdvLead = CAS_DKDV_LEAD;
+#ifndef CAS_DKDV_PRIO
+#define CAS_DKDV_PRIO 1
+#endif  // dK/dV: LDS fragments in flight ahead of their MFMA
 constexpr float kRefMargin = 64.0f;    // forward: largest score above the row's fixed offset (log2 units)
 
 struct TileInfo {
@@ -88,6 +91,14 @@ struct CopyLanes {
     }
   }
 };
+
+// Pins register values at this point: the compiler may not move their
+// computation past it (e.g. across a barrier into the next phase).
+template <typename T, int N>
+__device__ __forceinline__ void fence_regs(T (&v)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(v[i]));
+}
 
 // Workgroup barrier that orders LDS use: this wave's LDS reads have returned,
 // and the compiler moves no memory access across it. Outstanding direct
@@ -712,19 +723,21 @@ __global__ __launch_bounds__(256) void bwd_transpose_bf16_kernel(PreParams p) {
 // the transposed blocks Q^T and dO^T (written by the backward prologue) for
 // the dK and dV products.
 //
-// Copies (LDS double buffers), one instruction per four MFMAs of the issuing
-// wave's matrix phase: P waves issue dO rows of block i+2, Q^T_{i+1} and LSE2
-// of i+2 during A_i; dS waves issue Q rows of block i+3, dO^T_{i+2} and D of
-// i+2 during B_i. A wave waits for a batch at the end of its next matrix
-// phase. Copies for blocks past the end use an empty buffer resource (they
-// write zeros that nothing reads), so every batch has the same size.
+// Copies (LDS double buffers) are issued in VALU phases, interleaved with the
+// VALU work, so the matrix phases are MFMAs and LDS reads only: P waves issue
+// dO rows of block i+2, Q^T_{i+1} and LSE2 of i+2 during B_i; dS waves issue
+// Q rows of block i+2, dO^T_{i+1} and D of i+1 during A_i. A wave waits for
+// its batch at the end of its next matrix phase. The copy addresses (with
+// their segment-table loads) are prepared one VALU phase ahead. Copies for
+// blocks past the end use an empty buffer resource (they write zeros that
+// nothing reads).
 //
 // P needs no mask for keys beyond the tile (their dK / dV columns are never
 // stored) or rows beyond nrows (Q, dO, Q^T, dO^T, LSE2 and D all read as
 // zero there: P = 1 and dS = 0 add nothing). On self keys P = 0 for rows
 // before the key's position.
 // ---------------------------------------------------------------------------
-template <int D>
+template <int D, bool GFAST>
 __global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void dkdv_bf16_kernel(DkdvParams p) {
   constexpr int NSTEP = D / 16;
@@ -734,6 +747,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
   constexpr int RB = QB * D * 2;               // bytes of one 64 x D block
   constexpr int NMF = 4 * NSTEP;               // MFMAs of a wave's matrix phase
   constexpr int LEAD = kDkdvLead, RING = LEAD + 1;
+  constexpr int PRIO = CAS_DKDV_PRIO;          // wave priority during a matrix phase
   // One LDS arena. The P waves' matrix operands (Q rows, dO^T) fill the first
   // 4 RB bytes and the dS waves' (dO rows, Q^T) the next 4 RB, so each wave
   // reaches all of its fragments from one set of lane offsets plus 16-bit
@@ -834,17 +848,42 @@ void dkdv_bf16_kernel(DkdvParams p) {
   const int per_use = nqb - qb_first;
   const int nblk = __builtin_amdgcn_readfirstlane(per_use * (use_e - use_b));
 
-  auto block_src = [&](int blk, int &b, int &qb) __attribute__((always_inline)) {
-    const int u = blk / per_use;
-    qb = qb_first + (blk - u * per_use);
-    b = self ? self_b : load_const(p.uses, __builtin_amdgcn_readfirstlane(use_b + u));
+  // Block cursor: block blk of the workgroup's sequence is 64-row block
+  // qb_first + r of batch row b = uses[u] (r = blk mod per_use). Blocks past
+  // the end keep the last block's (b, r) and are not copied.
+  struct Cursor {
+    int blk, r, u, b;
+  };
+  auto use_row = [&](int u) __attribute__((always_inline)) {
+    int b = self ? self_b : load_const(p.uses, __builtin_amdgcn_readfirstlane(use_b + u));
+    // The table load is invariant, so the compiler could sink it (and its
+    // latency) past a barrier into a matrix phase; this pins it here.
+    asm volatile("" : "+s"(b));
+    return b;
+  };
+  auto cursor_at = [&](int blk) __attribute__((always_inline)) {
+    Cursor c;
+    c.blk = blk;
+    const int bl = min(blk, nblk - 1);
+    c.u = bl / per_use;
+    c.r = bl - c.u * per_use;
+    c.b = use_row(c.u);
+    return c;
+  };
+  auto advance = [&](Cursor &c) __attribute__((always_inline)) {
+    ++c.blk;
+    if (c.blk < nblk) {
+      if (++c.r == per_use) {
+        c.r = 0;
+        c.b = use_row(++c.u);
+      }
+    }
   };
 
   // --- copies of one block, by the four waves of one group ----------------
   // Packed row r0 + r of a block is query position (r0+r)/g, head (r0+r)%g of
-  // the group. When g divides 64 every block starts on a position boundary
-  // and a lane's element offset within the block is fixed.
-  const bool g_fast = (QB % g) == 0;
+  // the group. When g divides 64 (GFAST) every block starts on a position
+  // boundary and a lane's element offset within the block is fixed.
   constexpr int CPI = D / 8;                   // 16-byte chunks per row
   constexpr int RPER = QB * CPI / 64 / 4;      // row-block copy instructions per wave
   int qfix[RPER];
@@ -857,7 +896,8 @@ void dkdv_bf16_kernel(DkdvParams p) {
   CopyLanes<64, D, 4> ct;                      // transposed blocks: D rows of 64
   ct.init(q, lane);
   constexpr int TPER = CopyLanes<64, D, 4>::PER;
-  static_assert(RPER + TPER == NMF / 4, "one copy instruction per four MFMAs");
+  constexpr int NPIECE = RPER + TPER;          // copy instructions per wave per block (+ statistics)
+  static_assert(32 % NPIECE == 0, "copy pieces spread over the 32 VALU elements");
   int tvoff[TPER];
 #pragma unroll
   for (int i = 0; i < TPER; ++i) tvoff[i] = (ct.row[i] * 64 + ct.coff[i]) * 2;
@@ -866,29 +906,34 @@ void dkdv_bf16_kernel(DkdvParams p) {
     BufRsrc rs;
     int voff[RPER];
   };
-  // Rows of block blk of Q or dO (blocks past the end: empty resource).
-  auto prep_rows = [&](const void *src, int blk) __attribute__((always_inline)) {
+  // Rows of the cursor's block of Q or dO (blocks past the end: empty resource).
+  auto prep_rows = [&](const void *src, const Cursor &c) __attribute__((always_inline)) {
     RowJob jb;
-    const bool live = blk < nblk;
-    int b, qb;
-    block_src(live ? blk : nblk - 1, b, qb);
-    const int r0 = qb * QB;
-    const int nv = min(QB, nrows - r0);
-    const int t0 = r0 / g;
-    const int64_t head0 = (((int64_t)b * Sq + t0) * Hq + kvh * g) * D;
-    // Packed row r is at element ((t - t0) Hq + h) D; rows at or beyond nv lie
-    // outside the resource and read as zero.
-    auto rowoff = [&](int r) __attribute__((always_inline)) {
-      const int rr = r0 + r, t = rr / g;
-      return ((t - t0) * Hq + (rr - t * g)) * D;
-    };
-    const int last = rowoff(nv - 1) + D;
-    jb.rs = make_rsrc((const __bf16 *)src + head0, live ? last * 2 : 0);
+    const bool live = c.blk < nblk;
+    const int b = c.b, r0 = (qb_first + c.r) * QB;
+    if constexpr (GFAST) {
+      // The block starts at position t0 = r0 / g; rows at or beyond nrows are
+      // positions >= Sq, which lie past the group's last row at Sq - 1.
+      const int t0 = (qb_first + c.r) * (QB / g);
+      const int64_t head0 = (((int64_t)b * Sq + t0) * Hq + kvh * g) * D;
+      const int64_t lim = ((int64_t)(Sq - 1 - t0) * Hq + g) * D * 2;
+      jb.rs = make_rsrc((const __bf16 *)src + head0, live ? (int)min(lim, (int64_t)0x7fffffff) : 0);
 #pragma unroll
-    for (int i = 0; i < RPER; ++i) {
-      if (g_fast) {
-        jb.voff[i] = qfix[i] * 2;
-      } else {
+      for (int i = 0; i < RPER; ++i) jb.voff[i] = qfix[i] * 2;
+    } else {
+      const int nv = min(QB, nrows - r0);
+      const int t0 = r0 / g;
+      const int64_t head0 = (((int64_t)b * Sq + t0) * Hq + kvh * g) * D;
+      // Packed row r is at element ((t - t0) Hq + h) D; rows at or beyond nv
+      // lie outside the resource and read as zero.
+      auto rowoff = [&](int r) __attribute__((always_inline)) {
+        const int rr = r0 + r, t = rr / g;
+        return ((t - t0) * Hq + (rr - t * g)) * D;
+      };
+      const int last = rowoff(nv - 1) + D;
+      jb.rs = make_rsrc((const __bf16 *)src + head0, live ? last * 2 : 0);
+#pragma unroll
+      for (int i = 0; i < RPER; ++i) {
         const int pos = (q + 4 * i) * 64 + lane;
         const int r = pos / CPI;
         jb.voff[i] = (rowoff(r) + ((pos % CPI) ^ swz<D>(r)) * 8) * 2;
@@ -899,34 +944,24 @@ void dkdv_bf16_kernel(DkdvParams p) {
   auto issue_rows = [&](const RowJob &jb, int i, char *dst) __attribute__((always_inline)) {
     dma16(jb.rs, jb.voff[i], dst + (q + 4 * i) * 1024);
   };
-  // Transposed block blk of Q or dO.
-  auto prep_t = [&](const void *src, int blk) __attribute__((always_inline)) {
-    const bool live = blk < nblk;
-    int b, qb;
-    block_src(live ? blk : nblk - 1, b, qb);
-    const int64_t tb = (((int64_t)b * Hkv + kvh) * nqb + qb) * D * 64;
+  // Transposed block of Q or dO.
+  auto prep_t = [&](const void *src, const Cursor &c) __attribute__((always_inline)) {
+    const bool live = c.blk < nblk;
+    const int64_t tb = (((int64_t)c.b * Hkv + kvh) * nqb + qb_first + c.r) * D * 64;
     return make_rsrc((const __bf16 *)src + tb, live ? D * 128 : 0);
   };
   auto issue_t = [&](BufRsrc rs, int i, char *dst) __attribute__((always_inline)) {
     dma16(rs, tvoff[i], dst + (q + 4 * i) * 1024);
   };
-  // LSE2 or D of block blk (64 floats; lanes at or beyond nrows read zero).
-  auto prep_stat = [&](const float *src, int blk) __attribute__((always_inline)) {
-    const bool live = blk < nblk;
-    int b, qb;
-    block_src(live ? blk : nblk - 1, b, qb);
-    const int r0 = qb * QB;
-    const int64_t base = ((int64_t)b * Hkv + kvh) * nrows + r0;
+  // LSE2 or D (64 floats; lanes at or beyond nrows read zero).
+  auto prep_stat = [&](const float *src, const Cursor &c) __attribute__((always_inline)) {
+    const bool live = c.blk < nblk;
+    const int r0 = (qb_first + c.r) * QB;
+    const int64_t base = ((int64_t)c.b * Hkv + kvh) * nrows + r0;
     return make_rsrc(src + base, live ? min(QB, nrows - r0) * 4 : 0);
   };
   auto issue_stat = [&](BufRsrc rs, float *dst) __attribute__((always_inline)) {
     if (q == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t *)dst, 4, lane * 4, 0, 0, 0);
-  };
-  // Waits for all of this wave's copies but the batch issued in the current
-  // matrix phase.
-  auto wait_prev_batch = [&]() __attribute__((always_inline)) {
-    if (q == 0) wait_vmcnt<RPER + TPER + 1>();
-    else wait_vmcnt<RPER + TPER>();
   };
 
   // The two roles run separate code (PW: P wave); barriers pair up one to one.
@@ -964,9 +999,8 @@ void dkdv_bf16_kernel(DkdvParams p) {
     // Matrix phase: 2 NSTEP MFMAs on row fragments of `rows` (S or dP of the
     // next block) and 2 NSTEP on transposed fragments of `tr` times pk (dV or
     // dK of this block); TR_FIRST puts the transposed product first. One LDS
-    // fragment per MFMA, LEAD fragments ahead; copy piece k/4 after MFMA k
-    // when k % 4 == 3.
-    auto matrix = [&](auto TR_FIRST, const char *rows, const char *tr, auto &&piece) __attribute__((always_inline)) {
+    // fragment per MFMA, LEAD fragments ahead.
+    auto matrix = [&](auto TR_FIRST, const char *rows, const char *tr) __attribute__((always_inline)) {
       constexpr bool TF = decltype(TR_FIRST)::value;
       constexpr int H = 2 * NSTEP;
       auto frag = [&](auto K) __attribute__((always_inline)) {
@@ -978,6 +1012,9 @@ void dkdv_bf16_kernel(DkdvParams p) {
       };
       sp[0] = zero16();
       sp[1] = zero16();
+      // The SIMD's other wave is in its VALU phase: let this wave's MFMA
+      // stream issue first.
+      __builtin_amdgcn_s_setprio(PRIO);
       bf16x8 ring[RING];
       static_for<LEAD>([&](auto K) __attribute__((always_inline)) { ring[decltype(K)::value] = frag(K); });
       static_for<NMF>([&](auto K) __attribute__((always_inline)) {
@@ -988,9 +1025,9 @@ void dkdv_bf16_kernel(DkdvParams p) {
         if constexpr (k + LEAD < NMF) ring[(k + LEAD) % RING] = frag(std::integral_constant<int, k + LEAD>{});
         if constexpr (is_tr) acc[kk / 4] = Mma<__bf16>::run(ring[k % RING], pk[kk % 4], acc[kk / 4]);
         else sp[kk / NSTEP] = Mma<__bf16>::run(ring[k % RING], kv[kk % NSTEP], sp[kk / NSTEP]);
-        if constexpr ((k & 3) == 3) piece(k >> 2);
       });
       __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_setprio(0);
     };
     // S or dP of block 0 alone (prologue).
     auto first_rows = [&](const char *rows) __attribute__((always_inline)) {
@@ -1005,17 +1042,16 @@ void dkdv_bf16_kernel(DkdvParams p) {
     char *const xme = xch + q * 4096 + lane * 16;   // this lane's P slots (4 x 16 bytes, 1 KiB apart)
 
     // P wave VALU phase: P of block blk from sp (S) and its LSE2 in lsb; packed
-    // into pk and published to the SIMD's dS wave.
-    auto p_valu = [&](auto CAUSAL, int blk, const float *lsb) __attribute__((always_inline)) {
+    // into pk and published to the SIMD's dS wave. piece(n) issues copy
+    // instruction n, spread over the elements.
+    auto p_valu = [&](auto CAUSAL, int blk, const float *lsb, auto &&piece) __attribute__((always_inline)) {
       constexpr bool CA = decltype(CAUSAL)::value;
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub) {
         int lo = 0;
         if constexpr (CA) {
-          int b, qb;
-          block_src(blk, b, qb);
-          (void)b;
-          lo = abs_key * g - (qb * QB + 32 * sub) - 4 * G;   // rows at or after the key's position
+          // self tiles have a single use: block blk is 64-row block qb_first + blk
+          lo = abs_key * g - ((qb_first + blk) * QB + 32 * sub) - 4 * G;   // rows at or after the key's position
         }
         f32x4 lsv[4];
 #pragma unroll
@@ -1025,15 +1061,19 @@ void dkdv_bf16_kernel(DkdvParams p) {
           float pv = fast_exp2(fmaf(sp[sub][j], c, -lsv[j >> 2][j & 3]));
           if constexpr (CA) pv = crow(j, 0) >= lo ? pv : 0.0f;
           sp[sub][j] = pv;
+          constexpr int EPP = 32 / NPIECE;   // elements per copy piece
+          if ((16 * sub + j) % EPP == EPP - 1) piece((16 * sub + j) / EPP);
         }
         pk[2 * sub] = pack_bf16x8(sp[sub], 0);
         pk[2 * sub + 1] = pack_bf16x8(sp[sub], 1);
       }
 #pragma unroll
       for (int t = 0; t < 4; ++t) *reinterpret_cast<bf16x8 *>(xme + t * 1024) = pk[t];
+      fence_regs(pk);
     };
-    // dS wave VALU phase: dS of a block from the published P, sp (dP) and D in dvb.
-    auto ds_valu = [&](const float *dvb) __attribute__((always_inline)) {
+    // dS wave VALU phase: dS of a block from the published P, sp (dP) and D in
+    // dvb; piece(n) as for the P wave.
+    auto ds_valu = [&](const float *dvb, auto &&piece) __attribute__((always_inline)) {
       bf16x8 pv[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) pv[t] = *reinterpret_cast<const bf16x8 *>(xme + t * 1024);
@@ -1043,77 +1083,105 @@ void dkdv_bf16_kernel(DkdvParams p) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) dvv[k] = *reinterpret_cast<const f32x4 *>(dvb + 32 * sub + 8 * k + 4 * G);
 #pragma unroll
-        for (int j = 0; j < 16; ++j)
+        for (int j = 0; j < 16; ++j) {
           sp[sub][j] = (float)pv[2 * sub + (j >> 3)][j & 7] * (sp[sub][j] - dvv[j >> 2][j & 3]);
+          constexpr int EPP = 32 / NPIECE;
+          if ((16 * sub + j) % EPP == EPP - 1) piece((16 * sub + j) / EPP);
+        }
         pk[2 * sub] = pack_bf16x8(sp[sub], 0);
         pk[2 * sub + 1] = pack_bf16x8(sp[sub], 1);
       }
+      fence_regs(pk);
     };
 
-    // P wave, block i (A_i then B_i). Buffers: rows of i+1 (qrn), dO^T_i (ot);
-    // copies into orw (dO rows of i+2), qtw (Q^T_{i+1}), lsw (LSE2 of i+2);
-    // LSE2 of i+1 in lsn.
+    // One wave's copy batch: rows of a block of Q or dO, a transposed block,
+    // one statistics block (wave q == 0 of the group).
+    struct Batch {
+      RowJob rows;
+      BufRsrc tr, stat;
+    };
+    // Batch prepared one VALU phase ahead: rows (and the P wave's LSE2) of
+    // block `hi`, the transposed block (and the dS wave's D) of block hi - 1.
+    // The two cursors advance by one block per step.
+    Batch nb;
+    Cursor chi, clo;                             // set once nblk > 0 is known
+    auto prep = [&]() __attribute__((always_inline)) {
+      if constexpr (pwave) {
+        nb.rows = prep_rows(p.d_o, chi);
+        nb.tr = prep_t(p.qT, clo);
+        nb.stat = prep_stat(p.lse2, chi);
+      } else {
+        nb.rows = prep_rows(p.q, chi);
+        nb.tr = prep_t(p.doT, clo);
+        nb.stat = prep_stat(p.dvec, clo);
+      }
+      advance(chi);
+      advance(clo);
+    };
+    auto piece_fn = [&](const Batch &bt, char *rdst, char *tdst, float *sdst) __attribute__((always_inline)) {
+      return [&bt, rdst, tdst, sdst, &issue_rows, &issue_t, &issue_stat](int n) __attribute__((always_inline)) {
+        if (n < RPER) issue_rows(bt.rows, n, rdst);
+        else issue_t(bt.tr, n - RPER, tdst);
+        if (n == 0) issue_stat(bt.stat, sdst);
+      };
+    };
+
+    // P wave, block i. A_i: S_{i+1} from rows of i+1 (qrn), dV from dO^T_i (ot).
+    // B_i: P_{i+1} with LSE2 of i+1 (lsn), copying dO rows of i+2 (orw),
+    // Q^T_{i+1} (qtw) and LSE2 of i+2 (lsw); then the next batch is prepared.
     auto p_step = [&](auto CAUSAL, int i, const char *qrn, const char *ot, char *orw, char *qtw, float *lsw,
                       const float *lsn) __attribute__((always_inline)) {
-      const RowJob rj = prep_rows(p.d_o, i + 2);
-      const BufRsrc tj = prep_t(p.qT, i + 1);
-      const BufRsrc sj = prep_stat(p.lse2, i + 2);
-      __builtin_amdgcn_s_waitcnt(0xC07F);   // scalar loads done: exact LDS counts below
-      matrix(std::false_type{}, rel(qrn), rel(ot), [&](int k) __attribute__((always_inline)) {
-        if (k < RPER) issue_rows(rj, k, orw);
-        else issue_t(tj, k - RPER, qtw);
-        if (k == 0) issue_stat(sj, lsw);
-      });
-      wait_prev_batch();
+      matrix(std::false_type{}, rel(qrn), rel(ot));
+      wait_vmcnt<0>();                           // the batch issued in B_{i-1}
       lds_barrier();
-      p_valu(CAUSAL, i + 1, lsn);
-      lds_barrier();
+      const Batch cur = nb;
+      p_valu(CAUSAL, i + 1, lsn, piece_fn(cur, orw, qtw, lsw));
+      prep();                                    // rows of i+3, Q^T_{i+2}, LSE2 of i+3
+      lds_barrier();                             // also waits for any table load
     };
-    // dS wave, block i (A_i then B_i). Buffers: D_i (dvb), Q^T_i (qt), dO rows
-    // of i+1 (orn); copies into qrw (Q rows of i+3), otw (dO^T_{i+2}), dvw (D
-    // of i+2).
+    // dS wave, block i. A_i: dS_i with D_i (dvb), copying Q rows of i+2 (qrw),
+    // dO^T_{i+1} (otw) and D of i+1 (dvw); then the next batch is prepared.
+    // B_i: dK from Q^T_i (qt), dP_{i+1} from dO rows of i+1 (orn).
     auto ds_step = [&](int i, const float *dvb, const char *qt, const char *orn, char *qrw, char *otw,
                        float *dvw) __attribute__((always_inline)) {
-      ds_valu(dvb);
-      lds_barrier();
-      const RowJob rj = prep_rows(p.q, i + 3);
-      const BufRsrc tj = prep_t(p.doT, i + 2);
-      const BufRsrc sj = prep_stat(p.dvec, i + 2);
-      __builtin_amdgcn_s_waitcnt(0xC07F);
-      matrix(std::true_type{}, rel(orn), rel(qt), [&](int k) __attribute__((always_inline)) {
-        if (k < RPER) issue_rows(rj, k, qrw);
-        else issue_t(tj, k - RPER, otw);
-        if (k == 0) issue_stat(sj, dvw);
-      });
-      wait_prev_batch();
+      const Batch cur = nb;
+      ds_valu(dvb, piece_fn(cur, qrw, otw, dvw));
+      prep();                                    // Q rows of i+3, dO^T_{i+2}, D of i+2
+      lds_barrier();                             // also waits for any table load
+      matrix(std::true_type{}, rel(orn), rel(qt));
+      wait_vmcnt<0>();                           // the batch issued in A_i
       lds_barrier();
     };
 
     if (nblk > 0) {
+      chi = cursor_at(2);
+      clo = cursor_at(1);
       // Blocks 0 and 1: rows of 0 and 1, Q^T_0 / dO^T_0, LSE2 of 0 and 1, D_0.
       if constexpr (pwave) {
-        RowJob rj = prep_rows(p.q, 0);
+        const Cursor c0 = cursor_at(0);
+        RowJob rj = prep_rows(p.q, c0);
 #pragma unroll
         for (int k = 0; k < RPER; ++k) issue_rows(rj, k, qr0);
-        rj = prep_rows(p.q, 1);
+        rj = prep_rows(p.q, clo);
 #pragma unroll
         for (int k = 0; k < RPER; ++k) issue_rows(rj, k, qr1);
-        const BufRsrc tj = prep_t(p.qT, 0);
+        const BufRsrc tj = prep_t(p.qT, c0);
 #pragma unroll
         for (int k = 0; k < TPER; ++k) issue_t(tj, k, qt0);
-        issue_stat(prep_stat(p.lse2, 0), ls0);
-        issue_stat(prep_stat(p.lse2, 1), ls1);
+        issue_stat(prep_stat(p.lse2, c0), ls0);
+        issue_stat(prep_stat(p.lse2, clo), ls1);
       } else {
-        RowJob rj = prep_rows(p.d_o, 0);
+        const Cursor c0 = cursor_at(0);
+        RowJob rj = prep_rows(p.d_o, c0);
 #pragma unroll
         for (int k = 0; k < RPER; ++k) issue_rows(rj, k, or0);
-        rj = prep_rows(p.d_o, 1);
+        rj = prep_rows(p.d_o, clo);
 #pragma unroll
         for (int k = 0; k < RPER; ++k) issue_rows(rj, k, or1);
-        const BufRsrc tj = prep_t(p.doT, 0);
+        const BufRsrc tj = prep_t(p.doT, c0);
 #pragma unroll
         for (int k = 0; k < TPER; ++k) issue_t(tj, k, ot0);
-        issue_stat(prep_stat(p.dvec, 0), dv0);
+        issue_stat(prep_stat(p.dvec, c0), dv0);
       }
       wait_vmcnt<0>();
       lds_barrier();
@@ -1125,7 +1193,8 @@ void dkdv_bf16_kernel(DkdvParams p) {
           if constexpr (decltype(CAUSAL)::value) asm volatile("; causal tiles" ::: "memory");
           else asm volatile("; prefix tiles" ::: "memory");
           first_rows(rel(qr0));
-          p_valu(CAUSAL, 0, ls0);
+          p_valu(CAUSAL, 0, ls0, [](int) {});
+          prep();                                // batch of B_0: dO rows of 2, Q^T_1, LSE2 of 2
           lds_barrier();
           for (int i = 0; i < nblk; i += 2) {
             p_step(CAUSAL, i, qr1, ot0, or0, qt1, ls0, ls1);
@@ -1137,21 +1206,12 @@ void dkdv_bf16_kernel(DkdvParams p) {
         else run(std::false_type{});
       } else {
         first_rows(rel(or0));
+        prep();                                  // batch of A_0: Q rows of 2, dO^T_1, D_1
         lds_barrier();
-        // Copies that a B_{-1} phase would have issued: Q rows of 2, dO^T_1, D_1.
-        {
-          const RowJob rj = prep_rows(p.q, 2);
-#pragma unroll
-          for (int k = 0; k < RPER; ++k) issue_rows(rj, k, qr0);
-          const BufRsrc tj = prep_t(p.doT, 1);
-#pragma unroll
-          for (int k = 0; k < TPER; ++k) issue_t(tj, k, ot1);
-          issue_stat(prep_stat(p.dvec, 1), dv1);
-        }
         for (int i = 0; i < nblk; i += 2) {
-          ds_step(i, dv0, qt0, or1, qr1, ot0, dv0);
+          ds_step(i, dv0, qt0, or1, qr0, ot1, dv1);
           if (i + 1 >= nblk) break;
-          ds_step(i + 1, dv1, qt1, or0, qr0, ot1, dv1);
+          ds_step(i + 1, dv1, qt1, or0, qr1, ot0, dv0);
         }
       }
       wait_vmcnt<0>();
@@ -1196,10 +1256,15 @@ hipError_t launch_dq_bf16(const DqParams &p, int D, hipStream_t s) {
 }
 
 hipError_t launch_dkdv_bf16(const DkdvParams &p, int D, int gx, hipStream_t s) {
-  if (D == 64)
-    hipLaunchKernelGGL(dkdv_bf16_kernel<64>, dim3((unsigned)gx, (unsigned)p.Hkv), dim3(kFastThreads), 0, s, p);
-  else
-    hipLaunchKernelGGL(dkdv_bf16_kernel<128>, dim3((unsigned)gx, (unsigned)p.Hkv), dim3(kFastThreads), 0, s, p);
+  const dim3 grid((unsigned)gx, (unsigned)p.Hkv);
+  const bool gfast = kDkdvQBlock % p.g == 0;
+  if (D == 64) {
+    if (gfast) hipLaunchKernelGGL((dkdv_bf16_kernel<64, true>), grid, dim3(kFastThreads), 0, s, p);
+    else hipLaunchKernelGGL((dkdv_bf16_kernel<64, false>), grid, dim3(kFastThreads), 0, s, p);
+  } else {
+    if (gfast) hipLaunchKernelGGL((dkdv_bf16_kernel<128, true>), grid, dim3(kFastThreads), 0, s, p);
+    else hipLaunchKernelGGL((dkdv_bf16_kernel<128, false>), grid, dim3(kFastThreads), 0, s, p);
+  }
   return hipGetLastError();
 }
 
