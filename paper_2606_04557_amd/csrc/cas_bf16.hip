@@ -849,11 +849,16 @@ void dkdv_bf16_kernel(DkdvParams p) {
   const int nblk = __builtin_amdgcn_readfirstlane(per_use * (use_e - use_b));
 
   // Block cursor: block blk of the workgroup's sequence is 64-row block
-  // qb_first + r of batch row b = uses[u] (r = blk mod per_use). Blocks past
-  // the end keep the last block's (b, r) and are not copied.
+  // qb = qb_first + r of batch row b = uses[u] (r = blk mod per_use), with the
+  // element offsets of its rows (GFAST), transposed block and statistics.
+  // Advancing within a batch row adds constant strides; a new batch row (a
+  // table load) recomputes them. Blocks past the end keep the last block's
+  // offsets and are not copied.
   struct Cursor {
     int blk, r, u, b;
+    int64_t roff, rlim, toff, soff;   // rlim: bytes from roff to the group's last row
   };
+  const int64_t row_step = (int64_t)(QB / g) * Hq * D;   // GFAST: elements between consecutive blocks
   auto use_row = [&](int u) __attribute__((always_inline)) {
     int b = self ? self_b : load_const(p.uses, __builtin_amdgcn_readfirstlane(use_b + u));
     // The table load is invariant, so the compiler could sink it (and its
@@ -861,13 +866,23 @@ void dkdv_bf16_kernel(DkdvParams p) {
     asm volatile("" : "+s"(b));
     return b;
   };
+  auto cursor_set = [&](Cursor &c) __attribute__((always_inline)) {
+    c.b = use_row(c.u);
+    const int qb = qb_first + c.r;
+    const int t0 = qb * (QB / g);                 // GFAST only
+    c.roff = (((int64_t)c.b * Sq + t0) * Hq + kvh * g) * D;
+    // rows at or beyond nrows are positions >= Sq, past the group's last row
+    c.rlim = ((int64_t)(Sq - 1 - t0) * Hq + g) * D * 2;
+    c.toff = (((int64_t)c.b * Hkv + kvh) * nqb + qb) * D * 64;
+    c.soff = ((int64_t)c.b * Hkv + kvh) * nrows + qb * QB;
+  };
   auto cursor_at = [&](int blk) __attribute__((always_inline)) {
     Cursor c;
     c.blk = blk;
     const int bl = min(blk, nblk - 1);
     c.u = bl / per_use;
     c.r = bl - c.u * per_use;
-    c.b = use_row(c.u);
+    cursor_set(c);
     return c;
   };
   auto advance = [&](Cursor &c) __attribute__((always_inline)) {
@@ -875,7 +890,13 @@ void dkdv_bf16_kernel(DkdvParams p) {
     if (c.blk < nblk) {
       if (++c.r == per_use) {
         c.r = 0;
-        c.b = use_row(++c.u);
+        ++c.u;
+        cursor_set(c);
+      } else {
+        c.roff += row_step;
+        c.rlim -= row_step * 2;
+        c.toff += D * 64;
+        c.soff += QB;
       }
     }
   };
@@ -896,42 +917,47 @@ void dkdv_bf16_kernel(DkdvParams p) {
   CopyLanes<64, D, 4> ct;                      // transposed blocks: D rows of 64
   ct.init(q, lane);
   constexpr int TPER = CopyLanes<64, D, 4>::PER;
-  constexpr int NPIECE = RPER + TPER;          // copy instructions per wave per block (+ statistics)
-  static_assert(32 % NPIECE == 0, "copy pieces spread over the 32 VALU elements");
+  static_assert(RPER * 8 == NMF, "one row-block copy per eight MFMAs");
+  static_assert(32 % TPER == 0, "transposed-block copies spread over the 32 VALU elements");
   int tvoff[TPER];
 #pragma unroll
   for (int i = 0; i < TPER; ++i) tvoff[i] = (ct.row[i] * 64 + ct.coff[i]) * 2;
 
+  // A copy source: base address and resource size in bytes (0: nothing is
+  // read, the copy writes zeros). Both are pinned when prepared, so their
+  // scalar arithmetic stays in the VALU phase that prepares them; the buffer
+  // resource is assembled at the copy.
+  struct Src {
+    const char *base;
+    int bytes;
+  };
+  auto pin = [&](Src &x) __attribute__((always_inline)) { asm volatile("" : "+s"(x.base), "+s"(x.bytes)); };
   struct RowJob {
-    BufRsrc rs;
+    Src s;
     int voff[RPER];
   };
-  // Rows of the cursor's block of Q or dO (blocks past the end: empty resource).
+  // Rows of the cursor's block of Q or dO.
   auto prep_rows = [&](const void *src, const Cursor &c) __attribute__((always_inline)) {
     RowJob jb;
     const bool live = c.blk < nblk;
-    const int b = c.b, r0 = (qb_first + c.r) * QB;
     if constexpr (GFAST) {
-      // The block starts at position t0 = r0 / g; rows at or beyond nrows are
-      // positions >= Sq, which lie past the group's last row at Sq - 1.
-      const int t0 = (qb_first + c.r) * (QB / g);
-      const int64_t head0 = (((int64_t)b * Sq + t0) * Hq + kvh * g) * D;
-      const int64_t lim = ((int64_t)(Sq - 1 - t0) * Hq + g) * D * 2;
-      jb.rs = make_rsrc((const __bf16 *)src + head0, live ? (int)min(lim, (int64_t)0x7fffffff) : 0);
+      jb.s.base = (const char *)((const __bf16 *)src + c.roff);
+      jb.s.bytes = live ? (int)min(c.rlim, (int64_t)0x7fffffff) : 0;
 #pragma unroll
       for (int i = 0; i < RPER; ++i) jb.voff[i] = qfix[i] * 2;
     } else {
+      const int r0 = (qb_first + c.r) * QB;
       const int nv = min(QB, nrows - r0);
       const int t0 = r0 / g;
-      const int64_t head0 = (((int64_t)b * Sq + t0) * Hq + kvh * g) * D;
+      const int64_t head0 = (((int64_t)c.b * Sq + t0) * Hq + kvh * g) * D;
       // Packed row r is at element ((t - t0) Hq + h) D; rows at or beyond nv
       // lie outside the resource and read as zero.
       auto rowoff = [&](int r) __attribute__((always_inline)) {
         const int rr = r0 + r, t = rr / g;
         return ((t - t0) * Hq + (rr - t * g)) * D;
       };
-      const int last = rowoff(nv - 1) + D;
-      jb.rs = make_rsrc((const __bf16 *)src + head0, live ? last * 2 : 0);
+      jb.s.base = (const char *)((const __bf16 *)src + head0);
+      jb.s.bytes = live ? (rowoff(nv - 1) + D) * 2 : 0;
 #pragma unroll
       for (int i = 0; i < RPER; ++i) {
         const int pos = (q + 4 * i) * 64 + lane;
@@ -939,29 +965,31 @@ void dkdv_bf16_kernel(DkdvParams p) {
         jb.voff[i] = (rowoff(r) + ((pos % CPI) ^ swz<D>(r)) * 8) * 2;
       }
     }
+    pin(jb.s);
     return jb;
   };
   auto issue_rows = [&](const RowJob &jb, int i, char *dst) __attribute__((always_inline)) {
-    dma16(jb.rs, jb.voff[i], dst + (q + 4 * i) * 1024);
+    dma16(make_rsrc(jb.s.base, jb.s.bytes), jb.voff[i], dst + (q + 4 * i) * 1024);
   };
   // Transposed block of Q or dO.
   auto prep_t = [&](const void *src, const Cursor &c) __attribute__((always_inline)) {
-    const bool live = c.blk < nblk;
-    const int64_t tb = (((int64_t)c.b * Hkv + kvh) * nqb + qb_first + c.r) * D * 64;
-    return make_rsrc((const __bf16 *)src + tb, live ? D * 128 : 0);
+    Src x{(const char *)((const __bf16 *)src + c.toff), c.blk < nblk ? D * 128 : 0};
+    pin(x);
+    return x;
   };
-  auto issue_t = [&](BufRsrc rs, int i, char *dst) __attribute__((always_inline)) {
-    dma16(rs, tvoff[i], dst + (q + 4 * i) * 1024);
+  auto issue_t = [&](const Src &x, int i, char *dst) __attribute__((always_inline)) {
+    dma16(make_rsrc(x.base, x.bytes), tvoff[i], dst + (q + 4 * i) * 1024);
   };
   // LSE2 or D (64 floats; lanes at or beyond nrows read zero).
   auto prep_stat = [&](const float *src, const Cursor &c) __attribute__((always_inline)) {
-    const bool live = c.blk < nblk;
     const int r0 = (qb_first + c.r) * QB;
-    const int64_t base = ((int64_t)c.b * Hkv + kvh) * nrows + r0;
-    return make_rsrc(src + base, live ? min(QB, nrows - r0) * 4 : 0);
+    Src x{(const char *)(src + c.soff), c.blk < nblk ? min(QB, nrows - r0) * 4 : 0};
+    pin(x);
+    return x;
   };
-  auto issue_stat = [&](BufRsrc rs, float *dst) __attribute__((always_inline)) {
-    if (q == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t *)dst, 4, lane * 4, 0, 0, 0);
+  auto issue_stat = [&](const Src &x, float *dst) __attribute__((always_inline)) {
+    if (q == 0)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(x.base, x.bytes), (lds_void_t *)dst, 4, lane * 4, 0, 0, 0);
   };
 
   // The two roles run separate code (PW: P wave); barriers pair up one to one.
@@ -999,8 +1027,9 @@ void dkdv_bf16_kernel(DkdvParams p) {
     // Matrix phase: 2 NSTEP MFMAs on row fragments of `rows` (S or dP of the
     // next block) and 2 NSTEP on transposed fragments of `tr` times pk (dV or
     // dK of this block); TR_FIRST puts the transposed product first. One LDS
-    // fragment per MFMA, LEAD fragments ahead.
-    auto matrix = [&](auto TR_FIRST, const char *rows, const char *tr) __attribute__((always_inline)) {
+    // fragment per MFMA, LEAD fragments ahead; row-block copy piece n after
+    // MFMA 8n + 7.
+    auto matrix = [&](auto TR_FIRST, const char *rows, const char *tr, auto &&piece) __attribute__((always_inline)) {
       constexpr bool TF = decltype(TR_FIRST)::value;
       constexpr int H = 2 * NSTEP;
       auto frag = [&](auto K) __attribute__((always_inline)) {
@@ -1025,6 +1054,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
         if constexpr (k + LEAD < NMF) ring[(k + LEAD) % RING] = frag(std::integral_constant<int, k + LEAD>{});
         if constexpr (is_tr) acc[kk / 4] = Mma<__bf16>::run(ring[k % RING], pk[kk % 4], acc[kk / 4]);
         else sp[kk / NSTEP] = Mma<__bf16>::run(ring[k % RING], kv[kk % NSTEP], sp[kk / NSTEP]);
+        if constexpr ((k & 7) == 7) piece(k >> 3);
       });
       __builtin_amdgcn_sched_barrier(0);
       __builtin_amdgcn_s_setprio(0);
@@ -1061,7 +1091,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
           float pv = fast_exp2(fmaf(sp[sub][j], c, -lsv[j >> 2][j & 3]));
           if constexpr (CA) pv = crow(j, 0) >= lo ? pv : 0.0f;
           sp[sub][j] = pv;
-          constexpr int EPP = 32 / NPIECE;   // elements per copy piece
+          constexpr int EPP = 32 / TPER;     // elements per copy piece
           if ((16 * sub + j) % EPP == EPP - 1) piece((16 * sub + j) / EPP);
         }
         pk[2 * sub] = pack_bf16x8(sp[sub], 0);
@@ -1085,7 +1115,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
           sp[sub][j] = (float)pv[2 * sub + (j >> 3)][j & 7] * (sp[sub][j] - dvv[j >> 2][j & 3]);
-          constexpr int EPP = 32 / NPIECE;
+          constexpr int EPP = 32 / TPER;
           if ((16 * sub + j) % EPP == EPP - 1) piece((16 * sub + j) / EPP);
         }
         pk[2 * sub] = pack_bf16x8(sp[sub], 0);
@@ -1098,7 +1128,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
     // one statistics block (wave q == 0 of the group).
     struct Batch {
       RowJob rows;
-      BufRsrc tr, stat;
+      Src tr, stat;
     };
     // Batch prepared one VALU phase ahead: rows (and the P wave's LSE2) of
     // block `hi`, the transposed block (and the dS wave's D) of block hi - 1.
@@ -1118,38 +1148,48 @@ void dkdv_bf16_kernel(DkdvParams p) {
       advance(chi);
       advance(clo);
     };
-    auto piece_fn = [&](const Batch &bt, char *rdst, char *tdst, float *sdst) __attribute__((always_inline)) {
-      return [&bt, rdst, tdst, sdst, &issue_rows, &issue_t, &issue_stat](int n) __attribute__((always_inline)) {
-        if (n < RPER) issue_rows(bt.rows, n, rdst);
-        else issue_t(bt.tr, n - RPER, tdst);
+    auto rows_piece = [&](char *dst) __attribute__((always_inline)) {
+      return [&nb, dst, &issue_rows](int n) __attribute__((always_inline)) { issue_rows(nb.rows, n, dst); };
+    };
+    auto tr_piece = [&](const Batch &bt, char *tdst, float *sdst) __attribute__((always_inline)) {
+      return [&bt, tdst, sdst, &issue_t, &issue_stat](int n) __attribute__((always_inline)) {
+        issue_t(bt.tr, n, tdst);
         if (n == 0) issue_stat(bt.stat, sdst);
       };
     };
 
-    // P wave, block i. A_i: S_{i+1} from rows of i+1 (qrn), dV from dO^T_i (ot).
-    // B_i: P_{i+1} with LSE2 of i+1 (lsn), copying dO rows of i+2 (orw),
-    // Q^T_{i+1} (qtw) and LSE2 of i+2 (lsw); then the next batch is prepared.
+    // A wave's batch is split: its row-block copies go into a matrix phase (one
+    // per eight MFMAs), its transposed-block and statistics copies into a VALU
+    // phase, so no phase issues more than a few copies and the copy queue
+    // never stalls the issuing wave for long. At the end of each matrix phase
+    // a wave waits for everything but that phase's row copies.
+    //
+    // P wave, block i (batch i: dO rows of i+2, Q^T_{i+1}, LSE2 of i+2).
+    // A_i: S_{i+1} from rows of i+1 (qrn), dV from dO^T_i (ot); dO rows of
+    // i+2 into orw. B_i: P_{i+1} with LSE2 of i+1 (lsn); Q^T_{i+1} into qtw,
+    // LSE2 of i+2 into lsw; then batch i+1 is prepared.
     auto p_step = [&](auto CAUSAL, int i, const char *qrn, const char *ot, char *orw, char *qtw, float *lsw,
                       const float *lsn) __attribute__((always_inline)) {
-      matrix(std::false_type{}, rel(qrn), rel(ot));
-      wait_vmcnt<0>();                           // the batch issued in B_{i-1}
+      matrix(std::false_type{}, rel(qrn), rel(ot), rows_piece(orw));
+      wait_vmcnt<RPER>();                        // batch i-1 has landed
       lds_barrier();
       const Batch cur = nb;
-      p_valu(CAUSAL, i + 1, lsn, piece_fn(cur, orw, qtw, lsw));
-      prep();                                    // rows of i+3, Q^T_{i+2}, LSE2 of i+3
+      p_valu(CAUSAL, i + 1, lsn, tr_piece(cur, qtw, lsw));
+      prep();
       lds_barrier();                             // also waits for any table load
     };
-    // dS wave, block i. A_i: dS_i with D_i (dvb), copying Q rows of i+2 (qrw),
-    // dO^T_{i+1} (otw) and D of i+1 (dvw); then the next batch is prepared.
-    // B_i: dK from Q^T_i (qt), dP_{i+1} from dO rows of i+1 (orn).
+    // dS wave, block i (batch i: Q rows of i+2, dO^T_{i+1}, D of i+1; its
+    // rows were copied during B_{i-1}). A_i: dS_i with D_i (dvb); dO^T_{i+1}
+    // into otw, D of i+1 into dvw; then batch i+1 is prepared. B_i: dK from
+    // Q^T_i (qt), dP_{i+1} from dO rows of i+1 (orn); Q rows of i+3 into qrw.
     auto ds_step = [&](int i, const float *dvb, const char *qt, const char *orn, char *qrw, char *otw,
                        float *dvw) __attribute__((always_inline)) {
       const Batch cur = nb;
-      ds_valu(dvb, piece_fn(cur, qrw, otw, dvw));
-      prep();                                    // Q rows of i+3, dO^T_{i+2}, D of i+2
+      ds_valu(dvb, tr_piece(cur, otw, dvw));
+      prep();
       lds_barrier();                             // also waits for any table load
-      matrix(std::true_type{}, rel(orn), rel(qt));
-      wait_vmcnt<0>();                           // the batch issued in A_i
+      matrix(std::true_type{}, rel(orn), rel(qt), rows_piece(qrw));
+      wait_vmcnt<RPER>();                        // batch i has landed
       lds_barrier();
     };
 
@@ -1165,7 +1205,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
         rj = prep_rows(p.q, clo);
 #pragma unroll
         for (int k = 0; k < RPER; ++k) issue_rows(rj, k, qr1);
-        const BufRsrc tj = prep_t(p.qT, c0);
+        const Src tj = prep_t(p.qT, c0);
 #pragma unroll
         for (int k = 0; k < TPER; ++k) issue_t(tj, k, qt0);
         issue_stat(prep_stat(p.lse2, c0), ls0);
@@ -1178,7 +1218,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
         rj = prep_rows(p.d_o, clo);
 #pragma unroll
         for (int k = 0; k < RPER; ++k) issue_rows(rj, k, or1);
-        const BufRsrc tj = prep_t(p.doT, c0);
+        const Src tj = prep_t(p.doT, c0);
 #pragma unroll
         for (int k = 0; k < TPER; ++k) issue_t(tj, k, ot0);
         issue_stat(prep_stat(p.dvec, c0), dv0);
@@ -1194,7 +1234,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
           else asm volatile("; prefix tiles" ::: "memory");
           first_rows(rel(qr0));
           p_valu(CAUSAL, 0, ls0, [](int) {});
-          prep();                                // batch of B_0: dO rows of 2, Q^T_1, LSE2 of 2
+          prep();                                // batch 0
           lds_barrier();
           for (int i = 0; i < nblk; i += 2) {
             p_step(CAUSAL, i, qr1, ot0, or0, qt1, ls0, ls1);
@@ -1206,12 +1246,17 @@ void dkdv_bf16_kernel(DkdvParams p) {
         else run(std::false_type{});
       } else {
         first_rows(rel(or0));
-        prep();                                  // batch of A_0: Q rows of 2, dO^T_1, D_1
+        prep();                                  // batch 0
         lds_barrier();
+        {
+          auto rp = rows_piece(qr0);             // batch 0's rows (Q rows of 2)
+#pragma unroll
+          for (int k = 0; k < RPER; ++k) rp(k);
+        }
         for (int i = 0; i < nblk; i += 2) {
-          ds_step(i, dv0, qt0, or1, qr0, ot1, dv1);
+          ds_step(i, dv0, qt0, or1, qr1, ot1, dv1);
           if (i + 1 >= nblk) break;
-          ds_step(i + 1, dv1, qt1, or0, qr1, ot0, dv0);
+          ds_step(i + 1, dv1, qt1, or0, qr0, ot0, dv0);
         }
       }
       wait_vmcnt<0>();
