@@ -96,7 +96,7 @@ struct Plan {
   // workspace layout
   size_t off_segs = 0, off_rows = 0, off_tiles = 0, off_carts = 0, off_uses = 0, table_bytes = 0;
   size_t off_part_o = 0, off_part_lse = 0, off_ovf = 0, off_row_max = 0, ws_fwd = 0;
-  size_t off_dvec = 0, off_lse2 = 0, off_part_dq = 0, off_qT = 0, off_doT = 0, ws_bwd = 0;
+  size_t off_nd = 0, off_lse2 = 0, off_part_dq = 0, off_qT = 0, off_doT = 0, ws_bwd = 0;
 };
 
 constexpr int kTargetWgs = 512;   // two workgroups per CU on a 256-CU MI355X
@@ -315,7 +315,7 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
     }
     pl.ws_fwd = off;
   } else {
-    pl.off_dvec = off;
+    pl.off_nd = off;
     off = align_up(off + plane * 4, 256);
     pl.off_lse2 = off;
     off = align_up(off + plane * 4, 256);
@@ -671,7 +671,7 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
   s = upload_tables(pl, true, workspace, stream);
   if (s != CAS_OK) return s;
   char *ws = (char *)workspace;
-  float *dvec = (float *)(ws + pl.off_dvec);
+  float *nd = (float *)(ws + pl.off_nd);
   float *lse2 = (float *)(ws + pl.off_lse2);
   const float scale_log2 = pl.scale * 1.4426950408889634f;
 
@@ -679,7 +679,7 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
   pp.o = o;
   pp.d_o = d_o;
   pp.lse = lse;
-  pp.dvec = dvec;
+  pp.nd = nd;
   pp.lse2 = lse2;
   pp.B = pl.B;
   pp.Sq = pl.Sq;
@@ -701,7 +701,7 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
     kp.k_self = k_self;
     kp.v_self = v_self;
     kp.d_o = d_o;
-    kp.dvec = dvec;
+    kp.nd = nd;
     kp.lse2 = lse2;
     kp.qT = pp.qT;
     kp.doT = pp.doT;
@@ -733,7 +733,7 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
     dp.k_self = k_self;
     dp.v_self = v_self;
     dp.d_o = d_o;
-    dp.dvec = dvec;
+    dp.nd = nd;
     dp.lse2 = lse2;
     dp.dq = dq;
     dp.part_dq = pl.dq_splits > 1 ? (float *)(ws + pl.off_part_dq) : nullptr;

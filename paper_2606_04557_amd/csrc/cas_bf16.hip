@@ -543,7 +543,7 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
   to.init(lane);
 
   bf16x8 qf[NSTEP], df[NSTEP];
-  float lse2r = INFINITY, dvr = 0.0f;
+  float lse2r = INFINITY, ndr = 0.0f;
   if (my_row < nrows) {
     const int64_t off = (((int64_t)b * Sq + my_t) * Hq + kvh * g + (my_row - my_t * g)) * D;
     const __bf16 *qp = (const __bf16 *)p.q + off;
@@ -555,7 +555,7 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
     }
     const int64_t pk = ((int64_t)b * Hkv + kvh) * nrows + my_row;
     lse2r = p.lse2[pk];
-    dvr = p.dvec[pk];
+    ndr = p.nd[pk];
   } else {
 #pragma unroll
     for (int st = 0; st < NSTEP; ++st) {
@@ -600,7 +600,7 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
           const bool ok = key < ti.nvalid && (ti.self0 < 0 || ti.self0 + key <= my_t);
           pv = ok ? pv : 0.0f;
         }
-        sa[j] = pv * (dpa[j] - dvr);
+        sa[j] = pv * (dpa[j] + ndr);
       }
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
@@ -723,14 +723,14 @@ __global__ __launch_bounds__(256) void bwd_transpose_bf16_kernel(PreParams p) {
 // the transposed blocks Q^T and dO^T (written by the backward prologue) for
 // the dK and dV products.
 //
-// Copies (LDS double buffers) are issued in VALU phases, interleaved with the
-// VALU work, so the matrix phases are MFMAs and LDS reads only: P waves issue
-// dO rows of block i+2, Q^T_{i+1} and LSE2 of i+2 during B_i; dS waves issue
-// Q rows of block i+2, dO^T_{i+1} and D of i+1 during A_i. A wave waits for
-// its batch at the end of its next matrix phase. The copy addresses (with
-// their segment-table loads) are prepared one VALU phase ahead. Copies for
-// blocks past the end use an empty buffer resource (they write zeros that
-// nothing reads).
+// Copies (LDS double buffers): per block, P waves fetch dO rows of block i+2,
+// Q^T_{i+1} and LSE2 of i+2; dS waves fetch Q rows of block i+2, dO^T_{i+1}
+// and -D of i+2 (the statistic is stored negated and loaded straight into the
+// dP accumulators, so the MFMAs deliver dP - D). A wave's row-block copies go
+// into its matrix phase, one per eight MFMAs, the rest into its VALU phase.
+// Copy addresses (with their segment-table loads) are prepared one VALU phase
+// ahead. Copies for blocks past the end use an empty buffer resource (they
+// write zeros that nothing reads).
 //
 // P needs no mask for keys beyond the tile (their dK / dV columns are never
 // stored) or rows beyond nrows (Q, dO, Q^T, dO^T, LSE2 and D all read as
@@ -1024,12 +1024,26 @@ void dkdv_bf16_kernel(DkdvParams p) {
     f32x16 sp[2];                                // S (P waves) or dP (dS waves) of both 32-row subtiles
     bf16x8 pk[4];                                // P (P waves) or dS (dS waves), k-step 2 sub + h
 
+    // -D of a block's rows crow(j, G) of both subtiles, straight into the dP
+    // accumulators: register 4k + e of subtile sub is row 32 sub + 8k + 4G + e.
+    auto init_nd = [&](const float *ndn) __attribute__((always_inline)) {
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const f32x4 v = *reinterpret_cast<const f32x4 *>(ndn + 32 * sub + 8 * k + 4 * G);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) sp[sub][4 * k + e] = v[e];
+        }
+    };
     // Matrix phase: 2 NSTEP MFMAs on row fragments of `rows` (S or dP of the
     // next block) and 2 NSTEP on transposed fragments of `tr` times pk (dV or
     // dK of this block); TR_FIRST puts the transposed product first. One LDS
     // fragment per MFMA, LEAD fragments ahead; row-block copy piece n after
-    // MFMA 8n + 7.
-    auto matrix = [&](auto TR_FIRST, const char *rows, const char *tr, auto &&piece) __attribute__((always_inline)) {
+    // MFMA 8n + 7. With TR_FIRST (dS wave) the dP accumulator starts at -D of
+    // the next block (ndn), so the MFMAs deliver dP - D.
+    auto matrix = [&](auto TR_FIRST, const char *rows, const char *tr, const float *ndn, auto &&piece)
+                      __attribute__((always_inline)) {
       constexpr bool TF = decltype(TR_FIRST)::value;
       constexpr int H = 2 * NSTEP;
       auto frag = [&](auto K) __attribute__((always_inline)) {
@@ -1039,8 +1053,11 @@ void dkdv_bf16_kernel(DkdvParams p) {
         if constexpr (is_tr) return row_frag_at<64>(tr, rt, 32 * (kk / 4), kk % 4);
         else return row_frag_at<D>(rows, ro, 32 * (kk / NSTEP), kk % NSTEP);
       };
-      sp[0] = zero16();
-      sp[1] = zero16();
+      if constexpr (TF) init_nd(ndn);
+      else {
+        sp[0] = zero16();
+        sp[1] = zero16();
+      }
       // The SIMD's other wave is in its VALU phase: let this wave's MFMA
       // stream issue first.
       __builtin_amdgcn_s_setprio(PRIO);
@@ -1059,10 +1076,14 @@ void dkdv_bf16_kernel(DkdvParams p) {
       __builtin_amdgcn_sched_barrier(0);
       __builtin_amdgcn_s_setprio(0);
     };
-    // S or dP of block 0 alone (prologue).
-    auto first_rows = [&](const char *rows) __attribute__((always_inline)) {
-      sp[0] = zero16();
-      sp[1] = zero16();
+    // S or dP - D of block 0 alone (prologue).
+    auto first_rows = [&](const char *rows, const float *ndn) __attribute__((always_inline)) {
+      if constexpr (pwave) {
+        sp[0] = zero16();
+        sp[1] = zero16();
+      } else {
+        init_nd(ndn);
+      }
 #pragma unroll
       for (int s = 0; s < NSTEP; ++s) {
         sp[0] = Mma<__bf16>::run(row_frag_at<D>(rows, ro, 0, s), kv[s], sp[0]);
@@ -1101,20 +1122,17 @@ void dkdv_bf16_kernel(DkdvParams p) {
       for (int t = 0; t < 4; ++t) *reinterpret_cast<bf16x8 *>(xme + t * 1024) = pk[t];
       fence_regs(pk);
     };
-    // dS wave VALU phase: dS of a block from the published P, sp (dP) and D in
-    // dvb; piece(n) as for the P wave.
-    auto ds_valu = [&](const float *dvb, auto &&piece) __attribute__((always_inline)) {
+    // dS wave VALU phase: dS = P (dP - D) of a block from the published P and
+    // sp (dP - D); piece(n) as for the P wave.
+    auto ds_valu = [&](auto &&piece) __attribute__((always_inline)) {
       bf16x8 pv[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) pv[t] = *reinterpret_cast<const bf16x8 *>(xme + t * 1024);
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub) {
-        f32x4 dvv[4];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) dvv[k] = *reinterpret_cast<const f32x4 *>(dvb + 32 * sub + 8 * k + 4 * G);
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-          sp[sub][j] = (float)pv[2 * sub + (j >> 3)][j & 7] * (sp[sub][j] - dvv[j >> 2][j & 3]);
+          sp[sub][j] = (float)pv[2 * sub + (j >> 3)][j & 7] * sp[sub][j];
           constexpr int EPP = 32 / TPER;
           if ((16 * sub + j) % EPP == EPP - 1) piece((16 * sub + j) / EPP);
         }
@@ -1143,7 +1161,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
       } else {
         nb.rows = prep_rows(p.q, chi);
         nb.tr = prep_t(p.doT, clo);
-        nb.stat = prep_stat(p.dvec, clo);
+        nb.stat = prep_stat(p.nd, chi);
       }
       advance(chi);
       advance(clo);
@@ -1170,7 +1188,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
     // LSE2 of i+2 into lsw; then batch i+1 is prepared.
     auto p_step = [&](auto CAUSAL, int i, const char *qrn, const char *ot, char *orw, char *qtw, float *lsw,
                       const float *lsn) __attribute__((always_inline)) {
-      matrix(std::false_type{}, rel(qrn), rel(ot), rows_piece(orw));
+      matrix(std::false_type{}, rel(qrn), rel(ot), nullptr, rows_piece(orw));
       wait_vmcnt<RPER>();                        // batch i-1 has landed
       lds_barrier();
       const Batch cur = nb;
@@ -1178,17 +1196,18 @@ void dkdv_bf16_kernel(DkdvParams p) {
       prep();
       lds_barrier();                             // also waits for any table load
     };
-    // dS wave, block i (batch i: Q rows of i+2, dO^T_{i+1}, D of i+1; its
-    // rows were copied during B_{i-1}). A_i: dS_i with D_i (dvb); dO^T_{i+1}
-    // into otw, D of i+1 into dvw; then batch i+1 is prepared. B_i: dK from
-    // Q^T_i (qt), dP_{i+1} from dO rows of i+1 (orn); Q rows of i+3 into qrw.
-    auto ds_step = [&](int i, const float *dvb, const char *qt, const char *orn, char *qrw, char *otw,
-                       float *dvw) __attribute__((always_inline)) {
+    // dS wave, block i (batch i: Q rows of i+2, dO^T_{i+1}, -D of i+2; its
+    // rows were copied during B_{i-1}). A_i: dS_i; dO^T_{i+1} into otw, -D of
+    // i+2 into ndw; then batch i+1 is prepared. B_i: dK from Q^T_i (qt),
+    // dP_{i+1} - D from dO rows of i+1 (orn) and -D of i+1 (ndn); Q rows of
+    // i+3 into qrw.
+    auto ds_step = [&](int i, const float *ndn, const char *qt, const char *orn, char *qrw, char *otw,
+                       float *ndw) __attribute__((always_inline)) {
       const Batch cur = nb;
-      ds_valu(dvb, tr_piece(cur, otw, dvw));
+      ds_valu(tr_piece(cur, otw, ndw));
       prep();
       lds_barrier();                             // also waits for any table load
-      matrix(std::true_type{}, rel(orn), rel(qt), rows_piece(qrw));
+      matrix(std::true_type{}, rel(orn), rel(qt), ndn, rows_piece(qrw));
       wait_vmcnt<RPER>();                        // batch i has landed
       lds_barrier();
     };
@@ -1196,7 +1215,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
     if (nblk > 0) {
       chi = cursor_at(2);
       clo = cursor_at(1);
-      // Blocks 0 and 1: rows of 0 and 1, Q^T_0 / dO^T_0, LSE2 of 0 and 1, D_0.
+      // Blocks 0 and 1: rows of 0 and 1, Q^T_0 / dO^T_0, LSE2 and -D of 0 and 1.
       if constexpr (pwave) {
         const Cursor c0 = cursor_at(0);
         RowJob rj = prep_rows(p.q, c0);
@@ -1221,7 +1240,8 @@ void dkdv_bf16_kernel(DkdvParams p) {
         const Src tj = prep_t(p.doT, c0);
 #pragma unroll
         for (int k = 0; k < TPER; ++k) issue_t(tj, k, ot0);
-        issue_stat(prep_stat(p.dvec, c0), dv0);
+        issue_stat(prep_stat(p.nd, c0), dv0);
+        issue_stat(prep_stat(p.nd, clo), dv1);
       }
       wait_vmcnt<0>();
       lds_barrier();
@@ -1232,7 +1252,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
           // the other variant's loop).
           if constexpr (decltype(CAUSAL)::value) asm volatile("; causal tiles" ::: "memory");
           else asm volatile("; prefix tiles" ::: "memory");
-          first_rows(rel(qr0));
+          first_rows(rel(qr0), nullptr);
           p_valu(CAUSAL, 0, ls0, [](int) {});
           prep();                                // batch 0
           lds_barrier();
@@ -1245,7 +1265,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
         if (self) run(std::true_type{});
         else run(std::false_type{});
       } else {
-        first_rows(rel(or0));
+        first_rows(rel(or0), dv0);
         prep();                                  // batch 0
         lds_barrier();
         {
@@ -1254,9 +1274,9 @@ void dkdv_bf16_kernel(DkdvParams p) {
           for (int k = 0; k < RPER; ++k) rp(k);
         }
         for (int i = 0; i < nblk; i += 2) {
-          ds_step(i, dv0, qt0, or1, qr1, ot1, dv1);
+          ds_step(i, dv1, qt0, or1, qr1, ot1, dv0);
           if (i + 1 >= nblk) break;
-          ds_step(i + 1, dv1, qt1, or0, qr0, ot0, dv0);
+          ds_step(i + 1, dv0, qt1, or0, qr0, ot0, dv1);
         }
       }
       wait_vmcnt<0>();

@@ -49,7 +49,7 @@ __global__ __launch_bounds__(kThreads) void bwd_pre_kernel(PreParams p) {
 #pragma unroll
   for (int m = LPR / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, LPR);
   if (R < total && li == 0) {
-    p.dvec[R] = acc;
+    p.nd[R] = -acc;
     p.lse2[R] = p.lse[((int64_t)b * Hq + h) * p.Sq + t] * kLog2e;
   }
 }
@@ -71,7 +71,7 @@ __global__ __launch_bounds__(kThreads) void dkdv_kernel(DkdvParams p) {
   __shared__ __attribute__((aligned(16))) T q_oct[OSZ];
   __shared__ __attribute__((aligned(16))) T do_oct[OSZ];
   __shared__ float lse2_l[QB];
-  __shared__ float dvec_l[QB];
+  __shared__ float nd_l[QB];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int G = lane >> 5, n = lane & 31;
@@ -140,7 +140,7 @@ __global__ __launch_bounds__(kThreads) void dkdv_kernel(DkdvParams p) {
     const T *qb_base = (const T *)p.q + ((int64_t)b * Sq * Hq + kvh * g) * D;
     const T *dob_base = (const T *)p.d_o + ((int64_t)b * Sq * Hq + kvh * g) * D;
     const float *lse2_b = p.lse2 + ((int64_t)b * Hkv + kvh) * nrows;
-    const float *dvec_b = p.dvec + ((int64_t)b * Hkv + kvh) * nrows;
+    const float *nd_b = p.nd + ((int64_t)b * Hkv + kvh) * nrows;
     for (int qb = qb0; qb < nqb; ++qb) {
       const int r0 = qb * QB;
       const int nv = min(QB, nrows - r0);
@@ -163,7 +163,7 @@ __global__ __launch_bounds__(kThreads) void dkdv_kernel(DkdvParams p) {
       if (tid < QB) {
         const int rr = r0 + tid;
         lse2_l[tid] = rr < nrows ? lse2_b[rr] : INFINITY;
-        dvec_l[tid] = rr < nrows ? dvec_b[rr] : 0.0f;
+        nd_l[tid] = rr < nrows ? nd_b[rr] : 0.0f;
       }
       __syncthreads();
       if (!wave_has_keys) continue;
@@ -185,7 +185,7 @@ __global__ __launch_bounds__(kThreads) void dkdv_kernel(DkdvParams p) {
           float pv = exp2f(fmaf(sa[j], c, -lse2_l[ql]));
           if (need_mask) pv = (my_key <= (r0 + ql) / g) ? pv : 0.0f;
           pv = key_ok ? pv : 0.0f;
-          const float ds = pv * (dpa[j] - dvec_l[ql]);
+          const float ds = pv * (dpa[j] + nd_l[ql]);
           sa[j] = pv;
           dpa[j] = ds;
         }
@@ -271,7 +271,7 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(DqParams p) {
   const float c = p.scale_log2;
 
   Frag qf[QS][NSTEP], df[QS][NSTEP];
-  float lse2r[QS], dvr[QS];
+  float lse2r[QS], ndr[QS];
   const int64_t pk = ((int64_t)b * Hkv + kvh) * nrows;
 #pragma unroll
   for (int qs = 0; qs < QS; ++qs) {
@@ -285,7 +285,7 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(DqParams p) {
         df[qs][s] = global_frag<T>((const T *)p.d_o + off, s, G);
       }
       lse2r[qs] = p.lse2[pk + r];
-      dvr[qs] = p.dvec[pk + r];
+      ndr[qs] = p.nd[pk + r];
     } else {
 #pragma unroll
       for (int s = 0; s < NSTEP; ++s) {
@@ -293,7 +293,7 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(DqParams p) {
         df[qs][s] = M::zero();
       }
       lse2r[qs] = INFINITY;
-      dvr[qs] = 0.0f;
+      ndr[qs] = 0.0f;
     }
   }
   f32x16 acc[DT][QS];
@@ -377,7 +377,7 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(DqParams p) {
             const bool ok = key < nvalid && (self0 < 0 || self0 + key <= t);
             pv = ok ? pv : 0.0f;
           }
-          sa[qs][j] = pv * (dpa[qs][j] - dvr[qs]);
+          sa[qs][j] = pv * (dpa[qs][j] + ndr[qs]);
         }
       }
       if constexpr (BF16) {

@@ -95,7 +95,7 @@ struct PreParams {
   const void *o;
   const void *d_o;
   const float *lse;
-  float *dvec;   // [B][Hkv][nrows]  rowsum(dO * O)
+  float *nd;     // [B][Hkv][nrows]  -rowsum(dO * O)  (D negated)
   float *lse2;   // [B][Hkv][nrows]  LSE * log2(e)
   const void *q;
   void *qT;      // bf16: [B][Hkv][nqb][D][64] Q of each 64-row block, transposed
@@ -108,7 +108,7 @@ struct DqParams {
   const void *k_self;
   const void *v_self;
   const void *d_o;
-  const float *dvec;
+  const float *nd;        // -D
   const float *lse2;
   void *dq;
   float *part_dq;   // [splits][B][Hkv][nrows][D] when splits > 1
@@ -132,7 +132,7 @@ struct DkdvParams {
   const void *k_self;
   const void *v_self;
   const void *d_o;
-  const float *dvec;
+  const float *nd;        // -D
   const float *lse2;
   const void *qT;           // bf16: transposed Q / dO blocks (see PreParams)
   const void *doT;
