@@ -42,11 +42,20 @@ def log(*a):
 
 
 def kernel_source_hash() -> str:
-    """Hash of the bf16 kernel sources the recorded HBM counters belong to."""
+    """Hash of the bf16 kernel code the recorded HBM counters belong to
+    (comments and blank lines are left out: they do not change the kernel)."""
     import hashlib
+    import re
     csrc = os.path.join(ROOT, "paper_2606_04557_amd", "csrc")
-    data = b"".join(open(os.path.join(csrc, f), "rb").read() for f in ("cas_bf16.hip", "cas_device.h"))
-    return hashlib.sha256(data).hexdigest()[:16]
+    code = []
+    for f in ("cas_bf16.hip", "cas_device.h"):
+        text = open(os.path.join(csrc, f), encoding="utf-8").read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        for line in text.splitlines():
+            line = re.sub(r"//.*", "", line).rstrip()
+            if line.strip():
+                code.append(line)
+    return hashlib.sha256("\n".join(code).encode()).hexdigest()[:16]
 
 
 def cpu_baseline(wl, T, heads: int = 1):

@@ -1,11 +1,11 @@
 // bf16 fast path of multi-cartridge prefix attention for gfx950.
 //
 // All three kernels use 512-thread workgroups (8 waves, two per SIMD, so one
-// wave's softmax VALU work overlaps the other's MFMA work), swizzled row tiles
-// in LDS filled by asynchronous direct global->LDS copies, double buffering
-// (the copy of tile i+1 is in flight while tile i is computed; one barrier per
-// tile), and ds_read_b64_tr_b16 for every operand that is reduced along its
-// row axis (V in the forward, K in dQ, Q and dO in dK/dV).
+// wave's VALU work overlaps the other's MFMA work), swizzled row tiles in LDS
+// filled by asynchronous direct global->LDS copies and double buffering. An
+// operand reduced along its row axis comes from ds_read_b64_tr_b16 (V in the
+// forward, K in dQ) or, in dK/dV, from transposed copies of Q and dO that a
+// prologue kernel writes once per backward.
 #include <type_traits>
 #include <utility>
 
@@ -26,6 +26,9 @@ constexpr int kFastRowsPerWg = kNW * kFastRowsPerWave;   // 256
 constexpr int kDkdvLead = CAS_DKDV_LEAD;
 #ifndef CAS_DKDV_PRIO
 #define CAS_DKDV_PRIO 1
+#endif
+#ifndef CAS_DKDV_VPRIO
+#define CAS_DKDV_VPRIO 0
 #endif  // dK/dV: LDS fragments in flight ahead of their MFMA
 constexpr float kRefMargin = 64.0f;    // forward: largest score above the row's fixed offset (log2 units)
 
@@ -748,6 +751,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
   constexpr int NMF = 4 * NSTEP;               // MFMAs of a wave's matrix phase
   constexpr int LEAD = kDkdvLead, RING = LEAD + 1;
   constexpr int PRIO = CAS_DKDV_PRIO;          // wave priority during a matrix phase
+  constexpr int VPRIO = CAS_DKDV_VPRIO;        // wave priority during a VALU phase
   // One LDS arena. The P waves' matrix operands (Q rows, dO^T) fill the first
   // 4 RB bytes and the dS waves' (dO rows, Q^T) the next 4 RB, so each wave
   // reaches all of its fragments from one set of lane offsets plus 16-bit
@@ -1096,6 +1100,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
     // into pk and published to the SIMD's dS wave. piece(n) issues copy
     // instruction n, spread over the elements.
     auto p_valu = [&](auto CAUSAL, int blk, const float *lsb, auto &&piece) __attribute__((always_inline)) {
+      if constexpr (VPRIO != 0) __builtin_amdgcn_s_setprio(VPRIO);
       constexpr bool CA = decltype(CAUSAL)::value;
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub) {
@@ -1121,10 +1126,12 @@ void dkdv_bf16_kernel(DkdvParams p) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) *reinterpret_cast<bf16x8 *>(xme + t * 1024) = pk[t];
       fence_regs(pk);
+      if constexpr (VPRIO != 0) __builtin_amdgcn_s_setprio(0);
     };
     // dS wave VALU phase: dS = P (dP - D) of a block from the published P and
     // sp (dP - D); piece(n) as for the P wave.
     auto ds_valu = [&](auto &&piece) __attribute__((always_inline)) {
+      if constexpr (VPRIO != 0) __builtin_amdgcn_s_setprio(VPRIO);
       bf16x8 pv[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) pv[t] = *reinterpret_cast<const bf16x8 *>(xme + t * 1024);
@@ -1140,6 +1147,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
         pk[2 * sub + 1] = pack_bf16x8(sp[sub], 1);
       }
       fence_regs(pk);
+      if constexpr (VPRIO != 0) __builtin_amdgcn_s_setprio(0);
     };
 
     // One wave's copy batch: rows of a block of Q or dO, a transposed block,
