@@ -95,7 +95,7 @@ struct Plan {
   bool want_self_grad = false;
   // workspace layout
   size_t off_segs = 0, off_rows = 0, off_tiles = 0, off_carts = 0, off_uses = 0, table_bytes = 0;
-  size_t off_part_o = 0, off_part_lse = 0, off_ovf = 0, off_row_max = 0, ws_fwd = 0;
+  size_t off_part_o = 0, off_part_lse = 0, off_ovf = 0, ws_fwd = 0;
   size_t off_nd = 0, off_lse2 = 0, off_part_dq = 0, off_qT = 0, off_doT = 0, ws_bwd = 0;
 };
 
@@ -307,11 +307,9 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
       off = align_up(off + (size_t)pl.fwd_splits * plane * 4, 256);
     }
     if (pl.dt == kBF16) {
-      // Per-workgroup flags and per-row maxima of the exact-maximum pass.
+      // Per-workgroup flags of the exact (online-softmax) pass.
       pl.off_ovf = off;
       off = align_up(off + (size_t)pl.B * Hkv * pl.nqblk_fwd * pl.fwd_splits * 4, 256);
-      pl.off_row_max = off;
-      off = align_up(off + (size_t)pl.fwd_splits * plane * 4, 256);
     }
     pl.ws_fwd = off;
   } else {
@@ -607,7 +605,6 @@ cas_status_t cas_prefix_attn_fwd(const cas_problem_t *p, const void *q, const vo
   fp.rows = (const DevRow *)(ws + pl.off_rows);
   fp.tiles = (const DevTile *)(ws + pl.off_tiles);
   fp.ovf_flag = pl.dt == kBF16 ? (int32_t *)(ws + pl.off_ovf) : nullptr;
-  fp.row_max = pl.dt == kBF16 ? (float *)(ws + pl.off_row_max) : nullptr;
   fp.B = pl.B;
   fp.Sq = pl.Sq;
   fp.Hkv = pl.Hkv;

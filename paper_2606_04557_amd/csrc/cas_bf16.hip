@@ -30,7 +30,7 @@ constexpr int kDkdvLead = CAS_DKDV_LEAD;
 #ifndef CAS_DKDV_VPRIO
 #define CAS_DKDV_VPRIO 0
 #endif  // dK/dV: LDS fragments in flight ahead of their MFMA
-constexpr float kRefMargin = 64.0f;    // forward: largest score above the row's fixed offset (log2 units)
+constexpr int kRefMargin = 64;         // forward: row sums below 2^kRefMargin need no exact pass
 
 struct TileInfo {
   const __bf16 *kp;
@@ -163,12 +163,14 @@ struct TileTable {
 // group A's G_{i+1} reads at phase 2i+2.
 //
 // Softmax reference: a row's exponent offset m is fixed by the first tile in
-// which it sees a key, and never moved, so O is never rescaled in the loop.
-// Later scores may exceed m by up to kRefMargin (log2 units) -- P stays below
-// 2^kRefMargin, far inside fp32 and bf16 range. A row that goes beyond the
-// margin flags its workgroup; it records every row's exact maximum, and a
-// second launch (FIXUP) recomputes only the flagged workgroups with m set to
-// that maximum. Unflagged workgroups of the second launch exit at once.
+// which it sees a key (the only tile whose row maximum is computed), and never
+// moved, so O is never rescaled in the loop and later tiles need no maximum.
+// Later scores may exceed m: while the row sum stays below 2^kRefMargin every
+// P, every partial sum and O stay far inside fp32 and bf16 range. A row whose
+// sum reaches it (or overflows) flags its workgroup, and a second launch
+// (FIXUP) recomputes only the flagged workgroups with the exact online
+// softmax (running maximum, O and the sum rescaled at every tile). Unflagged
+// workgroups of the second launch exit at once.
 // ---------------------------------------------------------------------------
 template <int D, bool FIXUP>
 __global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -208,8 +210,6 @@ void fwd_bf16_kernel(FwdParams p) {
   const int my_row = row0 + n;
   const int my_t = my_row / g;
   const float c = p.scale_log2;
-  // This row's slot in the per-split row-maximum buffer.
-  const int64_t mrow = (((int64_t)split * p.B + b) * Hkv + kvh) * nrows + min(my_row, nrows - 1);
 
   // Wave-uniform tile range of this split (readfirstlane keeps it, and every
   // tile-table read that depends on it, in scalar registers).
@@ -244,11 +244,9 @@ void fwd_bf16_kernel(FwdParams p) {
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) oacc[dt] = zero16();
   // Exponent offset of this lane's row: fixed by its first visible tile, or
-  // (FIXUP) the exact row maximum the first launch recorded.
-  float m_run = FIXUP ? p.row_max[mrow] : -INFINITY;
-  float m_max = -INFINITY;    // exact running row max
+  // (FIXUP) the running row maximum.
+  float m_run = -INFINITY;
   float l_run = 0.0f;
-  bool beyond = false;        // a score exceeded m_run + kRefMargin
 
   // Group B's share of every tile copy (4 waves).
   CopyLanes<D, kKT, 4> cl;
@@ -334,6 +332,7 @@ void fwd_bf16_kernel(FwdParams p) {
       if constexpr (k + LEAD < N) sched_ds_read<(k + LEAD < NPV ? 2 : 1)>();
     });
   };
+  float alpha = 1.0f;   // FIXUP: O rescale factor of the current tile
   auto softmax = [&](auto MASK, int lim) __attribute__((always_inline)) {
     if constexpr (decltype(MASK)::value) {
       // lim: last visible key of this lane's query within the tile. Register
@@ -346,14 +345,25 @@ void fwd_bf16_kernel(FwdParams p) {
         s1[j] = 32 + crow(j, 0) <= limg ? s1[j] : -INFINITY;
       }
     }
-    float mx = -INFINITY;
+    auto tile_max = [&]() __attribute__((always_inline)) {
+      float mx = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < 16; j += 2) mx = fmaxf(fmaxf(mx, fmaxf(s0[j], s1[j])), fmaxf(s0[j + 1], s1[j + 1]));
-    const float mt = fmaxf(mx, xor32(mx)) * c;
+      for (int j = 0; j < 16; j += 2) mx = fmaxf(fmaxf(mx, fmaxf(s0[j], s1[j])), fmaxf(s0[j + 1], s1[j + 1]));
+      return fmaxf(mx, xor32(mx)) * c;
+    };
     if constexpr (!FIXUP) {
-      m_run = (m_run == -INFINITY) ? mt : m_run;
-      beyond = beyond || (mt > m_run + kRefMargin);
-      m_max = fmaxf(m_max, mt);
+      // Only until every row of the wave has seen a key.
+      if (wave_any(m_run == -INFINITY)) {
+        const float mt = tile_max();
+        m_run = (m_run == -INFINITY) ? mt : m_run;
+      }
+    } else {
+      // Running maximum; the sum is rescaled here, O by the caller (outside
+      // its branches, so the accumulators are written in one place).
+      const float m_new = fmaxf(m_run, tile_max());
+      alpha = (m_new == -INFINITY) ? 1.0f : fast_exp2(m_run - m_new);
+      l_run *= alpha;
+      m_run = m_new;
     }
     const float mu = (m_run == -INFINITY) ? 0.0f : m_run;
 #pragma unroll
@@ -384,7 +394,7 @@ void fwd_bf16_kernel(FwdParams p) {
   auto gphase = [&](int j, const char *kb, const char *vbp) __attribute__((always_inline)) {
     if (j <= nt && wave_active) matrix(std::true_type{}, std::true_type{}, kb, vbp);
   };
-  auto xphase = [&](int j) __attribute__((always_inline)) {
+  auto xphase_body = [&](int j) __attribute__((always_inline)) {
     if (j < 0 || j >= nt) return;
     if (!live(j)) {
 #pragma unroll
@@ -400,6 +410,14 @@ void fwd_bf16_kernel(FwdParams p) {
       softmax(std::true_type{}, lim);
     } else {
       softmax(std::false_type{}, kKT - 1);
+    }
+  };
+  auto xphase = [&](int j) __attribute__((always_inline)) {
+    if constexpr (FIXUP) alpha = 1.0f;
+    xphase_body(j);
+    if constexpr (FIXUP) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
     }
   };
 
@@ -471,11 +489,11 @@ void fwd_bf16_kernel(FwdParams p) {
     else run(std::false_type{});
   }
   if constexpr (!FIXUP) {
-    // Every wave reaches this point: flag the workgroup and keep the exact
-    // row maxima if any row went beyond the margin.
-    const int any = __syncthreads_or(beyond ? 1 : 0);
+    // Every wave reaches this point: flag the workgroup if a row sum reached
+    // 2^kRefMargin or overflowed (exponent field also catches inf and NaN).
+    const unsigned eb = (__float_as_uint(l_run) >> 23) & 0xffu;
+    const int any = __syncthreads_or(eb >= 127u + (unsigned)kRefMargin ? 1 : 0);
     if (tid == 0) p.ovf_flag[blockIdx.x] = any;
-    if (any && my_row < nrows && G == 0) p.row_max[mrow] = m_max;
   }
 
   const float lt = l_run + xor32(l_run);

@@ -78,7 +78,6 @@ struct FwdParams {
   const DevRow *rows;
   const DevTile *tiles;
   int32_t *ovf_flag;  // [grid] bf16: workgroup needs the exact-maximum pass
-  float *row_max;     // [splits][B][Hkv][nrows] bf16: exact row maxima (log2 units)
   int32_t B, Sq, Hkv, g, nrows, nqblk, splits;
   float scale_log2;   // softmax_scale * log2(e)
 };

@@ -151,6 +151,44 @@ def test_canaries_and_determinism():
     assert rel_err(host(outs["dq"]), rdq) <= TOL["bf16"]
 
 
+@pytest.mark.parametrize("splits", [0, 4])
+def test_score_spike_takes_exact_pass(splits):
+    """A key late in a row whose scores sit far above everything the row saw
+    first (more than 64 in log2 units) pushes the forward past its fixed
+    softmax offset: the workgroup is recomputed by the exact online-softmax
+    pass. O, LSE and all gradients must still match the oracle."""
+    import paper_2606_04557_amd as cas
+    wl = casgen.custom("probe", seed=305, cart_std=0.5, **PROBE)
+    T = casgen.make_tensors(wl)
+    q = casgen.to_float(T["q"], "bf16")
+    # Row 0's last cartridge (id 2, 200 tokens): token 150 of every KV head is
+    # aligned with query position 0 of that head's first query head, 60x its
+    # unit direction, so those queries score about 60 |q| ~ 680 above zero.
+    c, tok = wl.rows[0][-1], 150
+    k = casgen.to_float(T["cart_k"][c], "bf16")
+    for h in range(wl.num_kv_heads):
+        qv = q[0, 0, h * wl.group_size]
+        k[tok, h] = 60.0 * qv / np.linalg.norm(qv)
+    T["cart_k"][c] = casgen.rng.f64_to_bf16_bits(k)
+    spike = float(casgen.to_float(T["cart_k"][c], "bf16")[tok, 0] @ q[0, 0, 0]) * float(wl.scale)
+    assert spike / math.log(2) > 64 + 20          # far beyond the margin
+    case = GpuCase(wl, tensors=T)
+    try:
+        cas.set_tuning(fwd_splits=splits)
+        o, lse = case.fwd()
+    finally:
+        cas.set_tuning(0, 0)
+    dq, _, _ = case.bwd(o, lse)
+    _torch().cuda.synchronize()
+    O, LSE, (rdq, _, _, rdk, rdv) = full_oracle(case)
+    assert rel_err(host(o), O) <= TOL["bf16"]
+    assert float(np.abs(host(lse) - LSE).max()) <= 1e-3
+    assert rel_err(host(dq), rdq) <= TOL["bf16"]
+    for cc in case.dk:
+        assert rel_err(host(case.dk[cc]), rdk[cc]) <= TOL["bf16"]
+        assert rel_err(host(case.dv[cc]), rdv[cc]) <= TOL["bf16"]
+
+
 def test_order_invariance_and_concatenation():
     """Reordering a row's cartridges, or joining them into one cartridge, leaves O, LSE
     and dQ unchanged up to rounding and moves each cartridge's gradient with it."""
