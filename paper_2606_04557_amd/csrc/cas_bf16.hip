@@ -86,12 +86,15 @@ struct CopyLanes {
   // tile's rows (an out-of-range offset would read zeros, not fault), and
   // as MUBUF LDS loads they are counted on vmcnt alone.
   __device__ __forceinline__ void issue(char *tile, const __bf16 *base, int st, int nvalid, int wave) const {
-    const BufRsrc rs = make_rsrc(base, ((nvalid - 1) * st + D) * 2);
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int inst = wave + i * NW;
-      if (NI % NW == 0 || inst < NI) dma16(rs, (min(row[i], nvalid - 1) * st + coff[i]) * 2, tile + inst * 1024);
-    }
+    for (int i = 0; i < PER; ++i) issue_one(tile, base, st, nvalid, wave, i);
+  }
+  // Instruction i (< PER) of this wave's share only.
+  __device__ __forceinline__ void issue_one(char *tile, const __bf16 *base, int st, int nvalid, int wave,
+                                            int i) const {
+    const BufRsrc rs = make_rsrc(base, ((nvalid - 1) * st + D) * 2);
+    const int inst = wave + i * NW;
+    if (NI % NW == 0 || inst < NI) dma16(rs, (min(row[i], nvalid - 1) * st + coff[i]) * 2, tile + inst * 1024);
   }
 };
 
@@ -101,6 +104,18 @@ template <typename T, int N>
 __device__ __forceinline__ void fence_regs(T (&v)[N]) {
 #pragma unroll
   for (int i = 0; i < N; ++i) asm volatile("" : "+v"(v[i]));
+}
+
+// XCD-aware workgroup order. Consecutive workgroup ids are dispatched
+// round-robin over the 8 XCDs (each with its own L2); this remaps them so
+// that each XCD receives one contiguous range of logical ids. Workgroups that
+// stream the same K/V tiles (same batch row and KV head, adjacent logical
+// ids) then share one L2 instead of fetching every tile once per XCD.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int xcd_order(int bid, int n) {
+  const int per = n / kXcds;
+  if (bid >= per * kXcds) return bid;   // the remainder keeps its id
+  return (bid % kXcds) * per + bid / kXcds;
 }
 
 // Workgroup barrier that orders LDS use: this wave's LDS reads have returned,
@@ -188,7 +203,7 @@ void fwd_bf16_kernel(FwdParams p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2;
   const int G = lane >> 5, n = lane & 31;
-  int bid = blockIdx.x;
+  int bid = xcd_order(blockIdx.x, gridDim.x);
   const int qblk = __builtin_amdgcn_readfirstlane(bid % p.nqblk);
   bid /= p.nqblk;
   const int kvh = __builtin_amdgcn_readfirstlane(bid % p.Hkv);
@@ -539,7 +554,7 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = lane >> 5, n = lane & 31;
-  int bid = blockIdx.x;
+  int bid = xcd_order(blockIdx.x, gridDim.x);
   const int qblk = __builtin_amdgcn_readfirstlane(bid % p.nqblk);
   bid /= p.nqblk;
   const int kvh = __builtin_amdgcn_readfirstlane(bid % p.Hkv);
@@ -596,23 +611,48 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
   TileTable tt;
   tt.init(p.tiles, row, kvh);
 
+  // Tile copies, issued piece by piece inside the previous tile's compute
+  // (a burst of copy instructions would stall the issuing wave): piece n is
+  // K instruction n (n < PER) or V instruction n - PER.
+  CopyLanes<D, kKT, kNW> cl;
+  cl.init(wave, lane);
+  constexpr int PER = CopyLanes<D, kKT, kNW>::PER;
+  auto piece = [&](const TileInfo &ti, char *kb, char *vb, int n) __attribute__((always_inline)) {
+    if (n < PER) cl.issue_one(kb, ti.kp, ti.st, ti.nvalid, wave, n);
+    else cl.issue_one(vb, ti.vp, ti.st, ti.nvalid, wave, n - PER);
+  };
   auto issue = [&](const TileInfo &ti, char *kb, char *vb) __attribute__((always_inline)) {
-    dma_tile<D, kKT, kNW>(kb, ti.kp, [&](int r) { return r * ti.st; }, ti.nvalid, wave, lane);
-    dma_tile<D, kKT, kNW>(vb, ti.vp, [&](int r) { return r * ti.st; }, ti.nvalid, wave, lane);
+#pragma unroll
+    for (int n = 0; n < 2 * PER; ++n) piece(ti, kb, vb, n);
   };
 
-  auto compute = [&](const TileInfo &ti, const char *kb, const char *vb) __attribute__((always_inline)) {
-    if (!wave_active) return;
-    if (ti.self0 >= 0 && ti.self0 > wave_t_hi) return;
+  // compute(ti, ...) issues copy pieces 2h and 2h+1 of the next tile after
+  // half h's score products; with no next tile, or when this wave skips the
+  // tile, the pieces go first.
+  auto compute = [&](const TileInfo &ti, const char *kb, const char *vb, auto &&next) __attribute__((always_inline)) {
+    static_assert(2 * PER <= 4, "at most four copy pieces per tile");
+    auto at = [&](int point) __attribute__((always_inline)) {
+      if (point < 2 * PER) next(point);
+    };
+    if (!wave_active || (ti.self0 >= 0 && ti.self0 > wave_t_hi)) {
+#pragma unroll
+      for (int n = 0; n < 2 * PER; ++n) next(n);
+      return;
+    }
     const bool need_mask = (ti.nvalid < kKT) || (ti.self0 >= 0 && ti.self0 + kKT - 1 > wave_t_lo);
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
-      f32x16 sa = zero16(), dpa = zero16();
+      // dP accumulates onto -D, so the MFMAs deliver dP - D.
+      f32x16 sa = zero16(), dpa;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) dpa[j] = ndr;
 #pragma unroll
       for (int st = 0; st < NSTEP; ++st) {
         sa = Mma<__bf16>::run(row_frag_at<D>(kb, ro, 32 * sub, st), qf[st], sa);
         dpa = Mma<__bf16>::run(row_frag_at<D>(vb, ro, 32 * sub, st), df[st], dpa);
       }
+      at(2 * sub);
+      at(2 * sub + 1);
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         float pv = fast_exp2(fmaf(sa[j], c, -lse2r));
@@ -621,7 +661,7 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
           const bool ok = key < ti.nvalid && (ti.self0 < 0 || ti.self0 + key <= my_t);
           pv = ok ? pv : 0.0f;
         }
-        sa[j] = pv * (dpa[j] + ndr);
+        sa[j] = pv * dpa[j];
       }
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
@@ -638,21 +678,23 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
     issue(cur, kb0, vb0);
     __syncthreads();
     for (int it = tb; it < te; it += 2) {
+      // compute runs unconditionally (a branch around it would make the
+      // register allocator copy the accumulators); only the copies are
+      // conditional.
       TileInfo nxt;
       const bool has1 = it + 1 < te;
-      if (has1) {
-        nxt = tt.at(it + 1);
-        issue(nxt, kb1, vb1);
-      }
-      compute(cur, kb0, vb0);
+      if (has1) nxt = tt.at(it + 1);
+      compute(cur, kb0, vb0, [&](int n) __attribute__((always_inline)) {
+        if (has1) piece(nxt, kb1, vb1, n);
+      });
       __syncthreads();
       if (!has1) break;
       const bool has2 = it + 2 < te;
-      if (has2) {
-        cur = tt.at(it + 2);
-        issue(cur, kb0, vb0);
-      }
-      compute(nxt, kb1, vb1);
+      const TileInfo prev = nxt;
+      if (has2) cur = tt.at(it + 2);
+      compute(prev, kb1, vb1, [&](int n) __attribute__((always_inline)) {
+        if (has2) piece(cur, kb0, vb0, n);
+      });
       __syncthreads();
     }
   }
