@@ -79,6 +79,14 @@ SMALL = [
          head_dim=128, cart_lens=[70, 129], rows=[[0, 1], [1, 0], [0, 0]]),
     dict(name="no_prefix", dtype="bf16", batch=2, q_len=257, num_q_heads=4, num_kv_heads=2,
          head_dim=128, cart_lens=[], rows=[[], []]),
+    # GQA groups of 8 and 16 (a 64-row block starts on a position boundary)
+    # and of 5 (it does not), with d = 64 and 128
+    dict(name="g8_d64", dtype="bf16", batch=1, q_len=100, num_q_heads=16, num_kv_heads=2,
+         head_dim=64, cart_lens=[150, 77], rows=[[0, 1]], layouts=["padded", "head"]),
+    dict(name="g16", dtype="bf16", batch=2, q_len=50, num_q_heads=16, num_kv_heads=1,
+         head_dim=128, cart_lens=[300, 65], rows=[[0], [1, 0]]),
+    dict(name="g5_d64", dtype="bf16", batch=1, q_len=45, num_q_heads=10, num_kv_heads=2,
+         head_dim=64, cart_lens=[90, 40], rows=[[1, 0]]),
     dict(name="fp32_d128", dtype="fp32", batch=1, q_len=33, num_q_heads=4, num_kv_heads=2,
          head_dim=128, cart_lens=[65, 3], rows=[[0, 1]]),
     dict(name="fp32_alias", dtype="fp32", batch=2, q_len=20, num_q_heads=2, num_kv_heads=1,
