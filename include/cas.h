@@ -116,7 +116,9 @@ typedef struct {
  * (backward != 0) call on this problem needs, written to *bytes. The size
  * depends only on the problem and the current tuning (cas_set_tuning), not on
  * the device. Workspace is caller-owned, 256-byte aligned, and may be reused
- * by the next call once the stream has passed the previous one.
+ * by the next call once the stream has passed the previous one. Besides the
+ * segment tables and per-row statistics, a bf16 backward keeps a transposed
+ * copy of q and d_o in it (about twice the bytes of q).
  */
 cas_status_t cas_prefix_attn_workspace_size(const cas_problem_t *p, int backward, size_t *bytes);
 

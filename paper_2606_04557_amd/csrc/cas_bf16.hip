@@ -20,16 +20,8 @@ constexpr int kFastThreads = kNW * 64;
 constexpr int kKT = 64;                // keys per tile (forward, dQ)
 constexpr int kFastRowsPerWave = 32;
 constexpr int kFastRowsPerWg = kNW * kFastRowsPerWave;   // 256
-#ifndef CAS_DKDV_LEAD
-#define CAS_DKDV_LEAD 4
-#endif
-constexpr int kDkdvLead = CAS_DKDV_LEAD;
-#ifndef CAS_DKDV_PRIO
-#define CAS_DKDV_PRIO 1
-#endif
-#ifndef CAS_DKDV_VPRIO
-#define CAS_DKDV_VPRIO 0
-#endif  // dK/dV: LDS fragments in flight ahead of their MFMA
+constexpr int kDkdvLead = 4;           // dK/dV: LDS fragments in flight ahead of their MFMA
+constexpr int kDkdvPrio = 1;           // dK/dV: wave priority in a matrix phase (0 in VALU phases)
 constexpr int kRefMargin = 64;         // forward: row sums below 2^kRefMargin need no exact pass
 
 struct TileInfo {
@@ -810,8 +802,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
   constexpr int RB = QB * D * 2;               // bytes of one 64 x D block
   constexpr int NMF = 4 * NSTEP;               // MFMAs of a wave's matrix phase
   constexpr int LEAD = kDkdvLead, RING = LEAD + 1;
-  constexpr int PRIO = CAS_DKDV_PRIO;          // wave priority during a matrix phase
-  constexpr int VPRIO = CAS_DKDV_VPRIO;        // wave priority during a VALU phase
+  constexpr int PRIO = kDkdvPrio;
   // One LDS arena. The P waves' matrix operands (Q rows, dO^T) fill the first
   // 4 RB bytes and the dS waves' (dO rows, Q^T) the next 4 RB, so each wave
   // reaches all of its fragments from one set of lane offsets plus 16-bit
@@ -1160,7 +1151,6 @@ void dkdv_bf16_kernel(DkdvParams p) {
     // into pk and published to the SIMD's dS wave. piece(n) issues copy
     // instruction n, spread over the elements.
     auto p_valu = [&](auto CAUSAL, int blk, const float *lsb, auto &&piece) __attribute__((always_inline)) {
-      if constexpr (VPRIO != 0) __builtin_amdgcn_s_setprio(VPRIO);
       constexpr bool CA = decltype(CAUSAL)::value;
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub) {
@@ -1186,12 +1176,10 @@ void dkdv_bf16_kernel(DkdvParams p) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) *reinterpret_cast<bf16x8 *>(xme + t * 1024) = pk[t];
       fence_regs(pk);
-      if constexpr (VPRIO != 0) __builtin_amdgcn_s_setprio(0);
     };
     // dS wave VALU phase: dS = P (dP - D) of a block from the published P and
     // sp (dP - D); piece(n) as for the P wave.
     auto ds_valu = [&](auto &&piece) __attribute__((always_inline)) {
-      if constexpr (VPRIO != 0) __builtin_amdgcn_s_setprio(VPRIO);
       bf16x8 pv[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) pv[t] = *reinterpret_cast<const bf16x8 *>(xme + t * 1024);
@@ -1207,7 +1195,6 @@ void dkdv_bf16_kernel(DkdvParams p) {
         pk[2 * sub + 1] = pack_bf16x8(sp[sub], 1);
       }
       fence_regs(pk);
-      if constexpr (VPRIO != 0) __builtin_amdgcn_s_setprio(0);
     };
 
     // One wave's copy batch: rows of a block of Q or dO, a transposed block,
