@@ -84,7 +84,10 @@ struct CopyLanes {
   // Instruction i (< PER) of this wave's share only.
   __device__ __forceinline__ void issue_one(char *tile, const __bf16 *base, int st, int nvalid, int wave,
                                             int i) const {
-    const BufRsrc rs = make_rsrc(base, ((nvalid - 1) * st + D) * 2);
+    issue_rs(tile, make_rsrc(base, ((nvalid - 1) * st + D) * 2), st, nvalid, wave, i);
+  }
+  // The same through a given resource (an empty one writes zeros).
+  __device__ __forceinline__ void issue_rs(char *tile, BufRsrc rs, int st, int nvalid, int wave, int i) const {
     const int inst = wave + i * NW;
     if (NI % NW == 0 || inst < NI) dma16(rs, (min(row[i], nvalid - 1) * st + coff[i]) * 2, tile + inst * 1024);
   }
@@ -259,6 +262,8 @@ void fwd_bf16_kernel(FwdParams p) {
   CopyLanes<D, kKT, 4> cl;
   cl.init(wave & 3, lane);
   constexpr int kCopyInst = CopyLanes<D, kKT, 4>::PER;   // per wave per K or V tile
+  constexpr int kPieces = 2 * kCopyInst;                   // copy instructions per softmax phase
+  static_assert(16 % kPieces == 0, "copy pieces spread over the 16 exponential pairs");
 
   // Scores of the tile between its G and X phases; P of the tile between its
   // X phase and the next G phase.
@@ -340,7 +345,9 @@ void fwd_bf16_kernel(FwdParams p) {
     });
   };
   float alpha = 1.0f;   // FIXUP: O rescale factor of the current tile
-  auto softmax = [&](auto MASK, int lim) __attribute__((always_inline)) {
+  // piece(n), n < kPieces: copy instruction n of the phase (group B's tile
+  // copies), spread evenly over the exponentials.
+  auto softmax = [&](auto MASK, int lim, auto &&piece) __attribute__((always_inline)) {
     if constexpr (decltype(MASK)::value) {
       // lim: last visible key of this lane's query within the tile. Register
       // j of group G holds key crow(j, G) = crow(j, 0) + 4G, so comparing
@@ -377,6 +384,11 @@ void fwd_bf16_kernel(FwdParams p) {
     for (int j = 0; j < 16; ++j) {
       s0[j] = fast_exp2(fmaf(s0[j], c, -mu));
       s1[j] = fast_exp2(fmaf(s1[j], c, -mu));
+      constexpr int EPP = 16 / kPieces;
+      if (j % EPP == EPP - 1) {
+        asm volatile("" : "+v"(s0[j]), "+v"(s1[j]));   // keep the copies spread
+        piece(j / EPP);
+      }
     }
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
@@ -401,27 +413,35 @@ void fwd_bf16_kernel(FwdParams p) {
   auto gphase = [&](int j, const char *kb, const char *vbp) __attribute__((always_inline)) {
     if (j <= nt && wave_active) matrix(std::true_type{}, std::true_type{}, kb, vbp);
   };
-  auto xphase_body = [&](int j) __attribute__((always_inline)) {
-    if (j < 0 || j >= nt) return;
+  auto xphase_body = [&](int j, auto &&piece) __attribute__((always_inline)) {
+    auto all_pieces = [&]() __attribute__((always_inline)) {
+#pragma unroll
+      for (int n = 0; n < kPieces; ++n) piece(n);
+    };
+    if (j < 0 || j >= nt) {
+      all_pieces();
+      return;
+    }
     if (!live(j)) {
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
         for (int s = 0; s < 2; ++s) pf[a][s] = Mma<__bf16>::zero();
+      all_pieces();
       return;
     }
     const int self0 = self0_of(j);
     const int nvalid = __builtin_amdgcn_readfirstlane(tt.nvalid(tb + j));
     if (nvalid < kKT || (self0 >= 0 && self0 + kKT - 1 > wave_t_lo)) {
       const int lim = self0 < 0 ? nvalid - 1 : min(nvalid - 1, my_t - self0);
-      softmax(std::true_type{}, lim);
+      softmax(std::true_type{}, lim, piece);
     } else {
-      softmax(std::false_type{}, kKT - 1);
+      softmax(std::false_type{}, kKT - 1, piece);
     }
   };
-  auto xphase = [&](int j) __attribute__((always_inline)) {
+  auto xphase = [&](int j, auto &&piece) __attribute__((always_inline)) {
     if constexpr (FIXUP) alpha = 1.0f;
-    xphase_body(j);
+    xphase_body(j, piece);
     if constexpr (FIXUP) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
@@ -435,16 +455,21 @@ void fwd_bf16_kernel(FwdParams p) {
     tk = tt.at(tb + j);
     cl.issue(kbn, tk.kp, tk.st, tk.nvalid, wave & 3);
   };
-  // Phase 2i: K_{i+2} and V_{i+1}; then the copies of phase 2i-2 are waited for.
-  auto issue = [&](int i, char *kbn, char *vbn) __attribute__((always_inline)) {
-    if (i + 1 < nt) cl.issue(vbn, tk.vp, tk.st, tk.nvalid, wave & 3);
-    if (i + 2 < nt) copy_k(kbn, i + 2);
-  };
-  auto wait_older = [&](int i) __attribute__((always_inline)) {
-    // The newest batch (issued this phase) may still be in flight.
-    if (i + 2 < nt) wait_vmcnt<2 * kCopyInst>();
-    else if (i + 1 < nt) wait_vmcnt<kCopyInst>();
-    else wait_vmcnt<0>();
+  auto no_piece = [](int) {};
+  // Phase 2i: V_{i+1} and K_{i+2}, spread over the softmax of tile i-1 (copies
+  // past the last tile go through an empty resource and write zeros into
+  // buffers nothing reads); at its end the copies of phase 2i-2 are waited for.
+  auto even_b = [&](int i, char *kbn, char *vbn) __attribute__((always_inline)) {
+    const TileInfo tv = tk;                                   // tile i+1 (or the last)
+    const TileInfo tn = tt.at(tb + min(i + 2, nt - 1));
+    const BufRsrc rv = make_rsrc(tv.vp, i + 1 < nt ? ((tv.nvalid - 1) * tv.st + D) * 2 : 0);
+    const BufRsrc rk = make_rsrc(tn.kp, i + 2 < nt ? ((tn.nvalid - 1) * tn.st + D) * 2 : 0);
+    xphase(i - 1, [&](int n) __attribute__((always_inline)) {
+      if (n < kCopyInst) cl.issue_rs(vbn, rv, tv.st, tv.nvalid, wave & 3, n);
+      else cl.issue_rs(kbn, rk, tn.st, tn.nvalid, wave & 3, n - kCopyInst);
+    });
+    tk = tn;
+    wait_vmcnt<2 * kCopyInst>();
   };
 
   if (nt > 0) {
@@ -467,17 +492,12 @@ void fwd_bf16_kernel(FwdParams p) {
     auto run = [&](auto GROUP_A) __attribute__((always_inline)) {
       constexpr bool A = decltype(GROUP_A)::value;
       auto even = [&](int i, const char *kbi, const char *vbp, char *kbn, char *vbn) __attribute__((always_inline)) {
-        if constexpr (A) {
-          gphase(i, kbi, vbp);
-        } else {
-          issue(i, kbn, vbn);
-          xphase(i - 1);
-          wait_older(i);
-        }
+        if constexpr (A) gphase(i, kbi, vbp);
+        else even_b(i, kbn, vbn);
         lds_barrier();
       };
       auto odd = [&](int i, const char *kbi, const char *vbp) __attribute__((always_inline)) {
-        if constexpr (A) xphase(i);
+        if constexpr (A) xphase(i, no_piece);
         else gphase(i, kbi, vbp);
         lds_barrier();
       };
@@ -494,6 +514,7 @@ void fwd_bf16_kernel(FwdParams p) {
     };
     if (grp == 0) run(std::true_type{});
     else run(std::false_type{});
+    wait_vmcnt<0>();
   }
   if constexpr (!FIXUP) {
     // Every wave reaches this point: flag the workgroup if a row sum reached
