@@ -5,4 +5,4 @@ shapes, seeded random bits and the benchmark configurations. No attention
 arithmetic lives here.
 """
 from . import rng  # noqa: F401
-from .workloads import Workload, config, custom, make_tensors, to_float  # noqa: F401
+from .workloads import Workload, config, custom, make_tensors, packed, to_float  # noqa: F401

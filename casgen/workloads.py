@@ -45,6 +45,19 @@ class Workload:
     staged: Optional[List[int]] = None    # cartridge ids staged host -> HBM
     forward_only: bool = False
     description: str = ""
+    q_lens: Optional[List[int]] = None    # packed samples: per-row query tokens (q_len is 0)
+
+    @property
+    def packed(self) -> bool:
+        return self.q_lens is not None
+
+    @property
+    def row_lens(self) -> List[int]:
+        return list(self.q_lens) if self.packed else [self.q_len] * self.batch
+
+    @property
+    def q_offsets(self) -> List[int]:
+        return [0] + [int(x) for x in np.cumsum(self.row_lens)]
 
     @property
     def group_size(self) -> int:
@@ -60,9 +73,8 @@ class Workload:
     def visible_pairs(self) -> int:
         """Visible (query, key) pairs summed over query heads: each query
         sees its row's whole prefix plus self keys 0..t."""
-        sq = self.q_len
         tot = 0
-        for b in range(self.batch):
+        for b, sq in enumerate(self.row_lens):
             tot += sq * self.prefix_len(b) + sq * (sq + 1) // 2
         return tot * self.num_q_heads
 
@@ -125,6 +137,46 @@ def config(n: int) -> Workload:
     raise ValueError(f"no config {n}")
 
 
+def packed(seed: int = 6, total: int = 8192, pool: int = 20, k_max: int = 10,
+           p_iso: float = 0.75) -> Workload:
+    """Packed multi-sample training layout (paper: Section "Training with
+    Multiple Cartridges", Eq. mixing, and the hyperparameter table: packed
+    sequences of 8,192 tokens, a GPU pool of B = 20 cartridges, isolation
+    probability 0.75, up to 10 distractors per example).
+
+    Synthetic recipe (the paper fixes none of these lengths): cartridge
+    lengths uniform on [256, 2048] in multiples of 16 (the page size); sample
+    lengths uniform on [256, 2048], packed until ``total`` tokens (the last
+    sample cut to fit); each sample draws a target from the pool and, with
+    probability 1 - p_iso, k ~ U{1..k_max} distinct distractors, all in a
+    shuffled order. bf16, 32 query heads, 8 KV heads, d = 128."""
+    lens = [16 * int(x) for x in rng.randint(rng.stream_key(seed, rng.TAG_LENGTHS), pool, 16, 128)]
+    q_lens: List[int] = []
+    draws = rng.randint(rng.stream_key(seed, rng.TAG_LENGTHS, 1), 64, 256, 2048)
+    for x in draws:
+        room = total - sum(q_lens)
+        if room <= 0:
+            break
+        q_lens.append(int(min(int(x), room)))
+    assert sum(q_lens) == total
+    rows = []
+    for b in range(len(q_lens)):
+        u = rng.uniform(rng.stream_key(seed, rng.TAG_SELECT, b), 3)
+        target = int(np.floor(u[0] * pool))
+        k = 0 if u[1] < p_iso else 1 + int(np.floor(u[2] * k_max))
+        others = [c for c in range(pool) if c != target]
+        pick = [others[i] for i in rng.choose_distinct(rng.stream_key(seed, rng.TAG_SELECT, b, 1),
+                                                       pool - 1, k)]
+        order = rng.choose_distinct(rng.stream_key(seed, rng.TAG_SELECT, b, 2), k + 1, k + 1)
+        ids = [target] + pick
+        rows.append([ids[i] for i in order])
+    return Workload(
+        name="P8K", dtype="bf16", batch=len(q_lens), q_len=0, num_q_heads=32, num_kv_heads=8,
+        head_dim=128, cart_lens=lens, rows=rows, seed=seed, cart_std=0.5, q_lens=q_lens,
+        description=f"bf16 packed training layout: {len(q_lens)} samples in {total} tokens, each over "
+                    f"its own subset of a {pool}-cartridge pool (target + up to {k_max} distractors)")
+
+
 def custom(name: str, dtype: str, batch: int, q_len: int, num_q_heads: int,
            num_kv_heads: int, head_dim: int, cart_lens: List[int],
            rows: List[List[int]], seed: int, **kw) -> Workload:
@@ -153,18 +205,21 @@ def make_tensors(wl: Workload, carts: Optional[List[int]] = None,
     each cartridge has its own substream, so the subset does not change the
     bits of the ones drawn.
     """
-    B, Sq, Hq, Hkv, D = wl.batch, wl.q_len, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+    B, Hq, Hkv, D = wl.batch, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
     s = wl.seed
+    lens = wl.row_lens
+    # Fixed-length rows stack to [B, Sq, H, D]; packed samples concatenate to [T, H, D].
+    join = np.concatenate if wl.packed else np.stack
+
+    def per_row(tag, H, std):
+        return join([_draw(rng.stream_key(s, tag, b), (lens[b], H, D), std, wl.dtype) for b in range(B)])
+
     out: Dict[str, object] = {}
-    out["q"] = np.stack([_draw(rng.stream_key(s, rng.TAG_Q, b), (Sq, Hq, D), wl.q_std, wl.dtype)
-                         for b in range(B)])
-    out["k_self"] = np.stack([_draw(rng.stream_key(s, rng.TAG_K_SELF, b), (Sq, Hkv, D),
-                                    wl.self_std, wl.dtype) for b in range(B)])
-    out["v_self"] = np.stack([_draw(rng.stream_key(s, rng.TAG_V_SELF, b), (Sq, Hkv, D),
-                                    wl.self_std, wl.dtype) for b in range(B)])
+    out["q"] = per_row(rng.TAG_Q, Hq, wl.q_std)
+    out["k_self"] = per_row(rng.TAG_K_SELF, Hkv, wl.self_std)
+    out["v_self"] = per_row(rng.TAG_V_SELF, Hkv, wl.self_std)
     if with_grad_out and not wl.forward_only:
-        out["d_o"] = np.stack([_draw(rng.stream_key(s, rng.TAG_DO, b), (Sq, Hq, D), wl.do_std,
-                                     wl.dtype) for b in range(B)])
+        out["d_o"] = per_row(rng.TAG_DO, Hq, wl.do_std)
     want = range(len(wl.cart_lens)) if carts is None else carts
     ck: List[Optional[np.ndarray]] = [None] * len(wl.cart_lens)
     cv: List[Optional[np.ndarray]] = [None] * len(wl.cart_lens)

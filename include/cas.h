@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define CAS_ABI_VERSION 1
+#define CAS_ABI_VERSION 2
 
 typedef enum {
   CAS_OK = 0,
@@ -89,12 +89,26 @@ typedef struct {
  * Problem description, read only during the call (the host arrays may be
  * reused as soon as the call returns).
  *
+ * Two query layouts. With q_offsets == NULL every batch row has q_len >= 1
+ * query tokens (fixed-length batch). Otherwise the batch rows are packed
+ * samples of different lengths (the training layout in which several
+ * conversations, each with its own cartridges, share one token axis;
+ * paper: Section "Training with Multiple Cartridges" and Eq. mixing):
+ * q_offsets is a host array of batch+1 non-decreasing int32 with
+ * q_offsets[0] == 0, row b owns tokens q_offsets[b] .. q_offsets[b+1]-1 of a
+ * token axis of T = q_offsets[batch] >= 1 tokens, q_len must be 0, and each
+ * row's self keys are its own tokens only (block-diagonal causal masking).
+ * Rows may be empty. In both layouts let T be the token count (batch*q_len
+ * when fixed) and Hq = num_kv_heads*group_size.
+ *
  * Shapes (contiguous, in elements of dtype):
- *   q, o, d_o, dq:                [batch, q_len, num_kv_heads*group_size, head_dim]
- *   k_self, v_self, dk_self, dv_self: [batch, q_len, num_kv_heads, head_dim]
- *   lse (always float32, natural log): [batch, num_kv_heads*group_size, q_len]
+ *   q, o, d_o, dq:                    [T, Hq, head_dim]
+ *   k_self, v_self, dk_self, dv_self: [T, num_kv_heads, head_dim]
+ *   lse (always float32, natural log): [batch, Hq, q_len] (fixed) or [Hq, T] (packed)
+ * (a fixed-length batch is [batch, q_len, ...] in these terms).
  * Query head h reads kv head h / group_size (contiguous GQA groups).
- * head_dim is 64 or 128. softmax_scale must be finite and > 0.
+ * head_dim is 64 or 128. softmax_scale must be finite and > 0. T * Hq must
+ * stay below 2^31.
  * seg_offsets is a host array of batch+1 non-decreasing int32 with
  * seg_offsets[0] == 0; row b uses segments[seg_offsets[b] .. seg_offsets[b+1]).
  * segments may be NULL when seg_offsets[batch] == 0.
@@ -109,6 +123,7 @@ typedef struct {
   float softmax_scale;
   const cas_segment_t *segments;
   const int32_t *seg_offsets;
+  const int32_t *q_offsets; /* NULL (fixed q_len per row) or batch+1 token offsets (packed) */
 } cas_problem_t;
 
 /*

@@ -11,6 +11,10 @@ from .attention import (  # noqa: F401
     head_forward,
     key_grads,
     key_grads_many,
+    packed_backward,
+    packed_forward,
+    packed_key_grads_many,
+    packed_rows_forward_backward,
     row_keys,
     rows_forward_backward,
     visible_mask,

@@ -268,3 +268,112 @@ def key_grads_many(q, k_self, v_self, cart_k, cart_v, rows, scale, group_size, d
                     out[i][0][:] += dk
                     out[i][1][:] += dv
     return out
+
+
+# ---------------------------------------------------------------------------
+# Packed samples (paper: Section "Training with Multiple Cartridges" and Eq.
+# mixing: every training example carries its own target and distractor
+# cartridges). Several samples share one token axis; sample b owns tokens
+# q_offsets[b] .. q_offsets[b+1]-1 and attends over its own cartridges, then
+# causally over its own tokens only (block-diagonal self). Each sample is the
+# single-row problem above; a cartridge that several samples reference gets
+# the sum of their gradients.
+# ---------------------------------------------------------------------------
+
+def _sample(x, a: int, e: int):
+    return _f64(x)[None, a:e]
+
+
+def packed_forward(q, k_self, v_self, cart_k: Sequence, cart_v: Sequence,
+                   rows: Sequence[Sequence[int]], q_offsets: Sequence[int], scale: float,
+                   group_size: int):
+    """O [T, Hq, D] and LSE [Hq, T] of packed samples (q [T, Hq, D], k_self and
+    v_self [T, Hkv, D])."""
+    q = _f64(q)
+    T, Hq, Dh = q.shape
+    O = np.zeros((T, Hq, Dh))
+    LSE = np.zeros((Hq, T))
+    for b in range(len(rows)):
+        a, e = int(q_offsets[b]), int(q_offsets[b + 1])
+        if e == a:
+            continue
+        o, lse = forward(q[None, a:e], _sample(k_self, a, e), _sample(v_self, a, e), cart_k, cart_v,
+                         [rows[b]], scale, group_size)
+        O[a:e] = o[0]
+        LSE[:, a:e] = lse[0]
+    return O, LSE
+
+
+def packed_backward(q, k_self, v_self, cart_k: Sequence, cart_v: Sequence,
+                    rows: Sequence[Sequence[int]], q_offsets: Sequence[int], scale: float,
+                    group_size: int, d_o, O=None, LSE=None):
+    """Gradients of sum(dO * O) for packed samples: dq [T, Hq, D], dk_self and
+    dv_self [T, Hkv, D], and per-cartridge dK/dV summed over every sample (and
+    every reference within a sample) that uses the cartridge."""
+    q = _f64(q)
+    d_o = _f64(d_o)
+    T, Hq, Dh = q.shape
+    Hkv = np.asarray(k_self).shape[1]
+    if O is None or LSE is None:
+        O, LSE = packed_forward(q, k_self, v_self, cart_k, cart_v, rows, q_offsets, scale, group_size)
+    dq = np.zeros_like(q)
+    dk_self = np.zeros((T, Hkv, Dh))
+    dv_self = np.zeros((T, Hkv, Dh))
+    dck: List[Optional[np.ndarray]] = [None] * len(cart_k)
+    dcv: List[Optional[np.ndarray]] = [None] * len(cart_k)
+    for b in range(len(rows)):
+        a, e = int(q_offsets[b]), int(q_offsets[b + 1])
+        for c in rows[b]:
+            if dck[c] is None:
+                shp = np.asarray(cart_k[c]).shape
+                dck[c] = np.zeros(shp)
+                dcv[c] = np.zeros(shp)
+        if e == a:
+            continue
+        g = backward(q[None, a:e], _sample(k_self, a, e), _sample(v_self, a, e), cart_k, cart_v,
+                     [rows[b]], scale, group_size, d_o[None, a:e], O=_f64(O)[None, a:e],
+                     LSE=_f64(LSE)[None, :, a:e])
+        dq[a:e] = g[0][0]
+        dk_self[a:e] = g[1][0]
+        dv_self[a:e] = g[2][0]
+        for c in set(rows[b]):
+            dck[c] += g[3][c]
+            dcv[c] += g[4][c]
+    return dq, dk_self, dv_self, dck, dcv
+
+
+def packed_rows_forward_backward(q, k_self, v_self, cart_k, cart_v, rows, q_offsets, scale,
+                                 group_size, b: int, h: int, t_idx: Sequence[int], d_o=None):
+    """rows_forward_backward for sample b of packed samples (t_idx local to it)."""
+    a, e = int(q_offsets[b]), int(q_offsets[b + 1])
+    return rows_forward_backward(_sample(q, a, e), _sample(k_self, a, e), _sample(v_self, a, e),
+                                 cart_k, cart_v, [rows[b]], scale, group_size, 0, h, t_idx,
+                                 None if d_o is None else _sample(d_o, a, e))
+
+
+def packed_key_grads_many(q, k_self, v_self, cart_k, cart_v, rows, q_offsets, scale, group_size,
+                          d_o, kv: int, targets):
+    """key_grads_many for packed samples: a target (cart, toks) with cart >= 0
+    sums over every sample that references the cartridge; cart = -b-1 names
+    the self keys of sample b (toks local to it)."""
+    Dh = np.asarray(q).shape[2]
+    out = [(np.zeros((len(t), Dh)), np.zeros((len(t), Dh))) for _, t in targets]
+    for b in range(len(rows)):
+        a, e = int(q_offsets[b]), int(q_offsets[b + 1])
+        if e == a:
+            continue
+        local = []
+        for i, (cart, toks) in enumerate(targets):
+            if cart >= 0 and cart in rows[b]:
+                local.append((i, (cart, toks)))
+            elif cart < 0 and -cart - 1 == b:
+                local.append((i, (-1, toks)))
+        if not local:
+            continue
+        res = key_grads_many(_sample(q, a, e), _sample(k_self, a, e), _sample(v_self, a, e), cart_k,
+                             cart_v, [rows[b]], scale, group_size, _sample(d_o, a, e), kv,
+                             [t for _, t in local])
+        for (i, _), (dk, dv) in zip(local, res):
+            out[i][0][:] += dk
+            out[i][1][:] += dv
+    return out

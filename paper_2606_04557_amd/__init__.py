@@ -60,13 +60,21 @@ def _ptr(t) -> Optional[int]:
 
 
 class Problem:
-    """Host-side segment table (cas_problem_t) built from torch tensors."""
+    """Host-side segment table (cas_problem_t) built from torch tensors.
+
+    With ``q_offsets`` (batch+1 token offsets) the rows are packed samples of
+    different lengths on one token axis and ``q_len`` must be 0."""
 
     def __init__(self, dtype_code: int, batch: int, q_len: int, num_kv_heads: int,
                  group_size: int, head_dim: int, softmax_scale: float,
-                 rows: Sequence[Sequence[Segment]]):
+                 rows: Sequence[Sequence[Segment]], q_offsets: Optional[Sequence[int]] = None):
         if len(rows) != batch:
             raise ValueError("rows must have one segment list per batch row")
+        self._qoffs = None
+        if q_offsets is not None:
+            if len(q_offsets) != batch + 1:
+                raise ValueError("q_offsets must have batch+1 entries")
+            self._qoffs = (ctypes.c_int32 * (batch + 1))(*[int(x) for x in q_offsets])
         n = sum(len(r) for r in rows)
         self._segs = (_lib.Segment * max(n, 1))()
         self._offs = (ctypes.c_int32 * (batch + 1))()
@@ -89,17 +97,26 @@ class Problem:
                 e.stride_head = int(k.stride(1))
                 i += 1
         self._offs[batch] = i
+        qo = (ctypes.cast(self._qoffs, ctypes.POINTER(ctypes.c_int32)) if self._qoffs is not None
+              else ctypes.POINTER(ctypes.c_int32)())
         self.c = _lib.Problem(dtype_code, batch, q_len, num_kv_heads, group_size, head_dim,
                               float(softmax_scale),
                               ctypes.cast(self._segs, ctypes.POINTER(_lib.Segment)),
-                              ctypes.cast(self._offs, ctypes.POINTER(ctypes.c_int32)))
+                              ctypes.cast(self._offs, ctypes.POINTER(ctypes.c_int32)), qo)
 
     @classmethod
-    def from_tensors(cls, q, rows, num_kv_heads: int, group_size: int, softmax_scale: float):
-        B, Sq, Hq, D = q.shape
+    def from_tensors(cls, q, rows, num_kv_heads: int, group_size: int, softmax_scale: float,
+                     q_offsets: Optional[Sequence[int]] = None):
+        if q_offsets is None:
+            B, Sq, Hq, D = q.shape
+        else:
+            T, Hq, D = q.shape
+            B, Sq = len(q_offsets) - 1, 0
+            if int(q_offsets[-1]) != T:
+                raise ValueError("q_offsets[-1] must equal the packed token count")
         if Hq != num_kv_heads * group_size:
             raise ValueError("q heads must equal num_kv_heads * group_size")
-        return cls(_dtype_code(q), B, Sq, num_kv_heads, group_size, D, softmax_scale, rows)
+        return cls(_dtype_code(q), B, Sq, num_kv_heads, group_size, D, softmax_scale, rows, q_offsets)
 
 
 def workspace_size(problem: Problem, backward: bool) -> int:
@@ -138,15 +155,23 @@ def _workspace(nbytes: int, device):
 
 def prefix_attn_fwd(q, k_self, v_self, rows: Sequence[Sequence[Segment]], num_kv_heads: int,
                     group_size: int, softmax_scale: float, o=None, lse=None, need_lse: bool = True,
-                    stream=None, workspace=None) -> Tuple[object, Optional[object]]:
-    """O [B, Sq, Hq, d] and LSE [B, Hq, Sq] (fp32) over [row's segments || causal self]."""
+                    stream=None, workspace=None,
+                    q_offsets: Optional[Sequence[int]] = None) -> Tuple[object, Optional[object]]:
+    """O [B, Sq, Hq, d] and LSE [B, Hq, Sq] (fp32) over [row's segments || causal self].
+
+    With ``q_offsets`` the rows are packed samples: q, k_self and v_self are
+    [T, H, d], O is [T, Hq, d] and LSE is [Hq, T]."""
     import torch
-    prob = Problem.from_tensors(q, rows, num_kv_heads, group_size, softmax_scale)
-    B, Sq, Hq, D = q.shape
+    prob = Problem.from_tensors(q, rows, num_kv_heads, group_size, softmax_scale, q_offsets)
     if o is None:
         o = torch.empty_like(q)
     if lse is None and need_lse:
-        lse = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device)
+        if q_offsets is None:
+            B, Sq, Hq, _ = q.shape
+            lse = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device)
+        else:
+            T, Hq, _ = q.shape
+            lse = torch.empty((Hq, T), dtype=torch.float32, device=q.device)
     ws_n = workspace_size(prob, False)
     ws = workspace if workspace is not None and workspace.numel() >= ws_n else _workspace(ws_n, q.device)
     _check(load().cas_prefix_attn_fwd(ctypes.byref(prob.c), q.data_ptr(), k_self.data_ptr(),
@@ -158,10 +183,11 @@ def prefix_attn_fwd(q, k_self, v_self, rows: Sequence[Sequence[Segment]], num_kv
 def prefix_attn_bwd(q, k_self, v_self, rows: Sequence[Sequence[Segment]], num_kv_heads: int,
                     group_size: int, softmax_scale: float, o, lse, d_o, dq=None, dk_self=None,
                     dv_self=None, want_dq: bool = True, want_self: bool = True, stream=None,
-                    workspace=None):
-    """Returns (dq, dk_self, dv_self); segment gradients go to each Segment's dk/dv."""
+                    workspace=None, q_offsets: Optional[Sequence[int]] = None):
+    """Returns (dq, dk_self, dv_self); segment gradients go to each Segment's dk/dv.
+    ``q_offsets`` as for prefix_attn_fwd."""
     import torch
-    prob = Problem.from_tensors(q, rows, num_kv_heads, group_size, softmax_scale)
+    prob = Problem.from_tensors(q, rows, num_kv_heads, group_size, softmax_scale, q_offsets)
     if dq is None and want_dq:
         dq = torch.empty_like(q)
     if want_self:

@@ -36,7 +36,8 @@ class Problem(ctypes.Structure):
     _fields_ = [("dtype", ctypes.c_int32), ("batch", ctypes.c_int32), ("q_len", ctypes.c_int32),
                 ("num_kv_heads", ctypes.c_int32), ("group_size", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
-                ("segments", ctypes.POINTER(Segment)), ("seg_offsets", ctypes.POINTER(ctypes.c_int32))]
+                ("segments", ctypes.POINTER(Segment)), ("seg_offsets", ctypes.POINTER(ctypes.c_int32)),
+                ("q_offsets", ctypes.POINTER(ctypes.c_int32))]
 
 
 class StageCopy(ctypes.Structure):
@@ -58,6 +59,8 @@ class PlanInfo(ctypes.Structure):
 class KernelTime(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 48), ("launches", ctypes.c_int32), ("total_ms", ctypes.c_double)]
 
+
+ABI_VERSION = 2   # CAS_ABI_VERSION of include/cas.h (cas_problem_t with q_offsets)
 
 _lib = None
 
@@ -81,6 +84,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cas_last_error_message.argtypes = []
     lib.cas_last_error_message.restype = ctypes.c_char_p
     lib.cas_abi_version.restype = i32
+    if lib.cas_abi_version() != ABI_VERSION:
+        raise RuntimeError(f"libcas ABI {lib.cas_abi_version()} at {path}, this binding expects {ABI_VERSION}: rebuild")
     lib.cas_set_tuning.argtypes = [P(Tuning)]
     lib.cas_get_tuning.argtypes = [P(Tuning)]
     lib.cas_plan_info.argtypes = [P(Problem), P(PlanInfo)]

@@ -81,7 +81,14 @@ bool overlap_free(std::vector<Interval> &iv, std::string &msg) {
 struct Plan {
   DType dt;
   int esize;
-  int B, Sq, Hkv, g, Hq, D, nrows;
+  int B, Hkv, g, Hq, D;
+  bool packed = false;
+  int Sq = 0;              // fixed-length rows: q_len
+  int64_t T = 0;           // tokens over all rows
+  int Smax = 0;            // longest row
+  int nrows_max = 0;       // Smax * g
+  int nqb_max = 0;         // 64-row blocks of the longest row
+  std::vector<int32_t> tok0, len;
   float scale;
   std::vector<DevSeg> segs;
   std::vector<DevRow> rows;
@@ -114,19 +121,47 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
   if (!p) return fail(CAS_ERR_INVALID_ARGUMENT, "problem is NULL");
   if (p->dtype != CAS_DTYPE_BF16 && p->dtype != CAS_DTYPE_FP32)
     return fail(CAS_ERR_INVALID_ARGUMENT, "unknown dtype");
-  if (p->batch < 1 || p->q_len < 1 || p->num_kv_heads < 1 || p->group_size < 1 || p->head_dim < 1)
-    return fail(CAS_ERR_INVALID_ARGUMENT, "batch, q_len, num_kv_heads, group_size and head_dim must be >= 1");
+  if (p->batch < 1 || p->num_kv_heads < 1 || p->group_size < 1 || p->head_dim < 1)
+    return fail(CAS_ERR_INVALID_ARGUMENT, "batch, num_kv_heads, group_size and head_dim must be >= 1");
   if (p->head_dim != 64 && p->head_dim != 128)
     return fail(CAS_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
   if (!std::isfinite(p->softmax_scale) || !(p->softmax_scale > 0.0f))
     return fail(CAS_ERR_INVALID_ARGUMENT, "softmax_scale must be finite and > 0");
   const int64_t Hq = (int64_t)p->num_kv_heads * p->group_size;
-  const int64_t nrows = (int64_t)p->group_size * p->q_len;
-  if (Hq > (1 << 16) || nrows > (1 << 28))
-    return fail(CAS_ERR_UNSUPPORTED, "num_kv_heads*group_size or group_size*q_len too large");
+  if (Hq > (1 << 16)) return fail(CAS_ERR_UNSUPPORTED, "num_kv_heads*group_size above 2^16");
   if ((int64_t)p->num_kv_heads * p->head_dim > (1 << 22))
     return fail(CAS_ERR_UNSUPPORTED, "num_kv_heads*head_dim above 2^22 (self-token stride)");
-  if ((int64_t)p->batch * p->q_len * Hq * p->head_dim > (int64_t)1 << 40)
+  // Query layout: per-row token offsets and lengths.
+  pl.packed = p->q_offsets != nullptr;
+  pl.tok0.resize(p->batch);
+  pl.len.resize(p->batch);
+  if (pl.packed) {
+    if (p->q_len != 0) return fail(CAS_ERR_INVALID_ARGUMENT, "q_len must be 0 when q_offsets is given");
+    if (p->q_offsets[0] != 0) return fail(CAS_ERR_INVALID_ARGUMENT, "q_offsets[0] must be 0");
+    for (int b = 0; b < p->batch; ++b) {
+      if (p->q_offsets[b + 1] < p->q_offsets[b])
+        return fail(CAS_ERR_INVALID_ARGUMENT, "q_offsets must be non-decreasing");
+      pl.tok0[b] = p->q_offsets[b];
+      pl.len[b] = p->q_offsets[b + 1] - p->q_offsets[b];
+    }
+    pl.T = p->q_offsets[p->batch];
+    if (pl.T < 1) return fail(CAS_ERR_INVALID_ARGUMENT, "packed rows hold no query token");
+  } else {
+    if (p->q_len < 1) return fail(CAS_ERR_INVALID_ARGUMENT, "q_len must be >= 1");
+    if ((int64_t)p->batch * p->q_len > INT32_MAX)
+      return fail(CAS_ERR_UNSUPPORTED, "batch*q_len above 2^31");
+    for (int b = 0; b < p->batch; ++b) {
+      pl.tok0[b] = b * p->q_len;
+      pl.len[b] = p->q_len;
+    }
+    pl.T = (int64_t)p->batch * p->q_len;
+    pl.Sq = p->q_len;
+  }
+  pl.Smax = *std::max_element(pl.len.begin(), pl.len.end());
+  if (pl.T * Hq > INT32_MAX) return fail(CAS_ERR_UNSUPPORTED, "tokens*num_kv_heads*group_size above 2^31");
+  if ((int64_t)p->group_size * pl.Smax > (1 << 28))
+    return fail(CAS_ERR_UNSUPPORTED, "group_size*(longest row) above 2^28");
+  if (pl.T * Hq * p->head_dim > (int64_t)1 << 40)
     return fail(CAS_ERR_UNSUPPORTED, "query tensor too large");
   if (!p->seg_offsets) return fail(CAS_ERR_INVALID_ARGUMENT, "seg_offsets is NULL");
   if (p->seg_offsets[0] != 0) return fail(CAS_ERR_INVALID_ARGUMENT, "seg_offsets[0] must be 0");
@@ -140,21 +175,27 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
   pl.dt = p->dtype == CAS_DTYPE_BF16 ? kBF16 : kFP32;
   pl.esize = p->dtype == CAS_DTYPE_BF16 ? 2 : 4;
   pl.B = p->batch;
-  pl.Sq = p->q_len;
   pl.Hkv = p->num_kv_heads;
   pl.g = p->group_size;
   pl.Hq = (int)Hq;
   pl.D = p->head_dim;
-  pl.nrows = (int)nrows;
+  pl.nrows_max = pl.Smax * pl.g;
+  pl.nqb_max = (int)ceil_div(pl.nrows_max, 64);
   pl.scale = p->softmax_scale;
 
   const int D = pl.D, es = pl.esize, Hkv = pl.Hkv;
   int64_t min_row_tiles = INT64_MAX;
+  int64_t tblk = 0;
   pl.rows.resize(pl.B);
   for (int b = 0; b < pl.B; ++b) {
     DevRow r{};
     r.seg_begin = (int32_t)pl.segs.size();
     r.tile_begin = (int32_t)pl.tiles.size();
+    r.tok0 = pl.tok0[b];
+    r.len = pl.len[b];
+    r.lse0 = pl.packed ? pl.tok0[b] : (int32_t)((int64_t)b * Hq * pl.Sq);
+    r.tblk0 = (int32_t)tblk;
+    tblk += (int64_t)Hkv * ceil_div((int64_t)pl.len[b] * pl.g, 64);
     int64_t tiles = 0, plen = 0;
     for (int i = p->seg_offsets[b]; i < p->seg_offsets[b + 1]; ++i) {
       const cas_segment_t &s = p->segments[i];
@@ -191,20 +232,20 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
       plen += s.len;
       pl.segs.push_back(d);
     }
-    if (plen + pl.Sq > (int64_t)1 << 30)
+    if (plen + pl.len[b] > (int64_t)1 << 30)
       return fail(CAS_ERR_UNSUPPORTED, "row " + std::to_string(b) + ": prefix longer than 2^30 tokens");
     r.seg_end = (int32_t)pl.segs.size();
     r.prefix_tiles = (int32_t)tiles;
     // The row's causal self tiles follow its prefix tiles; k/v hold byte
     // offsets from k_self/v_self until bind_self_tiles adds the base.
-    for (int64_t s0 = 0; s0 < p->q_len; s0 += kKeyTile) {
+    for (int64_t s0 = 0; s0 < pl.len[b]; s0 += kKeyTile) {
       DevTile t{};
-      const int64_t off = (((int64_t)b * p->q_len + s0) * Hkv) * D * es;
+      const int64_t off = (((int64_t)pl.tok0[b] + s0) * Hkv) * D * es;
       t.k = (const void *)(uintptr_t)off;
       t.v = (const void *)(uintptr_t)off;
       t.stride_head = D;
       t.stride_tok = Hkv * D;
-      t.nvalid = (int32_t)std::min<int64_t>(kKeyTile, p->q_len - s0);
+      t.nvalid = (int32_t)std::min<int64_t>(kKeyTile, pl.len[b] - s0);
       pl.tiles.push_back(t);
     }
     pl.rows[b] = r;
@@ -214,13 +255,20 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
 
   const cas_tuning_t tu = tuning();
   const bool bf16 = pl.dt == kBF16;
-  pl.nqblk_fwd = (int)ceil_div(pl.nrows, bf16 ? kBf16RowsPerWg : kRowsPerWg);
-  pl.nqblk_dq = (int)ceil_div(pl.nrows, bf16 ? kBf16RowsPerWg : kDqRowsPerWg);
-  const int64_t base_fwd = (int64_t)pl.B * Hkv * pl.nqblk_fwd;
-  const int64_t base_dq = (int64_t)pl.B * Hkv * pl.nqblk_dq;
+  const int rpw_fwd = bf16 ? kBf16RowsPerWg : kRowsPerWg, rpw_dq = bf16 ? kBf16RowsPerWg : kDqRowsPerWg;
+  pl.nqblk_fwd = (int)ceil_div(pl.nrows_max, rpw_fwd);
+  pl.nqblk_dq = (int)ceil_div(pl.nrows_max, rpw_dq);
+  // The grids are sized for the longest row; the split heuristic counts the
+  // workgroups that have rows.
+  int64_t base_fwd = 0, base_dq = 0;
+  for (int b = 0; b < pl.B; ++b) {
+    base_fwd += Hkv * ceil_div((int64_t)pl.len[b] * pl.g, rpw_fwd);
+    base_dq += Hkv * ceil_div((int64_t)pl.len[b] * pl.g, rpw_dq);
+  }
   pl.fwd_splits = tu.fwd_splits > 0 ? std::min(tu.fwd_splits, kMaxSplits) : auto_splits(base_fwd, min_row_tiles);
   pl.dq_splits = tu.dq_splits > 0 ? std::min(tu.dq_splits, kMaxSplits) : auto_splits(base_dq, min_row_tiles);
-  if (base_fwd * pl.fwd_splits > INT32_MAX || base_dq * pl.dq_splits > INT32_MAX)
+  if ((int64_t)pl.B * Hkv * pl.nqblk_fwd * pl.fwd_splits > INT32_MAX ||
+      (int64_t)pl.B * Hkv * pl.nqblk_dq * pl.dq_splits > INT32_MAX)
     return fail(CAS_ERR_UNSUPPORTED, "grid too large");
 
   if (bwd) {
@@ -263,8 +311,16 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
       c.len = (int32_t)s.len;
       c.tile_begin = (int32_t)tiles;
       c.use_begin = (int32_t)pl.uses.size();
-      for (int32_t b : users[u]) pl.uses.push_back(b);
+      // Rows without queries add nothing and are left out.
+      int64_t nblk = 0;
+      for (int32_t b : users[u]) {
+        if (pl.len[b] == 0) continue;
+        pl.uses.push_back(b);
+        nblk += ceil_div((int64_t)pl.len[b] * pl.g, kDkdvQBlock);
+      }
       c.use_end = (int32_t)pl.uses.size();
+      if (nblk > INT32_MAX) return fail(CAS_ERR_UNSUPPORTED, "too many query blocks per cartridge");
+      c.nblk = (int32_t)nblk;
       tiles += ceil_div(s.len, kDkdvKeyTile);
       pl.carts.push_back(c);
       // A gradient buffer must not overlap itself under its strides.
@@ -298,7 +354,7 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
     off = align_up(off + pl.uses.size() * sizeof(int32_t), 256);
   }
   pl.table_bytes = off;
-  const size_t plane = (size_t)pl.B * Hkv * pl.nrows;
+  const size_t plane = (size_t)pl.T * pl.Hq;   // packed rows of all batch rows and KV heads
   if (!bwd) {
     if (pl.fwd_splits > 1) {
       pl.off_part_o = off;
@@ -319,11 +375,11 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
     off = align_up(off + plane * 4, 256);
     if (pl.dt == kBF16) {
       // Transposed Q and dO of every 64-row block (dK/dV operands).
-      const size_t tblk = (size_t)pl.B * Hkv * ceil_div(pl.nrows, 64) * 64 * D * 2;
+      const size_t tbytes = (size_t)tblk * 64 * D * 2;
       pl.off_qT = off;
-      off = align_up(off + tblk, 256);
+      off = align_up(off + tbytes, 256);
       pl.off_doT = off;
-      off = align_up(off + tblk, 256);
+      off = align_up(off + tbytes, 256);
     }
     if (pl.dq_splits > 1) {
       pl.off_part_dq = off;
@@ -338,7 +394,7 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
 void bind_self_tiles(Plan &pl, const void *k_self, const void *v_self) {
   for (int b = 0; b < pl.B; ++b) {
     const DevRow &r = pl.rows[b];
-    const int n = (int)ceil_div(pl.Sq, kKeyTile);
+    const int n = (int)ceil_div(pl.len[b], kKeyTile);
     for (int i = 0; i < n; ++i) {
       DevTile &t = pl.tiles[r.tile_begin + r.prefix_tiles + i];
       t.k = (const char *)k_self + (uintptr_t)t.k;
@@ -555,7 +611,7 @@ cas_status_t cas_plan_info(const cas_problem_t *p, cas_plan_info_t *out) {
   out->fwd_splits = pf.fwd_splits;
   out->dq_splits = pb.dq_splits;
   out->fwd_workgroups = pf.nqblk_fwd * pf.Hkv * pf.B * pf.fwd_splits;
-  const int self_tiles = (int)ceil_div(pb.Sq, kDkdvKeyTile);
+  const int self_tiles = (int)ceil_div(pb.Smax, kDkdvKeyTile);
   out->dkdv_workgroups = (pb.cart_tiles + pb.B * self_tiles) * pb.Hkv;
   out->unique_segments = (int32_t)pb.carts.size();
   out->total_key_tiles = pb.cart_tiles + pb.B * self_tiles;
@@ -574,14 +630,14 @@ cas_status_t cas_prefix_attn_fwd(const cas_problem_t *p, const void *q, const vo
   if (!q || !k_self || !v_self || !o) return fail(CAS_ERR_INVALID_ARGUMENT, "q, k_self, v_self and o must be non-NULL");
   if (!aligned16(q) || !aligned16(k_self) || !aligned16(v_self) || !aligned16(o) || ((uintptr_t)lse & 3u))
     return fail(CAS_ERR_ALIGNMENT, "tensors must be 16-byte aligned (lse 4-byte)");
-  const uintptr_t qbytes = (uintptr_t)pl.B * pl.Sq * pl.Hq * pl.D * pl.esize;
-  const uintptr_t kvbytes = (uintptr_t)pl.B * pl.Sq * pl.Hkv * pl.D * pl.esize;
+  const uintptr_t qbytes = (uintptr_t)pl.T * pl.Hq * pl.D * pl.esize;
+  const uintptr_t kvbytes = (uintptr_t)pl.T * pl.Hkv * pl.D * pl.esize;
   std::vector<Interval> iv;
   iv.push_back({(uintptr_t)q, (uintptr_t)q + qbytes, false, 0, "q"});
   iv.push_back({(uintptr_t)k_self, (uintptr_t)k_self + kvbytes, false, 0, "k_self"});
   iv.push_back({(uintptr_t)v_self, (uintptr_t)v_self + kvbytes, false, 0, "v_self"});
   iv.push_back({(uintptr_t)o, (uintptr_t)o + qbytes, true, (uintptr_t)o, "o"});
-  if (lse) iv.push_back({(uintptr_t)lse, (uintptr_t)lse + (uintptr_t)pl.B * pl.Hq * pl.Sq * 4, true, (uintptr_t)lse, "lse"});
+  if (lse) iv.push_back({(uintptr_t)lse, (uintptr_t)lse + (uintptr_t)pl.T * pl.Hq * 4, true, (uintptr_t)lse, "lse"});
   add_segment_intervals(pl, p, false, iv);
   std::string msg;
   if (!overlap_free(iv, msg)) return fail(CAS_ERR_INVALID_ARGUMENT, msg);
@@ -605,13 +661,15 @@ cas_status_t cas_prefix_attn_fwd(const cas_problem_t *p, const void *q, const vo
   fp.rows = (const DevRow *)(ws + pl.off_rows);
   fp.tiles = (const DevTile *)(ws + pl.off_tiles);
   fp.ovf_flag = pl.dt == kBF16 ? (int32_t *)(ws + pl.off_ovf) : nullptr;
+  fp.plane = pl.T * pl.Hq;
   fp.B = pl.B;
-  fp.Sq = pl.Sq;
+  fp.Smax = pl.Smax;
   fp.Hkv = pl.Hkv;
   fp.g = pl.g;
-  fp.nrows = pl.nrows;
+  fp.nrows_max = pl.nrows_max;
   fp.nqblk = pl.nqblk_fwd;
   fp.splits = pl.fwd_splits;
+  fp.lse_hs = pl.packed ? (int32_t)pl.T : pl.Sq;
   fp.scale_log2 = pl.scale * 1.4426950408889634f;
   hipError_t e = timed("fwd", stream, [&] { return launch_fwd(fp, pl.dt, pl.D, stream); });
   if (e != hipSuccess) return hip_fail("fwd launch", e);
@@ -621,12 +679,14 @@ cas_status_t cas_prefix_attn_fwd(const cas_problem_t *p, const void *q, const vo
     mp.part_lse = fp.part_lse;
     mp.o = o;
     mp.lse = lse;
+    mp.rows = fp.rows;
+    mp.plane = fp.plane;
     mp.B = pl.B;
-    mp.Sq = pl.Sq;
     mp.Hkv = pl.Hkv;
     mp.g = pl.g;
-    mp.nrows = pl.nrows;
+    mp.nrows_max = pl.nrows_max;
     mp.splits = pl.fwd_splits;
+    mp.lse_hs = fp.lse_hs;
     e = timed("fwd_merge", stream, [&] { return launch_fwd_merge(mp, pl.dt, pl.D, stream); });
     if (e != hipSuccess) return hip_fail("fwd_merge launch", e);
   }
@@ -645,14 +705,14 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
   if (!aligned16(q) || !aligned16(k_self) || !aligned16(v_self) || !aligned16(o) || !aligned16(d_o) ||
       !aligned16(dq) || !aligned16(dk_self) || !aligned16(dv_self) || ((uintptr_t)lse & 3u))
     return fail(CAS_ERR_ALIGNMENT, "tensors must be 16-byte aligned (lse 4-byte)");
-  const uintptr_t qbytes = (uintptr_t)pl.B * pl.Sq * pl.Hq * pl.D * pl.esize;
-  const uintptr_t kvbytes = (uintptr_t)pl.B * pl.Sq * pl.Hkv * pl.D * pl.esize;
+  const uintptr_t qbytes = (uintptr_t)pl.T * pl.Hq * pl.D * pl.esize;
+  const uintptr_t kvbytes = (uintptr_t)pl.T * pl.Hkv * pl.D * pl.esize;
   std::vector<Interval> iv;
   iv.push_back({(uintptr_t)q, (uintptr_t)q + qbytes, false, 0, "q"});
   iv.push_back({(uintptr_t)k_self, (uintptr_t)k_self + kvbytes, false, 0, "k_self"});
   iv.push_back({(uintptr_t)v_self, (uintptr_t)v_self + kvbytes, false, 0, "v_self"});
   iv.push_back({(uintptr_t)o, (uintptr_t)o + qbytes, false, 0, "o"});
-  iv.push_back({(uintptr_t)lse, (uintptr_t)lse + (uintptr_t)pl.B * pl.Hq * pl.Sq * 4, false, 0, "lse"});
+  iv.push_back({(uintptr_t)lse, (uintptr_t)lse + (uintptr_t)pl.T * pl.Hq * 4, false, 0, "lse"});
   iv.push_back({(uintptr_t)d_o, (uintptr_t)d_o + qbytes, false, 0, "d_o"});
   if (dq) iv.push_back({(uintptr_t)dq, (uintptr_t)dq + qbytes, true, (uintptr_t)dq, "dq"});
   if (dk_self) iv.push_back({(uintptr_t)dk_self, (uintptr_t)dk_self + kvbytes, true, (uintptr_t)dk_self, "dk_self"});
@@ -678,19 +738,20 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
   pp.lse = lse;
   pp.nd = nd;
   pp.lse2 = lse2;
+  pp.rows = (const DevRow *)(ws + pl.off_rows);
   pp.B = pl.B;
-  pp.Sq = pl.Sq;
   pp.Hkv = pl.Hkv;
   pp.g = pl.g;
-  pp.nrows = pl.nrows;
+  pp.nrows_max = pl.nrows_max;
+  pp.nqb_max = pl.nqb_max;
+  pp.lse_hs = pl.packed ? (int32_t)pl.T : pl.Sq;
   pp.q = q;
   pp.qT = pl.dt == kBF16 ? ws + pl.off_qT : nullptr;
   pp.doT = pl.dt == kBF16 ? ws + pl.off_doT : nullptr;
-  pp.nqb = (int)ceil_div(pl.nrows, 64);
   hipError_t e = timed("bwd_pre", stream, [&] { return launch_bwd_pre(pp, pl.dt, pl.D, stream); });
   if (e != hipSuccess) return hip_fail("bwd_pre launch", e);
 
-  const int self_tiles = (dk_self || dv_self) ? (int)ceil_div(pl.Sq, kDkdvKeyTile) : 0;
+  const int self_tiles = (dk_self || dv_self) ? (int)ceil_div(pl.Smax, kDkdvKeyTile) : 0;
   const int gx = pl.cart_tiles + pl.B * self_tiles;
   if (gx > 0) {
     DkdvParams kp{};
@@ -706,14 +767,13 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
     kp.dv_self = dv_self;
     kp.carts = (const DevCart *)(ws + pl.off_carts);
     kp.uses = (const int32_t *)(ws + pl.off_uses);
+    kp.rows = pp.rows;
     kp.n_carts = (int32_t)pl.carts.size();
     kp.cart_tiles = pl.cart_tiles;
     kp.self_tiles = std::max(self_tiles, 1);
     kp.B = pl.B;
-    kp.Sq = pl.Sq;
     kp.Hkv = pl.Hkv;
     kp.g = pl.g;
-    kp.nrows = pl.nrows;
     kp.scale_log2 = scale_log2;
     kp.scale = pl.scale;
     if (pl.dt == kBF16) {
@@ -737,11 +797,12 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
     dp.segs = (const DevSeg *)(ws + pl.off_segs);
     dp.tiles = (const DevTile *)(ws + pl.off_tiles);
     dp.rows = (const DevRow *)(ws + pl.off_rows);
+    dp.plane = pl.T * pl.Hq;
     dp.B = pl.B;
-    dp.Sq = pl.Sq;
+    dp.Smax = pl.Smax;
     dp.Hkv = pl.Hkv;
     dp.g = pl.g;
-    dp.nrows = pl.nrows;
+    dp.nrows_max = pl.nrows_max;
     dp.nqblk = pl.nqblk_dq;
     dp.splits = pl.dq_splits;
     dp.scale_log2 = scale_log2;
@@ -752,11 +813,12 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
       DqReduceParams rp{};
       rp.part_dq = dp.part_dq;
       rp.dq = dq;
+      rp.rows = dp.rows;
+      rp.plane = dp.plane;
       rp.B = pl.B;
-      rp.Sq = pl.Sq;
       rp.Hkv = pl.Hkv;
       rp.g = pl.g;
-      rp.nrows = pl.nrows;
+      rp.nrows_max = pl.nrows_max;
       rp.splits = pl.dq_splits;
       rp.scale = pl.scale;
       e = timed("dq_reduce", stream, [&] { return launch_dq_reduce(rp, pl.dt, pl.D, stream); });

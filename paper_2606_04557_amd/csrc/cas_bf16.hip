@@ -205,12 +205,16 @@ void fwd_bf16_kernel(FwdParams p) {
   bid /= p.Hkv;
   const int split = __builtin_amdgcn_readfirstlane(bid % p.splits);
   const int b = __builtin_amdgcn_readfirstlane(bid / p.splits);
+  const int g = p.g, Hkv = p.Hkv, Hq = Hkv * g;
+  const DevRow row = load_const(p.rows, b);
+  const int tok0 = __builtin_amdgcn_readfirstlane(row.tok0);
+  const int nrows = __builtin_amdgcn_readfirstlane(row.len) * g;
+  const int wg_row0 = qblk * kFastRowsPerWg;
+  if (wg_row0 >= nrows) return;   // grid sized for the longest row
   if constexpr (FIXUP) {
     if (load_const(p.ovf_flag, (int)blockIdx.x) == 0) return;
   }
 
-  const int g = p.g, Sq = p.Sq, Hkv = p.Hkv, Hq = Hkv * g, nrows = p.nrows;
-  const int wg_row0 = qblk * kFastRowsPerWg;
   const int wg_row1 = min(nrows, wg_row0 + kFastRowsPerWg);
   const int row0 = wg_row0 + wave * kFastRowsPerWave;
   const bool wave_active = row0 < nrows;
@@ -223,7 +227,6 @@ void fwd_bf16_kernel(FwdParams p) {
 
   // Wave-uniform tile range of this split (readfirstlane keeps it, and every
   // tile-table read that depends on it, in scalar registers).
-  const DevRow row = load_const(p.rows, b);
   const int ptiles = __builtin_amdgcn_readfirstlane(row.prefix_tiles);
   const int ntiles = ptiles + wg_t_hi / kKT + 1;
   const int tb = __builtin_amdgcn_readfirstlane((int)((int64_t)ntiles * split / p.splits));
@@ -239,7 +242,7 @@ void fwd_bf16_kernel(FwdParams p) {
 
   bf16x8 qf[NSTEP];
   if (my_row < nrows) {
-    const __bf16 *rp = (const __bf16 *)p.q + (((int64_t)b * Sq + my_t) * Hq + kvh * g + (my_row - my_t * g)) * D;
+    const __bf16 *rp = (const __bf16 *)p.q + (((int64_t)tok0 + my_t) * Hq + kvh * g + (my_row - my_t * g)) * D;
 #pragma unroll
     for (int st = 0; st < NSTEP; ++st) qf[st] = *reinterpret_cast<const bf16x8 *>(rp + st * 16 + G * 8);
   } else {
@@ -530,16 +533,17 @@ void fwd_bf16_kernel(FwdParams p) {
   const float m_out = m_run;
   if (p.splits == 1) {
     const float inv = 1.0f / lt;
-    __bf16 *op = (__bf16 *)p.o + (((int64_t)b * Sq + my_t) * Hq + h) * D;
+    __bf16 *op = (__bf16 *)p.o + (((int64_t)tok0 + my_t) * Hq + h) * D;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj)
         store4(op + dt * 32 + jj * 8 + G * 4, oacc[dt][jj * 4 + 0] * inv, oacc[dt][jj * 4 + 1] * inv,
                oacc[dt][jj * 4 + 2] * inv, oacc[dt][jj * 4 + 3] * inv);
-    if (G == 0 && p.lse != nullptr) p.lse[((int64_t)b * Hq + h) * Sq + my_t] = (m_out + log2f(lt)) * kLn2;
+    if (G == 0 && p.lse != nullptr)
+      p.lse[(int64_t)row.lse0 + (int64_t)h * p.lse_hs + my_t] = (m_out + log2f(lt)) * kLn2;
   } else {
-    const int64_t prow = (((int64_t)split * p.B + b) * Hkv + kvh) * nrows + my_row;
+    const int64_t prow = split * p.plane + (int64_t)tok0 * Hq + kvh * nrows + my_row;
     const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
     float *op = p.part_o + prow * D;
 #pragma unroll
@@ -575,8 +579,12 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
   const int split = __builtin_amdgcn_readfirstlane(bid % p.splits);
   const int b = __builtin_amdgcn_readfirstlane(bid / p.splits);
 
-  const int g = p.g, Sq = p.Sq, Hkv = p.Hkv, Hq = Hkv * g, nrows = p.nrows;
+  const int g = p.g, Hkv = p.Hkv, Hq = Hkv * g;
+  const DevRow row = load_const(p.rows, b);
+  const int tok0 = __builtin_amdgcn_readfirstlane(row.tok0);
+  const int nrows = __builtin_amdgcn_readfirstlane(row.len) * g;
   const int wg_row0 = qblk * kFastRowsPerWg;
+  if (wg_row0 >= nrows) return;   // grid sized for the longest row
   const int wg_row1 = min(nrows, wg_row0 + kFastRowsPerWg);
   const int row0 = wg_row0 + wave * kFastRowsPerWave;
   const bool wave_active = row0 < nrows;
@@ -594,7 +602,7 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
   bf16x8 qf[NSTEP], df[NSTEP];
   float lse2r = INFINITY, ndr = 0.0f;
   if (my_row < nrows) {
-    const int64_t off = (((int64_t)b * Sq + my_t) * Hq + kvh * g + (my_row - my_t * g)) * D;
+    const int64_t off = (((int64_t)tok0 + my_t) * Hq + kvh * g + (my_row - my_t * g)) * D;
     const __bf16 *qp = (const __bf16 *)p.q + off;
     const __bf16 *dp = (const __bf16 *)p.d_o + off;
 #pragma unroll
@@ -602,7 +610,7 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
       qf[st] = *reinterpret_cast<const bf16x8 *>(qp + st * 16 + G * 8);
       df[st] = *reinterpret_cast<const bf16x8 *>(dp + st * 16 + G * 8);
     }
-    const int64_t pk = ((int64_t)b * Hkv + kvh) * nrows + my_row;
+    const int64_t pk = (int64_t)tok0 * Hq + kvh * nrows + my_row;
     lse2r = p.lse2[pk];
     ndr = p.nd[pk];
   } else {
@@ -616,7 +624,6 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) acc[dt] = zero16();
 
-  const DevRow row = load_const(p.rows, b);
   const int ptiles = __builtin_amdgcn_readfirstlane(row.prefix_tiles);
   const int ntiles = ptiles + wg_t_hi / kKT + 1;
   const int tb = __builtin_amdgcn_readfirstlane((int)((int64_t)ntiles * split / p.splits));
@@ -716,7 +723,7 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
   const int h = kvh * g + (my_row - my_t * g);
   if (p.splits == 1) {
     const float sc = p.scale;
-    __bf16 *op = (__bf16 *)p.dq + (((int64_t)b * Sq + my_t) * Hq + h) * D;
+    __bf16 *op = (__bf16 *)p.dq + (((int64_t)tok0 + my_t) * Hq + h) * D;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -724,7 +731,7 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
         store4(op + dt * 32 + jj * 8 + G * 4, acc[dt][jj * 4 + 0] * sc, acc[dt][jj * 4 + 1] * sc,
                acc[dt][jj * 4 + 2] * sc, acc[dt][jj * 4 + 3] * sc);
   } else {
-    const int64_t prow = (((int64_t)split * p.B + b) * Hkv + kvh) * nrows + my_row;
+    const int64_t prow = split * p.plane + (int64_t)tok0 * Hq + kvh * nrows + my_row;
     float *op = p.part_dq + prow * D;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
@@ -738,28 +745,32 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
 // ---------------------------------------------------------------------------
 // Backward prologue for the bf16 dK/dV kernel: Q and dO of every 64-row
 // query block of each (batch row, KV head), transposed to [channel][64 rows],
-// zero beyond nrows. Within each 16-row group the rows are stored in the
-// order 0-3, 8-11, 4-7, 12-15, so the 8 rows that one lane group of a 32x32
-// MFMA fragment needs (4G..4G+3 and 8+4G..8+4G+3) are one 16-byte chunk.
+// zero beyond the row's last packed row. Within each 16-row group the rows
+// are stored in the order 0-3, 8-11, 4-7, 12-15, so the 8 rows that one lane
+// group of a 32x32 MFMA fragment needs (4G..4G+3 and 8+4G..8+4G+3) are one
+// 16-byte chunk.
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void bwd_transpose_bf16_kernel(PreParams p) {
   __shared__ __attribute__((aligned(16))) __bf16 tile[64][D + 8];
   const int tid = threadIdx.x;
-  const int qb = blockIdx.x % p.nqb;
-  const int bk = blockIdx.x / p.nqb;
-  const int kvh = bk % p.Hkv, b = bk / p.Hkv;
+  const int qb = blockIdx.x % p.nqb_max;
+  const int kvh = blockIdx.x / p.nqb_max, b = blockIdx.y;
   const int g = p.g, Hq = p.Hkv * g;
+  const DevRow row = p.rows[b];
+  const int nrows = row.len * g, nqb = (nrows + 63) / 64;
+  if (qb >= nqb) return;   // grid sized for the longest row
+  const int64_t blk = (int64_t)row.tblk0 + kvh * nqb + qb;
   for (int which = 0; which < 2; ++which) {
     const __bf16 *src = (const __bf16 *)(which ? p.d_o : p.q);
-    __bf16 *dst = (__bf16 *)(which ? p.doT : p.qT) + (int64_t)blockIdx.x * D * 64;
+    __bf16 *dst = (__bf16 *)(which ? p.doT : p.qT) + blk * D * 64;
     for (int i = tid; i < 64 * D / 8; i += 256) {
       const int r = i / (D / 8), c8 = i % (D / 8);
       const int rr = qb * 64 + r;
       uint4 v = uint4{0, 0, 0, 0};
-      if (rr < p.nrows) {
+      if (rr < nrows) {
         const int t = rr / g, h = kvh * g + (rr - t * g);
-        v = *reinterpret_cast<const uint4 *>(src + (((int64_t)b * p.Sq + t) * Hq + h) * D + c8 * 8);
+        v = *reinterpret_cast<const uint4 *>(src + (((int64_t)row.tok0 + t) * Hq + h) * D + c8 * 8);
       }
       *reinterpret_cast<uint4 *>(&tile[r][c8 * 8]) = v;
     }
@@ -809,9 +820,9 @@ __global__ __launch_bounds__(256) void bwd_transpose_bf16_kernel(PreParams p) {
 // write zeros that nothing reads).
 //
 // P needs no mask for keys beyond the tile (their dK / dV columns are never
-// stored) or rows beyond nrows (Q, dO, Q^T, dO^T, LSE2 and D all read as
-// zero there: P = 1 and dS = 0 add nothing). On self keys P = 0 for rows
-// before the key's position.
+// stored) or for packed rows beyond the batch row's last (Q, dO, Q^T, dO^T,
+// LSE2 and D all read as zero there: P = 1 and dS = 0 add nothing). On self
+// keys P = 0 for rows before the key's position.
 // ---------------------------------------------------------------------------
 template <int D, bool GFAST>
 __global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -845,7 +856,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
   const int q = wave & 3;                      // SIMD, key quarter, index within the wave's group
   const bool pwave = wave < 4;
   const int tile = blockIdx.x, kvh = blockIdx.y;
-  const int g = p.g, Sq = p.Sq, Hkv = p.Hkv, Hq = Hkv * g, nrows = p.nrows;
+  const int g = p.g, Hkv = p.Hkv, Hq = Hkv * g;
   const float c = p.scale_log2;
 
   const __bf16 *kbase;
@@ -853,7 +864,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
   __bf16 *dkp;
   __bf16 *dvp;
   int64_t st;
-  int klen, key0, use_b = 0, use_e = 1;
+  int klen, key0, use_b = 0, nblk_all;
   const bool self = tile >= p.cart_tiles;
   int self_b = 0;
   if (!self) {
@@ -871,18 +882,21 @@ void dkdv_bf16_kernel(DkdvParams p) {
     dvp = cd.dv ? (__bf16 *)cd.dv + kvh * cd.stride_head : nullptr;
     st = cd.stride_tok;
     use_b = cd.use_begin;
-    use_e = cd.use_end;
+    nblk_all = cd.nblk;
   } else {
     const int rel = tile - p.cart_tiles;
     self_b = rel / p.self_tiles;
     key0 = (rel % p.self_tiles) * KTB;
-    klen = Sq;
-    const int64_t base = ((int64_t)self_b * Sq * Hkv + kvh) * D;
+    const DevRow sr = load_const(p.rows, self_b);
+    klen = sr.len;
+    if (key0 >= klen) return;   // grid sized for the longest row
+    const int64_t base = ((int64_t)sr.tok0 * Hkv + kvh) * D;
     kbase = (const __bf16 *)p.k_self + base;
     vbase = (const __bf16 *)p.v_self + base;
     dkp = p.dk_self ? (__bf16 *)p.dk_self + base : nullptr;
     dvp = p.dv_self ? (__bf16 *)p.dv_self + base : nullptr;
     st = (int64_t)Hkv * D;
+    nblk_all = (klen * g + QB - 1) / QB - (key0 * g) / QB;
   }
   const int nk = __builtin_amdgcn_readfirstlane(min(KTB, klen - key0));   // valid keys (>= 1)
   const int my_key = 32 * q + n;               // lane's key within the tile
@@ -919,19 +933,18 @@ void dkdv_bf16_kernel(DkdvParams p) {
     lds_barrier();
   }
 
-  const int nqb = (nrows + QB - 1) / QB;
   const int qb_first = self ? (key0 * g) / QB : 0;
-  const int per_use = nqb - qb_first;
-  const int nblk = __builtin_amdgcn_readfirstlane(per_use * (use_e - use_b));
+  const int nblk = __builtin_amdgcn_readfirstlane(nblk_all);
 
   // Block cursor: block blk of the workgroup's sequence is 64-row block
-  // qb = qb_first + r of batch row b = uses[u] (r = blk mod per_use), with the
-  // element offsets of its rows (GFAST), transposed block and statistics.
-  // Advancing within a batch row adds constant strides; a new batch row (a
-  // table load) recomputes them. Blocks past the end keep the last block's
-  // offsets and are not copied.
+  // qb = qb_first + r of batch row b = uses[u] (the rows' block counts summed
+  // over earlier uses give blk - r), with the element offsets of its rows
+  // (GFAST), transposed block and statistics. Advancing within a batch row
+  // adds constant strides; a new batch row (table loads) recomputes them.
+  // Blocks past the end keep the last block's offsets and are not copied.
+  // Every use has at least one block (rows without queries are not listed).
   struct Cursor {
-    int blk, r, u, b;
+    int blk, r, u, b, pu, nr, tok0;   // pu: blocks of this use; nr: packed rows of the row
     int64_t roff, rlim, toff, soff;   // rlim: bytes from roff to the group's last row
   };
   const int64_t row_step = (int64_t)(QB / g) * Hq * D;   // GFAST: elements between consecutive blocks
@@ -942,29 +955,54 @@ void dkdv_bf16_kernel(DkdvParams p) {
     asm volatile("" : "+s"(b));
     return b;
   };
+  // Packed rows of batch row b (pinned like the use table load).
+  auto row_geo = [&](int b, int &tok0, int &len, int &tblk0) __attribute__((always_inline)) {
+    const DevRow rw = load_const(p.rows, b);
+    tok0 = rw.tok0;
+    len = rw.len;
+    tblk0 = rw.tblk0;
+    asm volatile("" : "+s"(tok0), "+s"(len), "+s"(tblk0));
+  };
   auto cursor_set = [&](Cursor &c) __attribute__((always_inline)) {
     c.b = use_row(c.u);
+    int tok0, len, tblk0;
+    row_geo(c.b, tok0, len, tblk0);
+    c.tok0 = tok0;
+    c.nr = len * g;
+    const int nqb = (c.nr + QB - 1) / QB;
+    c.pu = nqb - qb_first;
     const int qb = qb_first + c.r;
     const int t0 = qb * (QB / g);                 // GFAST only
-    c.roff = (((int64_t)c.b * Sq + t0) * Hq + kvh * g) * D;
-    // rows at or beyond nrows are positions >= Sq, past the group's last row
-    c.rlim = ((int64_t)(Sq - 1 - t0) * Hq + g) * D * 2;
-    c.toff = (((int64_t)c.b * Hkv + kvh) * nqb + qb) * D * 64;
-    c.soff = ((int64_t)c.b * Hkv + kvh) * nrows + qb * QB;
+    c.roff = (((int64_t)tok0 + t0) * Hq + kvh * g) * D;
+    // rows at or beyond the row's last packed row are positions >= len,
+    // past the group's last row
+    c.rlim = ((int64_t)(len - 1 - t0) * Hq + g) * D * 2;
+    c.toff = ((int64_t)tblk0 + kvh * nqb + qb) * D * 64;
+    c.soff = (int64_t)tok0 * Hq + kvh * c.nr + qb * QB;
   };
   auto cursor_at = [&](int blk) __attribute__((always_inline)) {
     Cursor c;
     c.blk = blk;
-    const int bl = min(blk, nblk - 1);
-    c.u = bl / per_use;
-    c.r = bl - c.u * per_use;
+    int bl = min(blk, nblk - 1);
+    c.u = 0;
+    if (!self) {
+      for (;;) {
+        int tok0, len, tblk0;
+        row_geo(use_row(c.u), tok0, len, tblk0);
+        const int nb = (len * g + QB - 1) / QB;
+        if (bl < nb) break;
+        bl -= nb;
+        ++c.u;
+      }
+    }
+    c.r = bl;
     cursor_set(c);
     return c;
   };
   auto advance = [&](Cursor &c) __attribute__((always_inline)) {
     ++c.blk;
     if (c.blk < nblk) {
-      if (++c.r == per_use) {
+      if (++c.r == c.pu) {
         c.r = 0;
         ++c.u;
         cursor_set(c);
@@ -1023,9 +1061,9 @@ void dkdv_bf16_kernel(DkdvParams p) {
       for (int i = 0; i < RPER; ++i) jb.voff[i] = qfix[i] * 2;
     } else {
       const int r0 = (qb_first + c.r) * QB;
-      const int nv = min(QB, nrows - r0);
+      const int nv = min(QB, c.nr - r0);
       const int t0 = r0 / g;
-      const int64_t head0 = (((int64_t)c.b * Sq + t0) * Hq + kvh * g) * D;
+      const int64_t head0 = (((int64_t)c.tok0 + t0) * Hq + kvh * g) * D;
       // Packed row r is at element ((t - t0) Hq + h) D; rows at or beyond nv
       // lie outside the resource and read as zero.
       auto rowoff = [&](int r) __attribute__((always_inline)) {
@@ -1056,10 +1094,10 @@ void dkdv_bf16_kernel(DkdvParams p) {
   auto issue_t = [&](const Src &x, int i, char *dst) __attribute__((always_inline)) {
     dma16(make_rsrc(x.base, x.bytes), tvoff[i], dst + (q + 4 * i) * 1024);
   };
-  // LSE2 or D (64 floats; lanes at or beyond nrows read zero).
+  // LSE2 or D (64 floats; lanes at or beyond the row's packed rows read zero).
   auto prep_stat = [&](const float *src, const Cursor &c) __attribute__((always_inline)) {
     const int r0 = (qb_first + c.r) * QB;
-    Src x{(const char *)(src + c.soff), c.blk < nblk ? min(QB, nrows - r0) * 4 : 0};
+    Src x{(const char *)(src + c.soff), c.blk < nblk ? min(QB, c.nr - r0) * 4 : 0};
     pin(x);
     return x;
   };
@@ -1410,11 +1448,11 @@ hipError_t launch_dkdv_bf16(const DkdvParams &p, int D, int gx, hipStream_t s) {
 }
 
 hipError_t launch_bwd_transpose_bf16(const PreParams &p, int D, hipStream_t s) {
-  const int64_t grid = (int64_t)p.B * p.Hkv * p.nqb;
+  const dim3 grid((unsigned)(p.Hkv * p.nqb_max), (unsigned)p.B);
   if (D == 64)
-    hipLaunchKernelGGL(bwd_transpose_bf16_kernel<64>, dim3((unsigned)grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(bwd_transpose_bf16_kernel<64>, grid, dim3(256), 0, s, p);
   else
-    hipLaunchKernelGGL(bwd_transpose_bf16_kernel<128>, dim3((unsigned)grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(bwd_transpose_bf16_kernel<128>, grid, dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

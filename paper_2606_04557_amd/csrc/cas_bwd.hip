@@ -22,25 +22,26 @@
 
 namespace cas {
 
+// 16 lanes per packed row; grid.y is the batch row.
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void bwd_pre_kernel(PreParams p) {
   constexpr int LPR = 16;            // lanes per packed row
   constexpr int CPL = D / LPR;       // channels per lane
   const int64_t gid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  const int64_t R = gid / LPR;
+  const int b = blockIdx.y;
+  const DevRow row = p.rows[b];
+  const int nrows = row.len * p.g;
+  const int64_t rb = gid / LPR;      // kvh * nrows + r
   const int li = (int)(gid % LPR);
-  const int64_t total = (int64_t)p.B * p.Hkv * p.nrows;
+  const bool live = rb < (int64_t)p.Hkv * nrows;
   const int Hq = p.Hkv * p.g;
   float acc = 0.0f;
-  int b = 0, h = 0, t = 0;
-  if (R < total) {
-    const int r = (int)(R % p.nrows);
-    const int64_t bk = R / p.nrows;
-    const int kvh = (int)(bk % p.Hkv);
-    b = (int)(bk / p.Hkv);
+  int h = 0, t = 0;
+  if (live) {
+    const int kvh = (int)(rb / nrows), r = (int)(rb % nrows);
     t = r / p.g;
     h = kvh * p.g + (r - t * p.g);
-    const int64_t off = (((int64_t)b * p.Sq + t) * Hq + h) * D + li * CPL;
+    const int64_t off = (((int64_t)row.tok0 + t) * Hq + h) * D + li * CPL;
     const T *op = (const T *)p.o + off;
     const T *dp = (const T *)p.d_o + off;
 #pragma unroll
@@ -48,9 +49,10 @@ __global__ __launch_bounds__(kThreads) void bwd_pre_kernel(PreParams p) {
   }
 #pragma unroll
   for (int m = LPR / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, LPR);
-  if (R < total && li == 0) {
+  if (live && li == 0) {
+    const int64_t R = (int64_t)row.tok0 * Hq + rb;
     p.nd[R] = -acc;
-    p.lse2[R] = p.lse[((int64_t)b * Hq + h) * p.Sq + t] * kLog2e;
+    p.lse2[R] = p.lse[(int64_t)row.lse0 + (int64_t)h * p.lse_hs + t] * kLog2e;
   }
 }
 
@@ -76,7 +78,7 @@ __global__ __launch_bounds__(kThreads) void dkdv_kernel(DkdvParams p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int G = lane >> 5, n = lane & 31;
   const int tile = blockIdx.x, kvh = blockIdx.y;
-  const int g = p.g, Sq = p.Sq, Hkv = p.Hkv, Hq = Hkv * g, nrows = p.nrows;
+  const int g = p.g, Hkv = p.Hkv, Hq = Hkv * g;
   const float c = p.scale_log2;
 
   const T *kbase;
@@ -107,8 +109,10 @@ __global__ __launch_bounds__(kThreads) void dkdv_kernel(DkdvParams p) {
     const int rel = tile - p.cart_tiles;
     self_b = rel / p.self_tiles;
     key0 = (rel % p.self_tiles) * kDkdvKeyTile;
-    klen = Sq;
-    const int64_t base = ((int64_t)self_b * Sq * Hkv + kvh) * D;
+    const DevRow sr = p.rows[self_b];
+    klen = sr.len;
+    if (key0 >= klen) return;   // grid sized for the longest row
+    const int64_t base = ((int64_t)sr.tok0 * Hkv + kvh) * D;
     kbase = (const T *)p.k_self + base;
     vbase = (const T *)p.v_self + base;
     dkp = p.dk_self ? (T *)p.dk_self + base : nullptr;
@@ -133,14 +137,16 @@ __global__ __launch_bounds__(kThreads) void dkdv_kernel(DkdvParams p) {
     dv[dt] = zero16();
   }
 
-  const int nqb = (nrows + QB - 1) / QB;
   const int qb0 = self ? (key0 * g) / QB : 0;
   for (int u = use_b; u < use_e; ++u) {
     const int b = self ? self_b : p.uses[u];
-    const T *qb_base = (const T *)p.q + ((int64_t)b * Sq * Hq + kvh * g) * D;
-    const T *dob_base = (const T *)p.d_o + ((int64_t)b * Sq * Hq + kvh * g) * D;
-    const float *lse2_b = p.lse2 + ((int64_t)b * Hkv + kvh) * nrows;
-    const float *nd_b = p.nd + ((int64_t)b * Hkv + kvh) * nrows;
+    const DevRow rw = p.rows[b];
+    const int nrows = rw.len * g;
+    const int nqb = (nrows + QB - 1) / QB;
+    const T *qb_base = (const T *)p.q + ((int64_t)rw.tok0 * Hq + kvh * g) * D;
+    const T *dob_base = (const T *)p.d_o + ((int64_t)rw.tok0 * Hq + kvh * g) * D;
+    const float *lse2_b = p.lse2 + (int64_t)rw.tok0 * Hq + (int64_t)kvh * nrows;
+    const float *nd_b = p.nd + (int64_t)rw.tok0 * Hq + (int64_t)kvh * nrows;
     for (int qb = qb0; qb < nqb; ++qb) {
       const int r0 = qb * QB;
       const int nv = min(QB, nrows - r0);
@@ -260,8 +266,11 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(DqParams p) {
   const int split = bid % p.splits;
   const int b = bid / p.splits;
 
-  const int g = p.g, Sq = p.Sq, Hkv = p.Hkv, Hq = Hkv * g, nrows = p.nrows;
+  const int g = p.g, Hkv = p.Hkv, Hq = Hkv * g;
+  const DevRow row = p.rows[b];
+  const int tok0 = row.tok0, len = row.len, nrows = len * g;
   const int wg_row0 = qblk * kDqRowsPerWg;
+  if (wg_row0 >= nrows) return;   // grid sized for the longest row
   const int wg_row1 = min(nrows, wg_row0 + kDqRowsPerWg);
   const int row0 = wg_row0 + wave * kDqRowsPerWave;
   const bool wave_active = row0 < nrows;
@@ -272,13 +281,13 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(DqParams p) {
 
   Frag qf[QS][NSTEP], df[QS][NSTEP];
   float lse2r[QS], ndr[QS];
-  const int64_t pk = ((int64_t)b * Hkv + kvh) * nrows;
+  const int64_t pk = (int64_t)tok0 * Hq + (int64_t)kvh * nrows;
 #pragma unroll
   for (int qs = 0; qs < QS; ++qs) {
     const int r = row0 + 32 * qs + n;
     if (r < nrows) {
       const int t = r / g, hh = r - t * g;
-      const int64_t off = (((int64_t)b * Sq + t) * Hq + kvh * g + hh) * D;
+      const int64_t off = (((int64_t)tok0 + t) * Hq + kvh * g + hh) * D;
 #pragma unroll
       for (int s = 0; s < NSTEP; ++s) {
         qf[qs][s] = global_frag<T>((const T *)p.q + off, s, G);
@@ -302,7 +311,6 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(DqParams p) {
 #pragma unroll
     for (int qs = 0; qs < QS; ++qs) acc[dt][qs] = zero16();
 
-  const DevRow row = p.rows[b];
   const int ptiles = row.prefix_tiles;
   const int ntiles = ptiles + wg_t_hi / KT + 1;
   const int tb = (int)((int64_t)ntiles * split / p.splits);
@@ -329,10 +337,10 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(DqParams p) {
       nvalid = min(KT, sd.len - key0);
     } else {
       self0 = (tile - ptiles) * KT;
-      kp = (const T *)p.k_self + (((int64_t)b * Sq + self0) * Hkv + kvh) * D;
-      vp = (const T *)p.v_self + (((int64_t)b * Sq + self0) * Hkv + kvh) * D;
+      kp = (const T *)p.k_self + (((int64_t)tok0 + self0) * Hkv + kvh) * D;
+      vp = (const T *)p.v_self + (((int64_t)tok0 + self0) * Hkv + kvh) * D;
       st = (int64_t)Hkv * D;
-      nvalid = min(KT, Sq - self0);
+      nvalid = min(KT, len - self0);
     }
     __syncthreads();
     if constexpr (BF16) {
@@ -415,7 +423,7 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(DqParams p) {
     const int t = r / g, h = kvh * g + (r - t * g);
     if (p.splits == 1) {
       const float sc = p.scale;
-      T *op = (T *)p.dq + (((int64_t)b * Sq + t) * Hq + h) * D;
+      T *op = (T *)p.dq + (((int64_t)tok0 + t) * Hq + h) * D;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -424,7 +432,7 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(DqParams p) {
                  acc[dt][qs][jj * 4 + 1] * sc, acc[dt][qs][jj * 4 + 2] * sc,
                  acc[dt][qs][jj * 4 + 3] * sc);
     } else {
-      const int64_t prow = (((int64_t)split * p.B + b) * Hkv + kvh) * nrows + r;
+      const int64_t prow = split * p.plane + pk + r;
       float *op = p.part_dq + prow * D;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
@@ -436,30 +444,33 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(DqParams p) {
   }
 }
 
+// One thread per 4 channels of a packed row; grid.y is the batch row.
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void dq_reduce_kernel(DqReduceParams p) {
   constexpr int CPR = D / 4;
   const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  const int64_t plane = (int64_t)p.B * p.Hkv * p.nrows;
-  const int64_t R = idx / CPR;
+  const int b = blockIdx.y;
+  const DevRow row = p.rows[b];
+  const int nrows = row.len * p.g;
+  const int64_t rb = idx / CPR;          // kvh * nrows + r
   const int c4 = (int)(idx % CPR);
-  if (R >= plane) return;
+  if (rb >= (int64_t)p.Hkv * nrows) return;
+  const int64_t plane = p.plane;
+  const int64_t R = (int64_t)row.tok0 * p.Hkv * p.g + rb;
   f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
   for (int s = 0; s < p.splits; ++s)
     acc += *reinterpret_cast<const f32x4 *>(p.part_dq + (s * plane + R) * D + c4 * 4);
-  const int r = (int)(R % p.nrows);
-  const int64_t bk = R / p.nrows;
-  const int kvh = (int)(bk % p.Hkv), b = (int)(bk / p.Hkv);
+  const int kvh = (int)(rb / nrows), r = (int)(rb % nrows);
   const int t = r / p.g, h = kvh * p.g + (r - t * p.g);
   const int Hq = p.Hkv * p.g;
-  T *op = (T *)p.dq + (((int64_t)b * p.Sq + t) * Hq + h) * D + c4 * 4;
+  T *op = (T *)p.dq + (((int64_t)row.tok0 + t) * Hq + h) * D + c4 * 4;
   store4(op, acc[0] * p.scale, acc[1] * p.scale, acc[2] * p.scale, acc[3] * p.scale);
 }
 
 template <typename T, int D>
 static hipError_t launch_pre_t(const PreParams &p, hipStream_t s) {
-  const int64_t n = (int64_t)p.B * p.Hkv * p.nrows * 16;
-  hipLaunchKernelGGL((bwd_pre_kernel<T, D>), dim3((unsigned)((n + kThreads - 1) / kThreads)),
+  const int64_t n = (int64_t)p.Hkv * p.nrows_max * 16;
+  hipLaunchKernelGGL((bwd_pre_kernel<T, D>), dim3((unsigned)((n + kThreads - 1) / kThreads), (unsigned)p.B),
                      dim3(kThreads), 0, s, p);
   return hipGetLastError();
 }
@@ -494,8 +505,8 @@ hipError_t launch_dq(const DqParams &p, DType dt, int D, hipStream_t s) {
 
 template <typename T, int D>
 static hipError_t launch_dq_reduce_t(const DqReduceParams &p, hipStream_t s) {
-  const int64_t n = (int64_t)p.B * p.Hkv * p.nrows * (D / 4);
-  hipLaunchKernelGGL((dq_reduce_kernel<T, D>), dim3((unsigned)((n + kThreads - 1) / kThreads)),
+  const int64_t n = (int64_t)p.Hkv * p.nrows_max * (D / 4);
+  hipLaunchKernelGGL((dq_reduce_kernel<T, D>), dim3((unsigned)((n + kThreads - 1) / kThreads), (unsigned)p.B),
                      dim3(kThreads), 0, s, p);
   return hipGetLastError();
 }

@@ -43,8 +43,11 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdParams p) {
   const int split = bid % p.splits;
   const int b = bid / p.splits;
 
-  const int g = p.g, Sq = p.Sq, Hkv = p.Hkv, Hq = Hkv * g, nrows = p.nrows;
+  const int g = p.g, Hkv = p.Hkv, Hq = Hkv * g;
+  const DevRow row = p.rows[b];
+  const int tok0 = row.tok0, len = row.len, nrows = len * g;
   const int wg_row0 = qblk * kRowsPerWg;
+  if (wg_row0 >= nrows) return;   // grid sized for the longest row
   const int wg_row1 = min(nrows, wg_row0 + kRowsPerWg);
   const int row0 = wg_row0 + wave * kRowsPerWave;
   const bool wave_active = row0 < nrows;
@@ -59,7 +62,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdParams p) {
     const int r = row0 + 32 * qs + n;
     if (r < nrows) {
       const int t = r / g, hh = r - t * g;
-      const T *rp = (const T *)p.q + (((int64_t)b * Sq + t) * Hq + kvh * g + hh) * D;
+      const T *rp = (const T *)p.q + (((int64_t)tok0 + t) * Hq + kvh * g + hh) * D;
 #pragma unroll
       for (int st = 0; st < NSTEP; ++st) qf[qs][st] = global_frag<T>(rp, st, G);
     } else {
@@ -80,7 +83,6 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdParams p) {
     l_run[qs] = 0.0f;
   }
 
-  const DevRow row = p.rows[b];
   const int ptiles = row.prefix_tiles;
   const int ntiles = ptiles + wg_t_hi / KT + 1;
   const int tb = (int)((int64_t)ntiles * split / p.splits);
@@ -107,10 +109,10 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdParams p) {
       nvalid = min(KT, sd.len - key0);
     } else {
       self0 = (tile - ptiles) * KT;
-      kp = (const T *)p.k_self + (((int64_t)b * Sq + self0) * Hkv + kvh) * D;
-      vp = (const T *)p.v_self + (((int64_t)b * Sq + self0) * Hkv + kvh) * D;
+      kp = (const T *)p.k_self + (((int64_t)tok0 + self0) * Hkv + kvh) * D;
+      vp = (const T *)p.v_self + (((int64_t)tok0 + self0) * Hkv + kvh) * D;
       st = (int64_t)Hkv * D;
-      nvalid = min(KT, Sq - self0);
+      nvalid = min(KT, len - self0);
     }
     __syncthreads();
     load_rows<T, D, KT>(k_lds, [&](int r) { return kp + r * st; }, nvalid, tid);
@@ -216,7 +218,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdParams p) {
     const int t = r / g, hh = r - t * g, h = kvh * g + hh;
     if (p.splits == 1) {
       const float inv = 1.0f / lt;
-      T *op = (T *)p.o + (((int64_t)b * Sq + t) * Hq + h) * D;
+      T *op = (T *)p.o + (((int64_t)tok0 + t) * Hq + h) * D;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -225,9 +227,9 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdParams p) {
                  oacc[dt][qs][jj * 4 + 1] * inv, oacc[dt][qs][jj * 4 + 2] * inv,
                  oacc[dt][qs][jj * 4 + 3] * inv);
       if (G == 0 && p.lse != nullptr)
-        p.lse[((int64_t)b * Hq + h) * Sq + t] = (m_run[qs] + log2f(lt)) * kLn2;
+        p.lse[(int64_t)row.lse0 + (int64_t)h * p.lse_hs + t] = (m_run[qs] + log2f(lt)) * kLn2;
     } else {
-      const int64_t prow = (((int64_t)split * p.B + b) * Hkv + kvh) * nrows + r;
+      const int64_t prow = split * p.plane + (int64_t)tok0 * Hq + kvh * nrows + r;
       const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
       float *op = p.part_o + prow * D;
 #pragma unroll
@@ -244,14 +246,19 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdParams p) {
 
 // LSE-weighted combination of split partials:
 //   LSE = log sum_s exp(LSE_s),  O = sum_s exp(LSE_s - LSE) O_s.
+// One thread per 4 channels of a packed row; grid.y is the batch row.
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void fwd_merge_kernel(MergeParams p) {
   constexpr int CPR = D / 4;
   const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  const int64_t plane = (int64_t)p.B * p.Hkv * p.nrows;
-  const int64_t R = idx / CPR;
+  const int b = blockIdx.y;
+  const DevRow row = p.rows[b];
+  const int nrows = row.len * p.g;
+  const int64_t rb = idx / CPR;          // kvh * nrows + r
   const int c4 = (int)(idx % CPR);
-  if (R >= plane) return;
+  if (rb >= (int64_t)p.Hkv * nrows) return;
+  const int64_t plane = p.plane;
+  const int64_t R = (int64_t)row.tok0 * p.Hkv * p.g + rb;
   float mx = -INFINITY;
   for (int s = 0; s < p.splits; ++s) mx = fmaxf(mx, p.part_lse[s * plane + R]);
   float w_sum = 0.0f;
@@ -264,14 +271,12 @@ __global__ __launch_bounds__(kThreads) void fwd_merge_kernel(MergeParams p) {
     acc += w * v;
   }
   const float inv = 1.0f / w_sum;
-  const int r = (int)(R % p.nrows);
-  const int64_t bk = R / p.nrows;
-  const int kvh = (int)(bk % p.Hkv), b = (int)(bk / p.Hkv);
+  const int kvh = (int)(rb / nrows), r = (int)(rb % nrows);
   const int t = r / p.g, h = kvh * p.g + (r - t * p.g);
   const int Hq = p.Hkv * p.g;
-  T *op = (T *)p.o + (((int64_t)b * p.Sq + t) * Hq + h) * D + c4 * 4;
+  T *op = (T *)p.o + (((int64_t)row.tok0 + t) * Hq + h) * D + c4 * 4;
   store4(op, acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
-  if (c4 == 0 && p.lse != nullptr) p.lse[((int64_t)b * Hq + h) * p.Sq + t] = mx + logf(w_sum);
+  if (c4 == 0 && p.lse != nullptr) p.lse[(int64_t)row.lse0 + (int64_t)h * p.lse_hs + t] = mx + logf(w_sum);
 }
 
 template <typename T, int D>
@@ -288,9 +293,9 @@ hipError_t launch_fwd(const FwdParams &p, DType dt, int D, hipStream_t s) {
 
 template <typename T, int D>
 static hipError_t launch_merge_t(const MergeParams &p, hipStream_t s) {
-  const int64_t n = (int64_t)p.B * p.Hkv * p.nrows * (D / 4);
-  const int64_t grid = (n + kThreads - 1) / kThreads;
-  hipLaunchKernelGGL((fwd_merge_kernel<T, D>), dim3((unsigned)grid), dim3(kThreads), 0, s, p);
+  const int64_t n = (int64_t)p.Hkv * p.nrows_max * (D / 4);
+  const dim3 grid((unsigned)((n + kThreads - 1) / kThreads), (unsigned)p.B);
+  hipLaunchKernelGGL((fwd_merge_kernel<T, D>), grid, dim3(kThreads), 0, s, p);
   return hipGetLastError();
 }
 

@@ -33,11 +33,20 @@ struct DevSeg {
   int32_t tile_begin;   // first kKeyTile tile of this entry within the row's prefix
 };
 
+// One batch row (a sample). Its query tokens are tokens tok0 .. tok0+len-1
+// of the token axis of q, o, d_o, dq and the self K/V (row b of a fixed-length
+// batch starts at b * q_len; packed samples start where the previous one
+// ends). Per-row statistics (-D, LSE2, split partials) of KV head kvh and
+// packed row r sit at tok0 * Hq + kvh * len * g + r.
 struct DevRow {
   int32_t seg_begin;
   int32_t seg_end;
   int32_t prefix_tiles;  // kKeyTile tiles over the row's whole prefix
   int32_t tile_begin;    // the row's first entry in the DevTile table
+  int32_t tok0;          // first query token of the row
+  int32_t len;           // query tokens of the row (>= 0)
+  int32_t lse0;          // lse index of (head 0, position 0); head h adds h * lse_hs
+  int32_t tblk0;         // bf16 backward: first transposed 64-row block of the row
 };
 
 // One kKeyTile-key tile of a row's prefix (bf16 forward and dQ): its first key
@@ -62,6 +71,8 @@ struct DevCart {
   int32_t tile_begin;   // first kDkdvKeyTile tile in the dK/dV grid
   int32_t use_begin;    // uses[use_begin .. use_end) = batch rows referencing it
   int32_t use_end;
+  int32_t nblk;         // 64-row query blocks over all uses (sum of the rows' block counts)
+  int32_t pad_;
 };
 
 enum DType : int32_t { kBF16 = 0, kFP32 = 1 };
@@ -72,13 +83,15 @@ struct FwdParams {
   const void *v_self;
   void *o;
   float *lse;
-  float *part_o;      // [splits][B][Hkv][nrows][D] when splits > 1
-  float *part_lse;    // [splits][B][Hkv][nrows]
+  float *part_o;      // [splits][plane][D] when splits > 1 (rows as the statistics)
+  float *part_lse;    // [splits][plane]
   const DevSeg *segs;
   const DevRow *rows;
   const DevTile *tiles;
   int32_t *ovf_flag;  // [grid] bf16: workgroup needs the exact-maximum pass
-  int32_t B, Sq, Hkv, g, nrows, nqblk, splits;
+  int64_t plane;      // T * Hq: rows of one split partial plane
+  int32_t B, Smax, Hkv, g, nrows_max, nqblk, splits;
+  int32_t lse_hs;     // lse head stride (q_len, or T for packed samples)
   float scale_log2;   // softmax_scale * log2(e)
 };
 
@@ -87,19 +100,22 @@ struct MergeParams {
   const float *part_lse;
   void *o;
   float *lse;
-  int32_t B, Sq, Hkv, g, nrows, splits;
+  const DevRow *rows;
+  int64_t plane;
+  int32_t B, Hkv, g, nrows_max, splits, lse_hs;
 };
 
 struct PreParams {
   const void *o;
   const void *d_o;
   const float *lse;
-  float *nd;     // [B][Hkv][nrows]  -rowsum(dO * O)  (D negated)
-  float *lse2;   // [B][Hkv][nrows]  LSE * log2(e)
+  float *nd;     // per-row statistics (see DevRow): -rowsum(dO * O)  (D negated)
+  float *lse2;   // LSE * log2(e)
   const void *q;
-  void *qT;      // bf16: [B][Hkv][nqb][D][64] Q of each 64-row block, transposed
+  void *qT;      // bf16: per row, [Hkv][nqb][D][64] Q of each 64-row block, transposed
   void *doT;     // bf16: same for dO
-  int32_t B, Sq, Hkv, g, nrows, nqb;
+  const DevRow *rows;
+  int32_t B, Hkv, g, nrows_max, nqb_max, lse_hs;
 };
 
 struct DqParams {
@@ -110,11 +126,12 @@ struct DqParams {
   const float *nd;        // -D
   const float *lse2;
   void *dq;
-  float *part_dq;   // [splits][B][Hkv][nrows][D] when splits > 1
+  float *part_dq;   // [splits][plane][D] when splits > 1 (rows as the statistics)
   const DevSeg *segs;
   const DevRow *rows;
   const DevTile *tiles;
-  int32_t B, Sq, Hkv, g, nrows, nqblk, splits;
+  int64_t plane;
+  int32_t B, Smax, Hkv, g, nrows_max, nqblk, splits;
   float scale_log2;
   float scale;
 };
@@ -122,7 +139,9 @@ struct DqParams {
 struct DqReduceParams {
   const float *part_dq;
   void *dq;
-  int32_t B, Sq, Hkv, g, nrows, splits;
+  const DevRow *rows;
+  int64_t plane;
+  int32_t B, Hkv, g, nrows_max, splits;
   float scale;
 };
 
@@ -139,10 +158,11 @@ struct DkdvParams {
   void *dv_self;
   const DevCart *carts;
   const int32_t *uses;
+  const DevRow *rows;
   int32_t n_carts;
   int32_t cart_tiles;       // dK/dV tiles over all distinct cartridges
-  int32_t self_tiles;       // dK/dV tiles per batch row over the self keys
-  int32_t B, Sq, Hkv, g, nrows;
+  int32_t self_tiles;       // dK/dV tiles per batch row over the self keys (longest row)
+  int32_t B, Hkv, g;
   float scale_log2;
   float scale;
 };

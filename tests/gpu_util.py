@@ -80,17 +80,24 @@ class GpuCase:
                      for r in wl.rows]
 
     # -- library calls ---------------------------------------------------------
+    def _layout_kw(self, kw):
+        if self.wl.packed:
+            kw = dict(kw)
+            kw.setdefault("q_offsets", self.wl.q_offsets)
+        return kw
+
     def fwd(self, **kw):
         import paper_2606_04557_amd as cas
         wl = self.wl
         return cas.prefix_attn_fwd(self.q, self.k_self, self.v_self, self.rows, wl.num_kv_heads,
-                                   wl.group_size, float(wl.scale), **kw)
+                                   wl.group_size, float(wl.scale), **self._layout_kw(kw))
 
     def bwd(self, o, lse, **kw):
         import paper_2606_04557_amd as cas
         wl = self.wl
         return cas.prefix_attn_bwd(self.q, self.k_self, self.v_self, self.rows, wl.num_kv_heads,
-                                   wl.group_size, float(wl.scale), o, lse, self.d_o, **kw)
+                                   wl.group_size, float(wl.scale), o, lse, self.d_o,
+                                   **self._layout_kw(kw))
 
     # -- oracle inputs ---------------------------------------------------------
     def oracle_args(self):
@@ -116,6 +123,14 @@ def rel_err(gpu: np.ndarray, ref: np.ndarray) -> float:
 
 def full_oracle(case: GpuCase, backward: bool = True):
     args = case.oracle_args()
+    if case.wl.packed:
+        q, ks, vs, ck, cv, rows, scale, g = args
+        qo = case.wl.q_offsets
+        O, LSE = oracle.packed_forward(q, ks, vs, ck, cv, rows, qo, scale, g)
+        if not backward:
+            return O, LSE, None
+        grads = oracle.packed_backward(q, ks, vs, ck, cv, rows, qo, scale, g, case.oracle_do(), O=O, LSE=LSE)
+        return O, LSE, grads
     O, LSE = oracle.forward(*args)
     if not backward:
         return O, LSE, None

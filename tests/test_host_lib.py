@@ -27,7 +27,7 @@ def test_exports_match_header(lib):
     assert declared == sorted(_lib.EXPORTS)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.cas_abi_version() == 1
+    assert lib.cas_abi_version() == _lib.ABI_VERSION == 2
     assert lib.cas_status_string(_lib.CAS_ERR_NOT_PINNED) == b"CAS_ERR_NOT_PINNED"
 
 
@@ -243,3 +243,55 @@ def test_stage_validation_without_device(lib):
     assert lib.cas_cartridge_stage(arr, 1, None, None) == _lib.CAS_ERR_INVALID_ARGUMENT
     # Zero copies is a no-op.
     assert lib.cas_cartridge_stage(None, 0, None, None) == _lib.CAS_OK
+
+
+def _packed(f, offs):
+    arr = (ctypes.c_int32 * len(offs))(*offs)
+    f.keep = arr
+    f.p.q_offsets = ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32))
+    f.p.q_len = 0
+
+
+@pytest.mark.parametrize("offs,q_len,ok", [
+    ((0, 5, 9), 0, True),
+    ((0, 0, 9), 0, True),            # an empty sample
+    ((0, 5, 9), 4, False),           # q_len must be 0 with q_offsets
+    ((1, 5, 9), 0, False),           # q_offsets[0] != 0
+    ((0, 6, 5), 0, False),           # decreasing
+    ((0, 0, 0), 0, False),           # no query token at all
+])
+def test_packed_offsets_validation(lib, offs, q_len, ok):
+    f = Fake(B=2, Sq=1, rows=((16,), (8,)))
+    _packed(f, offs)
+    f.p.q_len = q_len
+    n = ctypes.c_size_t(0)
+    st = lib.cas_prefix_attn_workspace_size(ctypes.byref(f.p), 1, ctypes.byref(n))
+    if ok:
+        assert st == _lib.CAS_OK, _msg(lib)
+        assert n.value > 0
+    else:
+        assert st == _lib.CAS_ERR_INVALID_ARGUMENT, _msg(lib)
+        assert f.fwd(lib) == _lib.CAS_ERR_INVALID_ARGUMENT
+
+
+def test_packed_equal_lengths_plan_like_fixed(lib):
+    """Equal-length packed samples plan exactly like the fixed-length batch."""
+    for bwd in (0, 1):
+        a = Fake(B=3, Sq=70, Hkv=2, g=4, D=128, rows=((40, 3), (129,), ()))
+        b = Fake(B=3, Sq=70, Hkv=2, g=4, D=128, rows=((40, 3), (129,), ()))
+        _packed(b, (0, 70, 140, 210))
+        na, nb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+        assert lib.cas_prefix_attn_workspace_size(ctypes.byref(a.p), bwd, ctypes.byref(na)) == _lib.CAS_OK
+        assert lib.cas_prefix_attn_workspace_size(ctypes.byref(b.p), bwd, ctypes.byref(nb)) == _lib.CAS_OK
+        assert na.value == nb.value
+    ia, ib = _lib.PlanInfo(), _lib.PlanInfo()
+    assert lib.cas_plan_info(ctypes.byref(a.p), ctypes.byref(ia)) == _lib.CAS_OK
+    assert lib.cas_plan_info(ctypes.byref(b.p), ctypes.byref(ib)) == _lib.CAS_OK
+    for fld, _ in _lib.PlanInfo._fields_:
+        assert getattr(ia, fld) == getattr(ib, fld), fld
+    # Uneven samples: grids are sized for the longest sample.
+    c = Fake(B=3, Sq=1, Hkv=2, g=4, D=128, rows=((40,), (), (7,)))
+    _packed(c, (0, 300, 301, 301))
+    ic = _lib.PlanInfo()
+    assert lib.cas_plan_info(ctypes.byref(c.p), ctypes.byref(ic)) == _lib.CAS_OK
+    assert ic.dkdv_workgroups == (1 + 1 + 3 * 3) * 2     # 2 cartridge tiles + 3 rows x 3 self tiles

@@ -378,3 +378,90 @@ def test_sampled_paths_match_full():
                 ek, ev = dks[-cart - 1, toks, kv], dvs[-cart - 1, toks, kv]
             assert np.abs(dk - ek).max() <= 1e-13
             assert np.abs(dv - ev).max() <= 1e-13
+
+
+# ---------------------------------------------------------------------------
+# Packed samples (one token axis, per-sample cartridges, block-diagonal self).
+# ---------------------------------------------------------------------------
+
+def _packed_problem(seed, q_lens=(3, 0, 2, 1), Hq=2, Hkv=1, D=4, lens=(2, 1, 3),
+                    rows=((0, 1), (2,), (1, 1, 0), ())):
+    r = np.random.default_rng(seed)
+    T = sum(q_lens)
+    qo = [0] + list(np.cumsum(q_lens))
+    return dict(q=r.standard_normal((T, Hq, D)), k_self=r.standard_normal((T, Hkv, D)),
+                v_self=r.standard_normal((T, Hkv, D)),
+                cart_k=[r.standard_normal((L, Hkv, D)) for L in lens],
+                cart_v=[r.standard_normal((L, Hkv, D)) for L in lens],
+                rows=[list(x) for x in rows], q_offsets=qo, scale=0.41, group_size=Hq // Hkv,
+                d_o=r.standard_normal((T, Hq, D)))
+
+
+def _pfwd(p, **over):
+    a = dict(p, **over)
+    return oracle.packed_forward(a["q"], a["k_self"], a["v_self"], a["cart_k"], a["cart_v"], a["rows"],
+                                 a["q_offsets"], a["scale"], a["group_size"])
+
+
+def test_p12_packed_finite_differences():
+    """P12: the packed backward equals central differences of sum(dO * O) for
+    every input element, with a cartridge shared by two samples (and twice in
+    one), an empty sample whose cartridge no one else uses, and a sample with
+    no cartridge."""
+    p = _packed_problem(12)
+    dq, dks, dvs, dck, dcv = oracle.packed_backward(
+        p["q"], p["k_self"], p["v_self"], p["cart_k"], p["cart_v"], p["rows"], p["q_offsets"],
+        p["scale"], p["group_size"], p["d_o"])
+
+    def loss(**over):
+        O, _ = _pfwd(p, **over)
+        return float((p["d_o"] * O).sum())
+
+    h = 1e-5
+
+    def fd(name, arr, idx=None):
+        out = np.zeros_like(arr)
+        for ix in itertools.product(*[range(n) for n in arr.shape]):
+            a1 = arr.copy(); a1[ix] += h
+            a2 = arr.copy(); a2[ix] -= h
+            if idx is None:
+                out[ix] = (loss(**{name: a1}) - loss(**{name: a2})) / (2 * h)
+            else:
+                l1 = list(p[name]); l1[idx] = a1
+                l2 = list(p[name]); l2[idx] = a2
+                out[ix] = (loss(**{name: l1}) - loss(**{name: l2})) / (2 * h)
+        return out
+
+    def close(a, b):
+        den = max(np.abs(b).max(), 1e-12)
+        assert np.abs(a - b).max() / den <= 1e-7, (np.abs(a - b).max(), den)
+
+    close(dq, fd("q", p["q"]))
+    close(dks, fd("k_self", p["k_self"]))
+    close(dvs, fd("v_self", p["v_self"]))
+    for c in range(len(p["cart_k"])):
+        close(dck[c], fd("cart_k", p["cart_k"][c], c))
+        close(dcv[c], fd("cart_v", p["cart_v"][c], c))
+    # Cartridge 2 is seen only by the empty sample: no gradient at all.
+    assert not dck[2].any() and not dcv[2].any()
+
+
+def test_p13_packed_block_diagonal_and_fixed_layout():
+    """P13: (a) a sample's outputs ignore every other sample's tokens
+    (block-diagonal self); (b) equal-length packed samples are the
+    fixed-length batch, with LSE laid out [Hq, T] instead of [B, Hq, Sq]."""
+    p = _packed_problem(13, q_lens=(3, 2), rows=((0, 2), (1,)))
+    O, LSE = _pfwd(p)
+    q2, k2 = p["q"].copy(), p["k_self"].copy()
+    q2[3:] += 5.0
+    k2[3:] -= 3.0
+    O2, LSE2 = _pfwd(p, q=q2, k_self=k2)
+    assert np.array_equal(O[:3], O2[:3]) and np.array_equal(LSE[:, :3], LSE2[:, :3])
+    assert not np.allclose(O[3:], O2[3:])
+    f = _packed_problem(14, q_lens=(2, 2, 2), rows=((0,), (1, 0), ()))
+    Of, LSEf = oracle.forward(f["q"].reshape(3, 2, 2, 4), f["k_self"].reshape(3, 2, 1, 4),
+                              f["v_self"].reshape(3, 2, 1, 4), f["cart_k"], f["cart_v"], f["rows"],
+                              f["scale"], f["group_size"])
+    Op, LSEp = _pfwd(f)
+    assert np.allclose(Op, Of.reshape(6, 2, 4), rtol=0, atol=1e-14)
+    assert np.allclose(LSEp, LSEf.transpose(1, 0, 2).reshape(2, 6), rtol=0, atol=1e-14)

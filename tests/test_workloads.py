@@ -71,3 +71,18 @@ def test_tensors_are_seeded_and_substreamed():
     assert np.array_equal(a["cart_k"][1], b["cart_k"][1])
     assert b["cart_k"][0] is None
     assert not np.array_equal(a["cart_k"][1][:2], a["cart_v"][1][:2])
+
+
+def test_packed_training_layout():
+    """8,192 packed tokens; every sample sees its target and at most 10
+    distractors, all distinct, from a 20-cartridge pool; cartridge lengths are
+    multiples of 16."""
+    w = casgen.packed()
+    assert w.packed and w.q_len == 0 and sum(w.q_lens) == 8192 and w.q_offsets[-1] == 8192
+    assert len(w.cart_lens) == 20 and all(L % 16 == 0 and 256 <= L <= 2048 for L in w.cart_lens)
+    assert all(1 <= len(r) <= 11 and len(set(r)) == len(r) for r in w.rows)
+    assert any(len(r) == 1 for r in w.rows) and any(len(r) > 1 for r in w.rows)
+    T = casgen.make_tensors(w)
+    assert T["q"].shape == (8192, 32, 128) and T["k_self"].shape == (8192, 8, 128)
+    pairs = sum(L * w.prefix_len(b) + L * (L + 1) // 2 for b, L in enumerate(w.q_lens)) * 32
+    assert w.visible_pairs() == pairs
