@@ -71,18 +71,20 @@ def cpu_baseline(wl, T, heads: int = 1):
     except Exception:
         cores = 1
     f = lambda a: None if a is None else casgen.to_float(a, wl.dtype)
-    q, ks, vs, do = f(T["q"]), f(T["k_self"]), f(T["v_self"]), f(T["d_o"])
+    # Batch row 0's query tokens in either layout.
+    row0 = (lambda a: a[0:wl.row_lens[0]]) if wl.packed else (lambda a: a[0])
+    q, ks, vs, do = (row0(f(T[n])) for n in ("q", "k_self", "v_self", "d_o"))
     ck = [f(a) for a in T["cart_k"]]
     cv = [f(a) for a in T["cart_v"]]
-    Sq = wl.q_len
+    Sq = wl.row_lens[0]
     t_all = np.arange(Sq)
     elapsed = 0.0
     pairs = 0
     for h in range(heads):
         kv = h // wl.group_size
-        K, V, npre = oracle.row_keys(ck, cv, wl.rows[0], ks[0], vs[0], kv)
-        qh = q[0, :, h, :].astype(np.float64)
-        doh = do[0, :, h, :].astype(np.float64)
+        K, V, npre = oracle.row_keys(ck, cv, wl.rows[0], ks, vs, kv)
+        qh = q[:, h, :].astype(np.float64)
+        doh = do[:, h, :].astype(np.float64)
         t0 = time.perf_counter()
         o, lse, _ = oracle.head_forward(qh, K, V, npre, Sq, t_all, float(wl.scale))
         oracle.head_backward(qh, K, V, npre, Sq, t_all, float(wl.scale), doh, o, lse)
@@ -100,6 +102,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=3, help="workload 1-4 (5 is forward-only)")
+    ap.add_argument("--packed", action="store_true",
+                    help="the 8,192-token packed training layout instead of --config")
     ap.add_argument("--cpu-heads", type=int, default=16, help="oracle heads timed for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "hbm_traffic_16x2k.json"),
@@ -130,7 +134,7 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "copies": 5}), flush=True)
         return
-    wl = casgen.config(args.config)
+    wl = casgen.packed() if args.packed else casgen.config(args.config)
     if wl.forward_only:
         print("bench.py times forward+backward; pick config 1-4", file=sys.stderr)
         sys.exit(2)
@@ -152,20 +156,23 @@ def main():
     dV = {c: torch.empty_like(V[c]) for c in used}
     rows = [[cas.Segment(K[c], V[c], dK[c], dV[c]) for c in r] for r in wl.rows]
     Hkv, g, scale = wl.num_kv_heads, wl.group_size, float(wl.scale)
+    qo = wl.q_offsets if wl.packed else None
     o = torch.empty_like(q)
-    lse = torch.empty((wl.batch, wl.num_q_heads, wl.q_len), dtype=torch.float32, device="cuda")
+    lse_shape = (wl.num_q_heads, sum(wl.row_lens)) if wl.packed else (wl.batch, wl.num_q_heads, wl.q_len)
+    lse = torch.empty(lse_shape, dtype=torch.float32, device="cuda")
     dq = torch.empty_like(q)
     dks, dvs = torch.empty_like(k_self), torch.empty_like(v_self)
-    prob = cas.Problem.from_tensors(q, rows, Hkv, g, scale)
+    prob = cas.Problem.from_tensors(q, rows, Hkv, g, scale, qo)
     ws = torch.empty(max(cas.workspace_size(prob, False), cas.workspace_size(prob, True)),
                      dtype=torch.uint8, device="cuda")
     plan = cas.plan_info(prob)
     log("plan", plan)
 
     def step():
-        cas.prefix_attn_fwd(q, k_self, v_self, rows, Hkv, g, scale, o=o, lse=lse, workspace=ws)
+        cas.prefix_attn_fwd(q, k_self, v_self, rows, Hkv, g, scale, o=o, lse=lse, workspace=ws,
+                            q_offsets=qo)
         cas.prefix_attn_bwd(q, k_self, v_self, rows, Hkv, g, scale, o, lse, d_o, dq=dq,
-                            dk_self=dks, dv_self=dvs, workspace=ws)
+                            dk_self=dks, dv_self=dvs, workspace=ws, q_offsets=qo)
 
     for _ in range(args.warmup):
         step()
@@ -194,7 +201,7 @@ def main():
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
     achieved = wl.flops(per_pair) / (avg_ms * 1e-3) / 1e12 if per_pair else None
     traffic = None
-    if args.traffic and os.path.exists(args.traffic) and args.config == 3:
+    if args.traffic and os.path.exists(args.traffic) and args.config == 3 and not args.packed:
         with open(args.traffic) as fh:
             rec = json.load(fh)
         if rec.get("source_sha256_16") == kernel_source_hash():
@@ -218,13 +225,19 @@ def main():
         "vs_baseline": None,
         "dtype": wl.dtype,
         "data": "synthetic (seeded Gaussian Q/K/V/dO; no model weights or datasets)",
-        "config": {"workload": f"{wl.name}: {wl.description}", "batch": wl.batch,
-                   "q_len": wl.q_len, "num_q_heads": wl.num_q_heads, "num_kv_heads": Hkv,
-                   "head_dim": wl.head_dim, "cartridges_per_row": len(wl.rows[0]),
-                   "prefix_tokens_per_row": wl.prefix_len(0), "parallelism": "single GPU"},
+        "config": ({"workload": f"{wl.name}: {wl.description}", "batch": wl.batch,
+                    "q_len": wl.q_len, "num_q_heads": wl.num_q_heads, "num_kv_heads": Hkv,
+                    "head_dim": wl.head_dim, "cartridges_per_row": len(wl.rows[0]),
+                    "prefix_tokens_per_row": wl.prefix_len(0), "parallelism": "single GPU"}
+                   if not wl.packed else
+                   {"workload": f"{wl.name}: {wl.description}", "samples": wl.batch,
+                    "sample_tokens": wl.row_lens, "cartridges_per_sample": [len(r) for r in wl.rows],
+                    "prefix_tokens_per_sample": [wl.prefix_len(b) for b in range(wl.batch)],
+                    "num_q_heads": wl.num_q_heads, "num_kv_heads": Hkv, "head_dim": wl.head_dim,
+                    "parallelism": "single GPU"}),
         "mfma_frac_of_step": value / peak,
         "tflops_fa14": wl.flops(14) / (ms * 1e-3) / 1e12,
-        "query_tokens_per_s": wl.batch * wl.q_len / (ms * 1e-3),
+        "query_tokens_per_s": sum(wl.row_lens) / (ms * 1e-3),
         "kernels": kernels,
         "roofline": roofline,
         "cpu_baseline": None,

@@ -95,13 +95,16 @@ struct Plan {
   std::vector<DevTile> tiles;
   std::vector<DevCart> carts;
   std::vector<int32_t> uses;
+  std::vector<DevWg> order;       // dK/dV workgroups, longest first
+  int self_tiles_max = 0;         // dK/dV self tiles of the longest row
+  int64_t order_cap = 0;          // order entries with every self tile
   int64_t max_prefix = 0;
   int fwd_splits = 1, dq_splits = 1;
   int nqblk_fwd = 0, nqblk_dq = 0;
-  int cart_tiles = 0, self_tiles = 0;
+  int cart_tiles = 0;
   bool want_self_grad = false;
   // workspace layout
-  size_t off_segs = 0, off_rows = 0, off_tiles = 0, off_carts = 0, off_uses = 0, table_bytes = 0;
+  size_t off_segs = 0, off_rows = 0, off_tiles = 0, off_carts = 0, off_uses = 0, off_order = 0, table_bytes = 0;
   size_t off_part_o = 0, off_part_lse = 0, off_ovf = 0, ws_fwd = 0;
   size_t off_nd = 0, off_lse2 = 0, off_part_dq = 0, off_qT = 0, off_doT = 0, ws_bwd = 0;
 };
@@ -337,6 +340,12 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
     }
     if (tiles > INT32_MAX / 2) return fail(CAS_ERR_UNSUPPORTED, "too many key tiles");
     pl.cart_tiles = (int)tiles;
+    pl.self_tiles_max = (int)ceil_div(pl.Smax, kDkdvKeyTile);
+    int64_t self_tiles = 0;
+    for (int b = 0; b < pl.B; ++b) self_tiles += ceil_div(pl.len[b], kDkdvKeyTile);
+    pl.order_cap = (tiles + self_tiles) * Hkv;
+    if (tiles + (int64_t)pl.B * pl.self_tiles_max > INT32_MAX / 2 || pl.order_cap > INT32_MAX)
+      return fail(CAS_ERR_UNSUPPORTED, "too many key tiles");
   }
 
   // Workspace layout.
@@ -352,6 +361,8 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
     off = align_up(off + pl.carts.size() * sizeof(DevCart), 256);
     pl.off_uses = off;
     off = align_up(off + pl.uses.size() * sizeof(int32_t), 256);
+    pl.off_order = off;
+    off = align_up(off + (size_t)pl.order_cap * sizeof(DevWg), 256);
   }
   pl.table_bytes = off;
   const size_t plane = (size_t)pl.T * pl.Hq;   // packed rows of all batch rows and KV heads
@@ -388,6 +399,41 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
     pl.ws_bwd = off;
   }
   return CAS_OK;
+}
+
+// dK/dV workgroup list: every cartridge tile (and, with self gradients, every
+// self tile of every row) at every KV head, sorted by the number of 64-row
+// query blocks the workgroup walks, most first; ties keep KV head, then tile
+// order. Longest-first dispatch keeps the long workgroups off the tail.
+void build_dkdv_order(Plan &pl, bool with_self) {
+  struct E {
+    int64_t nblk;
+    int32_t tile, kvh;
+  };
+  std::vector<E> v;
+  v.reserve((size_t)pl.order_cap);
+  for (const DevCart &c : pl.carts) {
+    const int n = (int)ceil_div(c.len, kDkdvKeyTile);
+    for (int kvh = 0; kvh < pl.Hkv; ++kvh)
+      for (int t = 0; t < n; ++t) v.push_back({c.nblk, c.tile_begin + t, kvh});
+  }
+  if (with_self) {
+    for (int b = 0; b < pl.B; ++b) {
+      const int64_t nqb = ceil_div((int64_t)pl.len[b] * pl.g, kDkdvQBlock);
+      const int n = (int)ceil_div(pl.len[b], kDkdvKeyTile);
+      for (int kvh = 0; kvh < pl.Hkv; ++kvh)
+        for (int j = 0; j < n; ++j)
+          v.push_back({nqb - ((int64_t)j * kDkdvKeyTile * pl.g) / kDkdvQBlock,
+                       pl.cart_tiles + b * pl.self_tiles_max + j, kvh});
+    }
+  }
+  std::stable_sort(v.begin(), v.end(), [](const E &a, const E &b) {
+    if (a.nblk != b.nblk) return a.nblk > b.nblk;
+    if (a.kvh != b.kvh) return a.kvh < b.kvh;
+    return a.tile < b.tile;
+  });
+  pl.order.resize(v.size());
+  for (size_t i = 0; i < v.size(); ++i) pl.order[i] = {v[i].tile, v[i].kvh};
 }
 
 // Turns the self-tile offsets of the tile table into pointers.
@@ -483,6 +529,7 @@ cas_status_t upload_tables(const Plan &pl, bool bwd, void *ws, hipStream_t strea
   if (bwd) {
     if (!pl.carts.empty()) std::memcpy(h + pl.off_carts, pl.carts.data(), pl.carts.size() * sizeof(DevCart));
     if (!pl.uses.empty()) std::memcpy(h + pl.off_uses, pl.uses.data(), pl.uses.size() * sizeof(int32_t));
+    if (!pl.order.empty()) std::memcpy(h + pl.off_order, pl.order.data(), pl.order.size() * sizeof(DevWg));
   }
   e = hipMemcpyAsync(ws, h, pl.table_bytes, hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipMemcpyAsync: ") + hipGetErrorString(e));
@@ -611,10 +658,9 @@ cas_status_t cas_plan_info(const cas_problem_t *p, cas_plan_info_t *out) {
   out->fwd_splits = pf.fwd_splits;
   out->dq_splits = pb.dq_splits;
   out->fwd_workgroups = pf.nqblk_fwd * pf.Hkv * pf.B * pf.fwd_splits;
-  const int self_tiles = (int)ceil_div(pb.Smax, kDkdvKeyTile);
-  out->dkdv_workgroups = (pb.cart_tiles + pb.B * self_tiles) * pb.Hkv;
+  out->dkdv_workgroups = (int32_t)pb.order_cap;
   out->unique_segments = (int32_t)pb.carts.size();
-  out->total_key_tiles = pb.cart_tiles + pb.B * self_tiles;
+  out->total_key_tiles = (int32_t)(pb.order_cap / pb.Hkv);
   out->max_prefix_len = pf.max_prefix;
   out->ws_fwd_bytes = pf.ws_fwd;
   out->ws_bwd_bytes = pb.ws_bwd;
@@ -725,6 +771,7 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
 
   hipStream_t stream = (hipStream_t)hip_stream;
   bind_self_tiles(pl, k_self, v_self);
+  build_dkdv_order(pl, dk_self || dv_self);
   s = upload_tables(pl, true, workspace, stream);
   if (s != CAS_OK) return s;
   char *ws = (char *)workspace;
@@ -751,9 +798,8 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
   hipError_t e = timed("bwd_pre", stream, [&] { return launch_bwd_pre(pp, pl.dt, pl.D, stream); });
   if (e != hipSuccess) return hip_fail("bwd_pre launch", e);
 
-  const int self_tiles = (dk_self || dv_self) ? (int)ceil_div(pl.Smax, kDkdvKeyTile) : 0;
-  const int gx = pl.cart_tiles + pl.B * self_tiles;
-  if (gx > 0) {
+  const int n_wg = (int)pl.order.size();
+  if (n_wg > 0) {
     DkdvParams kp{};
     kp.q = q;
     kp.k_self = k_self;
@@ -768,9 +814,10 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
     kp.carts = (const DevCart *)(ws + pl.off_carts);
     kp.uses = (const int32_t *)(ws + pl.off_uses);
     kp.rows = pp.rows;
+    kp.order = (const DevWg *)(ws + pl.off_order);
     kp.n_carts = (int32_t)pl.carts.size();
     kp.cart_tiles = pl.cart_tiles;
-    kp.self_tiles = std::max(self_tiles, 1);
+    kp.self_tiles = std::max(pl.self_tiles_max, 1);
     kp.B = pl.B;
     kp.Hkv = pl.Hkv;
     kp.g = pl.g;
@@ -780,7 +827,7 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
       e = timed("bwd_transpose", stream, [&] { return launch_bwd_transpose_bf16(pp, pl.D, stream); });
       if (e != hipSuccess) return hip_fail("bwd_transpose launch", e);
     }
-    e = timed("dkdv", stream, [&] { return launch_dkdv(kp, pl.dt, pl.D, gx, stream); });
+    e = timed("dkdv", stream, [&] { return launch_dkdv(kp, pl.dt, pl.D, n_wg, stream); });
     if (e != hipSuccess) return hip_fail("dkdv launch", e);
   }
 

@@ -105,7 +105,10 @@ __device__ __forceinline__ void fence_regs(T (&v)[N]) {
 // round-robin over the 8 XCDs (each with its own L2); this remaps them so
 // that each XCD receives one contiguous range of logical ids. Workgroups that
 // stream the same K/V tiles (same batch row and KV head, adjacent logical
-// ids) then share one L2 instead of fetching every tile once per XCD.
+// ids) then share one L2 instead of fetching every tile once per XCD. With
+// the KV head as the slowest logical index, each XCD gets whole KV heads
+// (when their count is a multiple of 8): the same work on every XCD even
+// when the batch rows differ in length.
 constexpr int kXcds = 8;
 __device__ __forceinline__ int xcd_order(int bid, int n) {
   const int per = n / kXcds;
@@ -198,13 +201,15 @@ void fwd_bf16_kernel(FwdParams p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2;
   const int G = lane >> 5, n = lane & 31;
+  // Logical order: row block fastest, then split, batch row, KV head (the
+  // KV heads split the XCDs evenly whatever the rows' lengths).
   int bid = xcd_order(blockIdx.x, gridDim.x);
   const int qblk = __builtin_amdgcn_readfirstlane(bid % p.nqblk);
   bid /= p.nqblk;
-  const int kvh = __builtin_amdgcn_readfirstlane(bid % p.Hkv);
-  bid /= p.Hkv;
   const int split = __builtin_amdgcn_readfirstlane(bid % p.splits);
-  const int b = __builtin_amdgcn_readfirstlane(bid / p.splits);
+  bid /= p.splits;
+  const int b = __builtin_amdgcn_readfirstlane(bid % p.B);
+  const int kvh = __builtin_amdgcn_readfirstlane(bid / p.B);
   const int g = p.g, Hkv = p.Hkv, Hq = Hkv * g;
   const DevRow row = load_const(p.rows, b);
   const int tok0 = __builtin_amdgcn_readfirstlane(row.tok0);
@@ -571,13 +576,15 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = lane >> 5, n = lane & 31;
+  // Logical order: row block fastest, then split, batch row, KV head (the
+  // KV heads split the XCDs evenly whatever the rows' lengths).
   int bid = xcd_order(blockIdx.x, gridDim.x);
   const int qblk = __builtin_amdgcn_readfirstlane(bid % p.nqblk);
   bid /= p.nqblk;
-  const int kvh = __builtin_amdgcn_readfirstlane(bid % p.Hkv);
-  bid /= p.Hkv;
   const int split = __builtin_amdgcn_readfirstlane(bid % p.splits);
-  const int b = __builtin_amdgcn_readfirstlane(bid / p.splits);
+  bid /= p.splits;
+  const int b = __builtin_amdgcn_readfirstlane(bid % p.B);
+  const int kvh = __builtin_amdgcn_readfirstlane(bid / p.B);
 
   const int g = p.g, Hkv = p.Hkv, Hq = Hkv * g;
   const DevRow row = load_const(p.rows, b);
@@ -855,7 +862,8 @@ void dkdv_bf16_kernel(DkdvParams p) {
   const int G = lane >> 5, n = lane & 31;
   const int q = wave & 3;                      // SIMD, key quarter, index within the wave's group
   const bool pwave = wave < 4;
-  const int tile = blockIdx.x, kvh = blockIdx.y;
+  const DevWg wg = load_const(p.order, (int)blockIdx.x);
+  const int tile = __builtin_amdgcn_readfirstlane(wg.tile), kvh = __builtin_amdgcn_readfirstlane(wg.kvh);
   const int g = p.g, Hkv = p.Hkv, Hq = Hkv * g;
   const float c = p.scale_log2;
 
@@ -1434,8 +1442,8 @@ hipError_t launch_dq_bf16(const DqParams &p, int D, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_dkdv_bf16(const DkdvParams &p, int D, int gx, hipStream_t s) {
-  const dim3 grid((unsigned)gx, (unsigned)p.Hkv);
+hipError_t launch_dkdv_bf16(const DkdvParams &p, int D, int n_wg, hipStream_t s) {
+  const dim3 grid((unsigned)n_wg);
   const bool gfast = kDkdvQBlock % p.g == 0;
   if (D == 64) {
     if (gfast) hipLaunchKernelGGL((dkdv_bf16_kernel<64, true>), grid, dim3(kFastThreads), 0, s, p);

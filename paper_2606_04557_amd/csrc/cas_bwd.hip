@@ -77,7 +77,8 @@ __global__ __launch_bounds__(kThreads) void dkdv_kernel(DkdvParams p) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int G = lane >> 5, n = lane & 31;
-  const int tile = blockIdx.x, kvh = blockIdx.y;
+  const DevWg wg = p.order[blockIdx.x];
+  const int tile = wg.tile, kvh = wg.kvh;
   const int g = p.g, Hkv = p.Hkv, Hq = Hkv * g;
   const float c = p.scale_log2;
 
@@ -481,14 +482,14 @@ hipError_t launch_bwd_pre(const PreParams &p, DType dt, int D, hipStream_t s) {
 }
 
 template <typename T, int D>
-static hipError_t launch_dkdv_t(const DkdvParams &p, int gx, hipStream_t s) {
-  hipLaunchKernelGGL((dkdv_kernel<T, D>), dim3((unsigned)gx, (unsigned)p.Hkv), dim3(kThreads), 0, s, p);
+static hipError_t launch_dkdv_t(const DkdvParams &p, int n_wg, hipStream_t s) {
+  hipLaunchKernelGGL((dkdv_kernel<T, D>), dim3((unsigned)n_wg), dim3(kThreads), 0, s, p);
   return hipGetLastError();
 }
 
-hipError_t launch_dkdv(const DkdvParams &p, DType dt, int D, int gx, hipStream_t s) {
-  if (dt == kBF16) return launch_dkdv_bf16(p, D, gx, s);
-  return D == 64 ? launch_dkdv_t<float, 64>(p, gx, s) : launch_dkdv_t<float, 128>(p, gx, s);
+hipError_t launch_dkdv(const DkdvParams &p, DType dt, int D, int n_wg, hipStream_t s) {
+  if (dt == kBF16) return launch_dkdv_bf16(p, D, n_wg, s);
+  return D == 64 ? launch_dkdv_t<float, 64>(p, n_wg, s) : launch_dkdv_t<float, 128>(p, n_wg, s);
 }
 
 template <typename T, int D>

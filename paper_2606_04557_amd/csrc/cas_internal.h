@@ -75,6 +75,15 @@ struct DevCart {
   int32_t pad_;
 };
 
+// One dK/dV workgroup: a key tile (cartridge tiles first, then self tile
+// j of batch row b as cart_tiles + b * self_tiles + j) and a KV head. The host
+// lists them longest first (most query blocks), so the long workgroups of
+// every KV head start in the first wave of the dispatch.
+struct DevWg {
+  int32_t tile;
+  int32_t kvh;
+};
+
 enum DType : int32_t { kBF16 = 0, kFP32 = 1 };
 
 struct FwdParams {
@@ -159,6 +168,7 @@ struct DkdvParams {
   const DevCart *carts;
   const int32_t *uses;
   const DevRow *rows;
+  const DevWg *order;       // [grid] the workgroups' tiles and KV heads
   int32_t n_carts;
   int32_t cart_tiles;       // dK/dV tiles over all distinct cartridges
   int32_t self_tiles;       // dK/dV tiles per batch row over the self keys (longest row)
@@ -173,12 +183,12 @@ hipError_t launch_fwd_merge(const MergeParams &p, DType dt, int D, hipStream_t s
 hipError_t launch_bwd_pre(const PreParams &p, DType dt, int D, hipStream_t s);
 hipError_t launch_dq(const DqParams &p, DType dt, int D, hipStream_t s);
 hipError_t launch_dq_reduce(const DqReduceParams &p, DType dt, int D, hipStream_t s);
-hipError_t launch_dkdv(const DkdvParams &p, DType dt, int D, int grid_x, hipStream_t s);
+hipError_t launch_dkdv(const DkdvParams &p, DType dt, int D, int n_wg, hipStream_t s);
 // bf16 fast path (8-wave workgroups; forward and dQ take 256 packed rows per workgroup).
 constexpr int kBf16RowsPerWg = 256;
 hipError_t launch_fwd_bf16(const FwdParams &p, int D, hipStream_t s);
 hipError_t launch_dq_bf16(const DqParams &p, int D, hipStream_t s);
-hipError_t launch_dkdv_bf16(const DkdvParams &p, int D, int grid_x, hipStream_t s);
+hipError_t launch_dkdv_bf16(const DkdvParams &p, int D, int n_wg, hipStream_t s);
 hipError_t launch_bwd_transpose_bf16(const PreParams &p, int D, hipStream_t s);
 
 }  // namespace cas

@@ -289,9 +289,9 @@ def test_packed_equal_lengths_plan_like_fixed(lib):
     assert lib.cas_plan_info(ctypes.byref(b.p), ctypes.byref(ib)) == _lib.CAS_OK
     for fld, _ in _lib.PlanInfo._fields_:
         assert getattr(ia, fld) == getattr(ib, fld), fld
-    # Uneven samples: grids are sized for the longest sample.
+    # Uneven samples: the dK/dV list holds each row's own self tiles.
     c = Fake(B=3, Sq=1, Hkv=2, g=4, D=128, rows=((40,), (), (7,)))
     _packed(c, (0, 300, 301, 301))
     ic = _lib.PlanInfo()
     assert lib.cas_plan_info(ctypes.byref(c.p), ctypes.byref(ic)) == _lib.CAS_OK
-    assert ic.dkdv_workgroups == (1 + 1 + 3 * 3) * 2     # 2 cartridge tiles + 3 rows x 3 self tiles
+    assert ic.dkdv_workgroups == (1 + 1 + 3 + 1 + 0) * 2   # 2 cartridge tiles + self tiles 3, 1, 0
