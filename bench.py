@@ -104,6 +104,8 @@ def main():
     ap.add_argument("--config", type=int, default=3, help="workload 1-4 (5 is forward-only)")
     ap.add_argument("--packed", action="store_true",
                     help="the 8,192-token packed training layout instead of --config")
+    ap.add_argument("--adam", action="store_true",
+                    help="time the cartridge Adam step over the packed layout's 20-cartridge pool")
     ap.add_argument("--cpu-heads", type=int, default=16, help="oracle heads timed for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "hbm_traffic_16x2k.json"),
@@ -134,6 +136,8 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "copies": 5}), flush=True)
         return
+    if args.adam:
+        return run_adam(args)
     wl = casgen.packed() if args.packed else casgen.config(args.config)
     if wl.forward_only:
         print("bench.py times forward+backward; pick config 1-4", file=sys.stderr)
@@ -245,6 +249,79 @@ def main():
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(wl, T, heads=args.cpu_heads)
+    print(json.dumps(out), flush=True)
+
+
+def run_adam(args):
+    """One fused Adam step (cas_cartridge_adam) over the K and V of the 20
+    cartridges of the packed training layout's GPU pool (8 KV heads x 128, bf16
+    parameters and gradients, fp32 moments, one frozen token each). Bound by
+    HBM: 22 bytes move per updated element (2 + 2 read, 2 written for the
+    parameter and its gradient; 8 read and 8 written for the two moments)."""
+    import numpy as np
+    import torch
+    import casgen
+    import paper_2606_04557_amd as cas
+    from casgen import rng
+    wl = casgen.packed()
+    Hkv, D = wl.num_kv_heads, wl.head_dim
+    carts = []
+    for c, L in enumerate(wl.cart_lens):
+        t = {}
+        for i, n in enumerate(("k", "v", "dk", "dv")):
+            bits = rng.f64_to_bf16_bits(rng.normal(rng.stream_key(wl.seed, 30 + i, c), L * Hkv * D,
+                                                   0.5 if len(n) == 1 else 1e-2))
+            t[n] = torch.from_numpy(bits.view(np.int16).reshape(L, Hkv, D)).view(torch.bfloat16).cuda()
+        for n in ("m1_k", "m2_k", "m1_v", "m2_v"):
+            t[n] = torch.zeros((L, Hkv, D), dtype=torch.float32, device="cuda")
+        carts.append(cas.AdamCartridge(**t, step=25, frozen_tokens=1))
+    elems = sum(2 * (L - 1) * Hkv * D for L in wl.cart_lens)
+    nbytes = 22 * elems
+    ws = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")
+    cfg = dict(lr=0.05, beta1=0.9, beta2=0.999, eps=1e-8, warmup_steps=20, warmup_buckets=4)
+    for _ in range(args.warmup):
+        cas.cartridge_adam(carts, workspace=ws, **cfg)
+    torch.cuda.synchronize()
+    cas.timing_reset()
+    cas.timing_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        cas.cartridge_adam(carts, workspace=ws, **cfg)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    cas.timing_enable(False)
+    kt = cas.timing_read()
+    n, tot = kt["adam"]
+    avg = tot / n
+    ms = (t1 - t0) * 1e3 / args.steps
+    achieved = nbytes / (avg * 1e-3) / 1e9
+    out = {
+        "metric": "cartridge Adam step, HBM GB/s (20-cartridge pool, 8 KV heads x 128)",
+        "value": nbytes / (ms * 1e-3) / 1e9, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32 (moments) / bf16 (parameters)",
+        "data": "synthetic (seeded Gaussian parameters and gradients)",
+        "config": {"workload": "Adam over the packed layout's cartridge pool", "cartridges": len(wl.cart_lens),
+                   "tokens": sum(wl.cart_lens), "updated_elements": elems, "parallelism": "single GPU"},
+        "kernels": {"adam": {"launches": n, "avg_ms": avg}},
+        "roofline": {"bound": "hbm", "kernel": "adam", "achieved": achieved, "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+                     "avg_launch_ms": avg, "bytes_per_launch": nbytes},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        h = {k: np.asarray(v.float().cpu().numpy()) for k, v in
+             (("x", carts[0].k), ("g", carts[0].dk), ("m1", carts[0].m1_k), ("m2", carts[0].m2_k))}
+        t0 = time.perf_counter()
+        reps = 0
+        while time.perf_counter() - t0 < 2.0:
+            oracle.adam.adam_step(h["x"], h["g"], h["m1"], h["m2"], 25, frozen_tokens=1, **cfg)
+            reps += 1
+        el = time.perf_counter() - t0
+        per = 22 * (h["x"].shape[0] - 1) * Hkv * D
+        out["cpu_baseline"] = {"value": reps * per / el / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+                               "sample": f"cartridge 0's K ({h['x'].shape[0]} tokens), {reps} steps in {el:.1f} s"}
     print(json.dumps(out), flush=True)
 
 

@@ -179,6 +179,75 @@ typedef struct {
 cas_status_t cas_cartridge_stage(const cas_stage_copy_t *copies, int32_t n, void *side_stream,
                                  void *done_event);
 
+/*
+ * Optimizer step of the trainable cartridges (paper: Section "Optimization
+ * Dynamics", paragraphs "Optimizer" and "Per-cartridge LR warmup"; the
+ * hyperparameter table's Adam (FP32), per-cartridge warmup W_c = 20 and one
+ * frozen token). Adam (Kingma and Ba, Algorithm 1) with fp32 moments on bf16
+ * parameters, one fused launch over every listed cartridge's K and V.
+ *
+ * For each element x of k and v (and its gradient g from dk / dv), with
+ * t = step + 1 and lr_c = lr * cas_adam_lr_scale(step, warmup_steps,
+ * warmup_buckets):
+ *   m1 = beta1 m1 + (1 - beta1) g;   m2 = beta2 m2 + (1 - beta2) g g
+ *   x  = bf16_rne(x - lr_c (m1 / (1 - beta1^t)) / (sqrt(m2 / (1 - beta2^t)) + eps))
+ * all in fp32 with one rounding per operation, in this order (1 - beta^t is
+ * evaluated in double and rounded to fp32). The first frozen_tokens tokens
+ * of each cartridge (the BOS token) are neither read nor written.
+ *
+ * k, v, dk, dv: bf16 device tensors with the strides of cas_segment_t
+ *   (element (j, h, c) at base + j*stride_tok + h*stride_head + c).
+ * m1_k, m2_k, m1_v, m2_v: fp32 device moments, contiguous
+ *   [len, num_kv_heads, head_dim], zero before a cartridge's first step.
+ * step: optimizer steps the cartridge has already received (the caller
+ *   increments it after the call; moving a cartridge out of the GPU pool and
+ *   back keeps its step count and moments).
+ * Every pointer 16-byte aligned, strides multiples of 8 elements; parameters
+ * may not overlap their gradients or moments, or another cartridge's
+ * tensors. Validation happens before anything is enqueued; on error nothing
+ * runs. The workspace holds the launch tables (size from
+ * cas_cartridge_adam_workspace_size; reusable once the stream has passed).
+ */
+typedef struct {
+  void *k;
+  void *v;
+  const void *dk;
+  const void *dv;
+  float *m1_k;
+  float *m2_k;
+  float *m1_v;
+  float *m2_v;
+  int64_t len;
+  int64_t stride_tok;
+  int64_t stride_head;
+  int32_t step;
+  int32_t frozen_tokens;
+} cas_adam_cartridge_t;
+
+typedef struct {
+  float lr;               /* eta_t of the global schedule at this step, >= 0 */
+  float beta1, beta2;     /* in [0, 1) */
+  float eps;              /* > 0 */
+  int32_t warmup_steps;   /* W_c; 0 disables the per-cartridge warmup */
+  int32_t warmup_buckets; /* N_b >= 1 */
+} cas_adam_config_t;
+
+/*
+ * Per-cartridge warmup factor (host only): min(1, step / warmup_steps)
+ * rounded up to one of warmup_buckets levels 1/N_b, 2/N_b, ..., 1 (the first
+ * level also for step 0), so at most N_b distinct learning rates occur in a
+ * step. 1 when warmup_steps <= 0; NaN for warmup_buckets < 1 or step < 0.
+ */
+float cas_adam_lr_scale(int32_t step, int32_t warmup_steps, int32_t warmup_buckets);
+
+cas_status_t cas_cartridge_adam_workspace_size(const cas_adam_cartridge_t *carts, int32_t n,
+                                               int32_t num_kv_heads, int32_t head_dim,
+                                               size_t *bytes);
+
+cas_status_t cas_cartridge_adam(const cas_adam_cartridge_t *carts, int32_t n, int32_t num_kv_heads,
+                                int32_t head_dim, const cas_adam_config_t *cfg, void *workspace,
+                                size_t ws_bytes, void *hip_stream);
+
 /* Static description of a status code. */
 const char *cas_status_string(cas_status_t s);
 /* Message of the last failed call on this thread ("" if none). */

@@ -19,3 +19,4 @@ from .attention import (  # noqa: F401
     rows_forward_backward,
     visible_mask,
 )
+from . import adam  # noqa: F401,E402

@@ -16,7 +16,8 @@ from ._lib import load  # noqa: F401
 
 __all__ = ["Segment", "Problem", "CasError", "load", "prefix_attn_fwd", "prefix_attn_bwd",
            "workspace_size", "plan_info", "set_tuning", "get_tuning", "cartridge_stage",
-           "timing_enable", "timing_reset", "timing_read"]
+           "timing_enable", "timing_reset", "timing_read", "AdamCartridge", "adam_lr_scale",
+           "cartridge_adam"]
 
 
 class CasError(RuntimeError):
@@ -202,6 +203,68 @@ def prefix_attn_bwd(q, k_self, v_self, rows: Sequence[Sequence[Segment]], num_kv
                                       _ptr(dq), _ptr(dk_self), _ptr(dv_self), ws.data_ptr(),
                                       ws.numel(), _stream_handle(q.device, stream)))
     return dq, dk_self, dv_self
+
+
+@dataclasses.dataclass
+class AdamCartridge:
+    """One cartridge for the optimizer step: bf16 k, v ([len, Hkv, d] views, any
+    token/head strides) with their gradients dk, dv (same strides), fp32
+    moments m1_k, m2_k, m1_v, m2_v (contiguous [len, Hkv, d]), the optimizer
+    steps it has received and its frozen leading tokens."""
+    k: object
+    v: object
+    dk: object
+    dv: object
+    m1_k: object
+    m2_k: object
+    m1_v: object
+    m2_v: object
+    step: int = 0
+    frozen_tokens: int = 1
+
+
+def adam_lr_scale(step: int, warmup_steps: int = 20, warmup_buckets: int = 4) -> float:
+    """The bucketed per-cartridge warmup factor (cas_adam_lr_scale)."""
+    return float(load().cas_adam_lr_scale(int(step), int(warmup_steps), int(warmup_buckets)))
+
+
+def _adam_array(carts: Sequence[AdamCartridge]):
+    arr = (_lib.AdamCartridge * max(len(carts), 1))()
+    for i, c in enumerate(carts):
+        if c.k.dim() != 3 or c.k.shape != c.v.shape or c.k.stride() != c.v.stride():
+            raise ValueError("k and v must be [len, Hkv, d] views with equal strides")
+        for t in (c.dk, c.dv):
+            if t.shape != c.k.shape or t.stride() != c.k.stride():
+                raise ValueError("dk and dv must match k's shape and strides")
+        for t in (c.m1_k, c.m2_k, c.m1_v, c.m2_v):
+            if t.shape != c.k.shape or not t.is_contiguous():
+                raise ValueError("moments must be contiguous with k's shape")
+        e = arr[i]
+        e.k, e.v, e.dk, e.dv = c.k.data_ptr(), c.v.data_ptr(), c.dk.data_ptr(), c.dv.data_ptr()
+        e.m1_k, e.m2_k, e.m1_v, e.m2_v = (c.m1_k.data_ptr(), c.m2_k.data_ptr(), c.m1_v.data_ptr(),
+                                          c.m2_v.data_ptr())
+        e.len, e.stride_tok, e.stride_head = int(c.k.shape[0]), int(c.k.stride(0)), int(c.k.stride(1))
+        e.step, e.frozen_tokens = int(c.step), int(c.frozen_tokens)
+    return arr
+
+
+def cartridge_adam(carts: Sequence[AdamCartridge], lr: float, beta1: float = 0.9, beta2: float = 0.999,
+                   eps: float = 1e-8, warmup_steps: int = 20, warmup_buckets: int = 4, stream=None,
+                   workspace=None) -> None:
+    """One fused Adam step over every cartridge's K and V (cas_cartridge_adam).
+    The caller increments each cartridge's step afterwards."""
+    if not carts:
+        return
+    arr = _adam_array(carts)
+    Hkv, D = int(carts[0].k.shape[1]), int(carts[0].k.shape[2])
+    n = ctypes.c_size_t(0)
+    P = ctypes.POINTER(_lib.AdamCartridge)
+    _check(load().cas_cartridge_adam_workspace_size(ctypes.cast(arr, P), len(carts), Hkv, D, ctypes.byref(n)))
+    dev = carts[0].k.device
+    ws = workspace if workspace is not None and workspace.numel() >= n.value else _workspace(n.value, dev)
+    cfg = _lib.AdamConfig(lr, beta1, beta2, eps, warmup_steps, warmup_buckets)
+    _check(load().cas_cartridge_adam(ctypes.cast(arr, P), len(carts), Hkv, D, ctypes.byref(cfg), ws.data_ptr(),
+                                     ws.numel(), _stream_handle(dev, stream)))
 
 
 def cartridge_stage(copies: Sequence[Tuple[object, object]], side_stream, done_event=None) -> None:

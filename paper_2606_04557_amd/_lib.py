@@ -22,7 +22,8 @@ EXPORTS = [
     "cas_prefix_attn_workspace_size", "cas_prefix_attn_fwd", "cas_prefix_attn_bwd",
     "cas_cartridge_stage", "cas_status_string", "cas_last_error_message", "cas_abi_version",
     "cas_set_tuning", "cas_get_tuning", "cas_plan_info", "cas_timing_enable",
-    "cas_timing_reset", "cas_timing_read",
+    "cas_timing_reset", "cas_timing_read", "cas_adam_lr_scale", "cas_cartridge_adam_workspace_size",
+    "cas_cartridge_adam",
 ]
 
 
@@ -38,6 +39,20 @@ class Problem(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
                 ("segments", ctypes.POINTER(Segment)), ("seg_offsets", ctypes.POINTER(ctypes.c_int32)),
                 ("q_offsets", ctypes.POINTER(ctypes.c_int32))]
+
+
+class AdamCartridge(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("dk", ctypes.c_void_p),
+                ("dv", ctypes.c_void_p), ("m1_k", ctypes.c_void_p), ("m2_k", ctypes.c_void_p),
+                ("m1_v", ctypes.c_void_p), ("m2_v", ctypes.c_void_p), ("len", ctypes.c_int64),
+                ("stride_tok", ctypes.c_int64), ("stride_head", ctypes.c_int64),
+                ("step", ctypes.c_int32), ("frozen_tokens", ctypes.c_int32)]
+
+
+class AdamConfig(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("warmup_steps", ctypes.c_int32),
+                ("warmup_buckets", ctypes.c_int32)]
 
 
 class StageCopy(ctypes.Structure):
@@ -86,6 +101,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cas_abi_version.restype = i32
     if lib.cas_abi_version() != ABI_VERSION:
         raise RuntimeError(f"libcas ABI {lib.cas_abi_version()} at {path}, this binding expects {ABI_VERSION}: rebuild")
+    lib.cas_adam_lr_scale.argtypes = [i32, i32, i32]
+    lib.cas_adam_lr_scale.restype = ctypes.c_float
+    lib.cas_cartridge_adam_workspace_size.argtypes = [P(AdamCartridge), i32, i32, i32, P(sz)]
+    lib.cas_cartridge_adam.argtypes = [P(AdamCartridge), i32, i32, i32, P(AdamConfig), vp, sz, vp]
     lib.cas_set_tuning.argtypes = [P(Tuning)]
     lib.cas_get_tuning.argtypes = [P(Tuning)]
     lib.cas_plan_info.argtypes = [P(Problem), P(PlanInfo)]
@@ -94,7 +113,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cas_timing_read.argtypes = [P(KernelTime), i32, P(i32)]
     for name in ("cas_prefix_attn_workspace_size", "cas_prefix_attn_fwd", "cas_prefix_attn_bwd",
                  "cas_cartridge_stage", "cas_set_tuning", "cas_get_tuning", "cas_plan_info",
-                 "cas_timing_enable", "cas_timing_reset", "cas_timing_read"):
+                 "cas_timing_enable", "cas_timing_reset", "cas_timing_read",
+                 "cas_cartridge_adam_workspace_size", "cas_cartridge_adam"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib

@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libcas.so")
-SOURCES = ["cas_api.cpp", "cas_fwd.hip", "cas_bwd.hip", "cas_bf16.hip"]
+SOURCES = ["cas_api.cpp", "cas_fwd.hip", "cas_bwd.hip", "cas_bf16.hip", "cas_adam.hip"]
 ARCH = "gfx950"
 
 # -packed-fp32-ops: no packed fp32 ALU instructions are generated on gfx950.
@@ -31,7 +31,10 @@ COMMON_FLAGS = [
 # The bf16 kernels produce no NaN of their own (masked scores are -inf, never
 # NaN), so max/min need not quiet signalling NaNs: without this every fmaxf
 # on an MFMA result costs an extra canonicalising instruction.
-FILE_FLAGS = {"cas_bf16.hip": ["-fno-honor-nans"]}
+#
+# The optimizer step rounds once per operation in a documented order, so no
+# multiply-add contraction there.
+FILE_FLAGS = {"cas_bf16.hip": ["-fno-honor-nans"], "cas_adam.hip": ["-ffp-contract=off"]}
 
 
 def hipcc() -> str:

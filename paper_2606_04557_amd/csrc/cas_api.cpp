@@ -483,7 +483,10 @@ struct Ring {
 std::mutex g_ring_mu;
 std::map<int, Ring> g_rings;
 
-cas_status_t upload_tables(const Plan &pl, bool bwd, void *ws, hipStream_t stream) {
+// Copies `bytes` of launch tables, written by fill() into a pinned slot,
+// to the workspace on the stream.
+template <typename Fill>
+cas_status_t ring_upload(size_t bytes, void *ws, hipStream_t stream, Fill &&fill) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
@@ -495,7 +498,7 @@ cas_status_t upload_tables(const Plan &pl, bool bwd, void *ws, hipStream_t strea
       if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipEventCreate: ") + hipGetErrorString(e));
     }
   }
-  if (!r.host || pl.table_bytes > r.slot_bytes) {
+  if (!r.host || bytes > r.slot_bytes) {
     // (Re)allocate the pinned ring once every earlier upload from it is done.
     for (int i = 0; i < kSlots; ++i) {
       if (!r.used[i]) continue;
@@ -506,7 +509,7 @@ cas_status_t upload_tables(const Plan &pl, bool bwd, void *ws, hipStream_t strea
     if (r.host) hipHostFree(r.host);
     r.host = nullptr;
     size_t sb = kMinSlotBytes;
-    while (sb < pl.table_bytes) sb *= 2;
+    while (sb < bytes) sb *= 2;
     e = hipHostMalloc((void **)&r.host, sb * kSlots, hipHostMallocDefault);
     if (e != hipSuccess) {
       r.host = nullptr;
@@ -522,20 +525,125 @@ cas_status_t upload_tables(const Plan &pl, bool bwd, void *ws, hipStream_t strea
     if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipEventSynchronize: ") + hipGetErrorString(e));
   }
   char *h = r.host + (size_t)slot * r.slot_bytes;
-  std::memset(h, 0, pl.table_bytes);
-  if (!pl.segs.empty()) std::memcpy(h + pl.off_segs, pl.segs.data(), pl.segs.size() * sizeof(DevSeg));
-  std::memcpy(h + pl.off_rows, pl.rows.data(), pl.rows.size() * sizeof(DevRow));
-  if (!pl.tiles.empty()) std::memcpy(h + pl.off_tiles, pl.tiles.data(), pl.tiles.size() * sizeof(DevTile));
-  if (bwd) {
-    if (!pl.carts.empty()) std::memcpy(h + pl.off_carts, pl.carts.data(), pl.carts.size() * sizeof(DevCart));
-    if (!pl.uses.empty()) std::memcpy(h + pl.off_uses, pl.uses.data(), pl.uses.size() * sizeof(int32_t));
-    if (!pl.order.empty()) std::memcpy(h + pl.off_order, pl.order.data(), pl.order.size() * sizeof(DevWg));
-  }
-  e = hipMemcpyAsync(ws, h, pl.table_bytes, hipMemcpyHostToDevice, stream);
+  std::memset(h, 0, bytes);
+  fill(h);
+  e = hipMemcpyAsync(ws, h, bytes, hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipMemcpyAsync: ") + hipGetErrorString(e));
   e = hipEventRecord(r.ev[slot], stream);
   if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipEventRecord: ") + hipGetErrorString(e));
   r.used[slot] = true;
+  return CAS_OK;
+}
+
+cas_status_t upload_tables(const Plan &pl, bool bwd, void *ws, hipStream_t stream) {
+  return ring_upload(pl.table_bytes, ws, stream, [&](char *h) {
+    if (!pl.segs.empty()) std::memcpy(h + pl.off_segs, pl.segs.data(), pl.segs.size() * sizeof(DevSeg));
+    std::memcpy(h + pl.off_rows, pl.rows.data(), pl.rows.size() * sizeof(DevRow));
+    if (!pl.tiles.empty()) std::memcpy(h + pl.off_tiles, pl.tiles.data(), pl.tiles.size() * sizeof(DevTile));
+    if (bwd) {
+      if (!pl.carts.empty()) std::memcpy(h + pl.off_carts, pl.carts.data(), pl.carts.size() * sizeof(DevCart));
+      if (!pl.uses.empty()) std::memcpy(h + pl.off_uses, pl.uses.data(), pl.uses.size() * sizeof(int32_t));
+      if (!pl.order.empty()) std::memcpy(h + pl.off_order, pl.order.data(), pl.order.size() * sizeof(DevWg));
+    }
+  });
+}
+
+// ---------------------------------------------------------------------------
+// Cartridge Adam step: validation and launch tables.
+// ---------------------------------------------------------------------------
+struct AdamPlan {
+  std::vector<DevAdamT> tensors;
+  std::vector<DevAdamChunk> chunks;
+  size_t off_chunks = 0, bytes = 0;
+};
+
+float lr_scale(int32_t step, int32_t warmup, int32_t buckets) {
+  if (buckets < 1 || step < 0) return NAN;
+  if (warmup <= 0 || step >= warmup) return 1.0f;
+  // ceil(buckets * step / warmup), at least the first level
+  const int64_t lvl = std::max<int64_t>(1, ((int64_t)buckets * step + warmup - 1) / warmup);
+  return (float)std::min<int64_t>(lvl, buckets) / (float)buckets;
+}
+
+cas_status_t build_adam(const cas_adam_cartridge_t *carts, int32_t n, int32_t Hkv, int32_t D,
+                        const cas_adam_config_t *cfg, AdamPlan &ap) {
+  if (n < 0) return fail(CAS_ERR_INVALID_ARGUMENT, "n must be >= 0");
+  if (n > 0 && !carts) return fail(CAS_ERR_INVALID_ARGUMENT, "carts is NULL");
+  if (Hkv < 1) return fail(CAS_ERR_INVALID_ARGUMENT, "num_kv_heads must be >= 1");
+  if (D != 64 && D != 128) return fail(CAS_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (cfg) {
+    if (!std::isfinite(cfg->lr) || cfg->lr < 0.0f) return fail(CAS_ERR_INVALID_ARGUMENT, "lr must be finite and >= 0");
+    if (!(cfg->beta1 >= 0.0f && cfg->beta1 < 1.0f) || !(cfg->beta2 >= 0.0f && cfg->beta2 < 1.0f))
+      return fail(CAS_ERR_INVALID_ARGUMENT, "beta1 and beta2 must lie in [0, 1)");
+    if (!std::isfinite(cfg->eps) || !(cfg->eps > 0.0f)) return fail(CAS_ERR_INVALID_ARGUMENT, "eps must be finite and > 0");
+    if (cfg->warmup_buckets < 1 || cfg->warmup_steps < 0)
+      return fail(CAS_ERR_INVALID_ARGUMENT, "warmup_buckets must be >= 1 and warmup_steps >= 0");
+  }
+  std::vector<Interval> iv;
+  for (int i = 0; i < n; ++i) {
+    const cas_adam_cartridge_t &c = carts[i];
+    const std::string who = "cartridge " + std::to_string(i);
+    if (c.len < 0 || c.step < 0 || c.frozen_tokens < 0)
+      return fail(CAS_ERR_INVALID_ARGUMENT, who + ": len, step and frozen_tokens must be >= 0");
+    if (c.len > (1 << 30)) return fail(CAS_ERR_UNSUPPORTED, who + ": longer than 2^30 tokens");
+    if (c.len <= c.frozen_tokens) continue;   // nothing to update
+    const void *ptrs[8] = {c.k, c.v, c.dk, c.dv, c.m1_k, c.m2_k, c.m1_v, c.m2_v};
+    for (const void *q : ptrs)
+      if (!q) return fail(CAS_ERR_INVALID_ARGUMENT, who + ": NULL tensor");
+    for (const void *q : ptrs)
+      if (!aligned16(q)) return fail(CAS_ERR_ALIGNMENT, who + ": tensors must be 16-byte aligned");
+    if (c.stride_tok < 1 || c.stride_head < 0 || (Hkv > 1 && c.stride_head < 1))
+      return fail(CAS_ERR_INVALID_ARGUMENT, who + ": bad strides");
+    if (c.stride_tok % 8 != 0 || c.stride_head % 8 != 0)
+      return fail(CAS_ERR_ALIGNMENT, who + ": strides must be multiples of 8 elements");
+    int64_t s1 = c.stride_tok, n1 = c.len, s2 = c.stride_head, n2 = Hkv;
+    if (s1 > s2 || n1 == 1) {
+      std::swap(s1, s2);
+      std::swap(n1, n2);
+    }
+    if ((n1 > 1 && s1 < D) || (n2 > 1 && (s2 < D || (n1 > 1 && s2 < s1 * n1))))
+      return fail(CAS_ERR_INVALID_ARGUMENT, who + ": parameter layout overlaps itself");
+    const uintptr_t span = (uintptr_t)(((c.len - 1) * c.stride_tok + (int64_t)(Hkv - 1) * c.stride_head + D) * 2);
+    const uintptr_t mom = (uintptr_t)c.len * Hkv * D * 4;
+    // Every written tensor is its own owner: no two may overlap, even at equal addresses.
+    const uintptr_t own = (uintptr_t)i * 8 + 1;
+    iv.push_back({(uintptr_t)c.k, (uintptr_t)c.k + span, true, own, "k"});
+    iv.push_back({(uintptr_t)c.v, (uintptr_t)c.v + span, true, own + 1, "v"});
+    iv.push_back({(uintptr_t)c.dk, (uintptr_t)c.dk + span, false, 0, "dk"});
+    iv.push_back({(uintptr_t)c.dv, (uintptr_t)c.dv + span, false, 0, "dv"});
+    int j = 2;
+    for (float *m : {c.m1_k, c.m2_k, c.m1_v, c.m2_v})
+      iv.push_back({(uintptr_t)m, (uintptr_t)m + mom, true, own + j++, "moment"});
+  }
+  std::string msg;
+  if (!overlap_free(iv, msg)) return fail(CAS_ERR_INVALID_ARGUMENT, msg);
+  for (int i = 0; i < n; ++i) {
+    const cas_adam_cartridge_t &c = carts[i];
+    if (c.len <= c.frozen_tokens) continue;
+    const double t = (double)c.step + 1.0;
+    for (int which = 0; which < 2; ++which) {
+      DevAdamT d{};
+      d.x = (__bf16 *)(which ? c.v : c.k);
+      d.g = (const __bf16 *)(which ? c.dv : c.dk);
+      d.m1 = which ? c.m1_v : c.m1_k;
+      d.m2 = which ? c.m2_v : c.m2_k;
+      d.stride_tok = c.stride_tok;
+      d.stride_head = c.stride_head;
+      d.len = (int32_t)c.len;
+      d.frozen = c.frozen_tokens;
+      if (cfg) {
+        d.lr = cfg->lr * lr_scale(c.step, cfg->warmup_steps, cfg->warmup_buckets);
+        d.bc1 = (float)(1.0 - std::pow((double)cfg->beta1, t));
+        d.bc2 = (float)(1.0 - std::pow((double)cfg->beta2, t));
+      }
+      const int32_t ti = (int32_t)ap.tensors.size();
+      ap.tensors.push_back(d);
+      for (int64_t tok = c.frozen_tokens; tok < c.len; tok += kAdamChunk) ap.chunks.push_back({ti, (int32_t)tok});
+    }
+    if (ap.chunks.size() > (size_t)INT32_MAX) return fail(CAS_ERR_UNSUPPORTED, "too many chunks");
+  }
+  ap.off_chunks = align_up(ap.tensors.size() * sizeof(DevAdamT), 256);
+  ap.bytes = align_up(ap.off_chunks + ap.chunks.size() * sizeof(DevAdamChunk), 256);
   return CAS_OK;
 }
 
@@ -623,6 +731,50 @@ const char *cas_status_string(cas_status_t s) {
 }
 
 const char *cas_last_error_message(void) { return g_err.c_str(); }
+
+float cas_adam_lr_scale(int32_t step, int32_t warmup_steps, int32_t warmup_buckets) {
+  return lr_scale(step, warmup_steps, warmup_buckets);
+}
+
+cas_status_t cas_cartridge_adam_workspace_size(const cas_adam_cartridge_t *carts, int32_t n,
+                                               int32_t num_kv_heads, int32_t head_dim, size_t *bytes) {
+  if (!bytes) return fail(CAS_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  AdamPlan ap;
+  cas_status_t s = build_adam(carts, n, num_kv_heads, head_dim, nullptr, ap);
+  if (s != CAS_OK) return s;
+  *bytes = ap.bytes;
+  return CAS_OK;
+}
+
+cas_status_t cas_cartridge_adam(const cas_adam_cartridge_t *carts, int32_t n, int32_t num_kv_heads,
+                                int32_t head_dim, const cas_adam_config_t *cfg, void *workspace,
+                                size_t ws_bytes, void *hip_stream) {
+  if (!cfg) return fail(CAS_ERR_INVALID_ARGUMENT, "cfg is NULL");
+  AdamPlan ap;
+  cas_status_t s = build_adam(carts, n, num_kv_heads, head_dim, cfg, ap);
+  if (s != CAS_OK) return s;
+  if (ap.chunks.empty()) return CAS_OK;
+  s = check_workspace(workspace, ws_bytes, ap.bytes);
+  if (s != CAS_OK) return s;
+  hipStream_t stream = (hipStream_t)hip_stream;
+  s = ring_upload(ap.bytes, workspace, stream, [&](char *h) {
+    std::memcpy(h, ap.tensors.data(), ap.tensors.size() * sizeof(DevAdamT));
+    std::memcpy(h + ap.off_chunks, ap.chunks.data(), ap.chunks.size() * sizeof(DevAdamChunk));
+  });
+  if (s != CAS_OK) return s;
+  AdamParams p{};
+  p.tensors = (const DevAdamT *)workspace;
+  p.chunks = (const DevAdamChunk *)((char *)workspace + ap.off_chunks);
+  p.Hkv = num_kv_heads;
+  p.beta1 = cfg->beta1;
+  p.beta2 = cfg->beta2;
+  p.omb1 = 1.0f - cfg->beta1;
+  p.omb2 = 1.0f - cfg->beta2;
+  p.eps = cfg->eps;
+  hipError_t e = timed("adam", stream, [&] { return launch_adam_bf16(p, head_dim, (int)ap.chunks.size(), stream); });
+  if (e != hipSuccess) return hip_fail("adam launch", e);
+  return CAS_OK;
+}
 
 cas_status_t cas_set_tuning(const cas_tuning_t *t) {
   if (!t) return fail(CAS_ERR_INVALID_ARGUMENT, "tuning is NULL");

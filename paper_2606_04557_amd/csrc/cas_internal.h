@@ -177,6 +177,36 @@ struct DkdvParams {
   float scale;
 };
 
+// Cartridge Adam step: one trainable tensor (a cartridge's K or V).
+struct DevAdamT {
+  __bf16 *x;             // parameters (strided like the segment)
+  const __bf16 *g;       // gradient, same strides
+  float *m1;             // moments, contiguous [len][Hkv][d]
+  float *m2;
+  int64_t stride_tok;
+  int64_t stride_head;
+  int32_t len;
+  int32_t frozen;        // leading tokens left untouched
+  float lr;              // lr * warmup factor
+  float bc1, bc2;        // 1 - beta^t, rounded to fp32
+  int32_t pad_[3];
+};
+
+// One workgroup's share: kAdamChunk tokens of tensor `t` from token `tok0`.
+struct DevAdamChunk {
+  int32_t t;
+  int32_t tok0;
+};
+constexpr int kAdamChunk = 16;
+
+struct AdamParams {
+  const DevAdamT *tensors;
+  const DevAdamChunk *chunks;
+  int32_t Hkv;
+  float beta1, beta2, omb1, omb2;   // omb = 1 - beta (fp32)
+  float eps;
+};
+
 // Kernel launchers (defined in the .hip files).
 hipError_t launch_fwd(const FwdParams &p, DType dt, int D, hipStream_t s);
 hipError_t launch_fwd_merge(const MergeParams &p, DType dt, int D, hipStream_t s);
@@ -190,5 +220,6 @@ hipError_t launch_fwd_bf16(const FwdParams &p, int D, hipStream_t s);
 hipError_t launch_dq_bf16(const DqParams &p, int D, hipStream_t s);
 hipError_t launch_dkdv_bf16(const DkdvParams &p, int D, int n_wg, hipStream_t s);
 hipError_t launch_bwd_transpose_bf16(const PreParams &p, int D, hipStream_t s);
+hipError_t launch_adam_bf16(const AdamParams &p, int D, int n_chunks, hipStream_t s);
 
 }  // namespace cas

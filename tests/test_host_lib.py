@@ -295,3 +295,44 @@ def test_packed_equal_lengths_plan_like_fixed(lib):
     ic = _lib.PlanInfo()
     assert lib.cas_plan_info(ctypes.byref(c.p), ctypes.byref(ic)) == _lib.CAS_OK
     assert ic.dkdv_workgroups == (1 + 1 + 3 + 1 + 0) * 2   # 2 cartridge tiles + self tiles 3, 1, 0
+
+
+def _adam_cart(f, L=40, Hkv=2, D=64, step=0, frozen=1, stride_tok=None):
+    c = _lib.AdamCartridge()
+    st = stride_tok or Hkv * D
+    nb = L * st * 2 + 4096
+    c.k, c.v, c.dk, c.dv = f.alloc(nb), f.alloc(nb), f.alloc(nb), f.alloc(nb)
+    mb = L * Hkv * D * 4
+    c.m1_k, c.m2_k, c.m1_v, c.m2_v = f.alloc(mb), f.alloc(mb), f.alloc(mb), f.alloc(mb)
+    c.len, c.stride_tok, c.stride_head, c.step, c.frozen_tokens = L, st, D, step, frozen
+    return c
+
+
+def test_adam_validation(lib):
+    f = Fake()
+    arr = (_lib.AdamCartridge * 3)(_adam_cart(f), _adam_cart(f, L=1), _adam_cart(f, L=17, frozen=0))
+    P = ctypes.cast(arr, ctypes.POINTER(_lib.AdamCartridge))
+    n = ctypes.c_size_t(0)
+    assert lib.cas_cartridge_adam_workspace_size(P, 3, 2, 64, ctypes.byref(n)) == _lib.CAS_OK, _msg(lib)
+    # 4 tensor records (80 bytes each, padded to 512), then 2 x ceil(39/16) + 0 (only the
+    # frozen token) + 2 x ceil(17/16) = 10 chunk records of 8 bytes (padded to 256)
+    assert n.value == 512 + 256
+    cfg = _lib.AdamConfig(0.05, 0.9, 0.999, 1e-8, 20, 4)
+    for bad in (dict(lr=-1.0), dict(beta1=1.0), dict(eps=0.0), dict(warmup_buckets=0), dict(lr=float("nan"))):
+        c2 = _lib.AdamConfig(0.05, 0.9, 0.999, 1e-8, 20, 4)
+        for k, v in bad.items():
+            setattr(c2, k, v)
+        assert lib.cas_cartridge_adam(P, 3, 2, 64, ctypes.byref(c2), f.ws, 1 << 20, None) == \
+            _lib.CAS_ERR_INVALID_ARGUMENT, bad
+    assert lib.cas_cartridge_adam(P, 3, 2, 96, ctypes.byref(cfg), f.ws, 1 << 20, None) == _lib.CAS_ERR_UNSUPPORTED
+    arr[0].m2_k = arr[0].m1_k                                  # moments share a buffer
+    assert lib.cas_cartridge_adam_workspace_size(P, 3, 2, 64, ctypes.byref(n)) == _lib.CAS_ERR_INVALID_ARGUMENT
+    arr[0].m2_k = arr[2].k                                     # a moment over another cartridge's k
+    assert lib.cas_cartridge_adam_workspace_size(P, 3, 2, 64, ctypes.byref(n)) == _lib.CAS_ERR_INVALID_ARGUMENT
+    arr[0] = _adam_cart(f, stride_tok=2 * 64 + 4)              # stride not a multiple of 8 elements
+    assert lib.cas_cartridge_adam_workspace_size(P, 3, 2, 64, ctypes.byref(n)) == _lib.CAS_ERR_ALIGNMENT
+    arr[0] = _adam_cart(f, stride_tok=32)                      # tokens overlap each other
+    assert lib.cas_cartridge_adam_workspace_size(P, 3, 2, 64, ctypes.byref(n)) == _lib.CAS_ERR_INVALID_ARGUMENT
+    arr[0] = _adam_cart(f, step=-1)
+    assert lib.cas_cartridge_adam_workspace_size(P, 3, 2, 64, ctypes.byref(n)) == _lib.CAS_ERR_INVALID_ARGUMENT
+    assert lib.cas_cartridge_adam_workspace_size(P, 0, 2, 64, ctypes.byref(n)) == _lib.CAS_OK and n.value == 0
