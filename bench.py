@@ -106,6 +106,8 @@ def main():
                     help="the 8,192-token packed training layout instead of --config")
     ap.add_argument("--adam", action="store_true",
                     help="time the cartridge Adam step over the packed layout's 20-cartridge pool")
+    ap.add_argument("--decode", action="store_true",
+                    help="time one paged decode step of the retrieval mix (64 requests x 4 cartridges)")
     ap.add_argument("--cpu-heads", type=int, default=16, help="oracle heads timed for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "hbm_traffic_16x2k.json"),
@@ -138,6 +140,8 @@ def main():
         return
     if args.adam:
         return run_adam(args)
+    if args.decode:
+        return run_decode(args)
     wl = casgen.packed() if args.packed else casgen.config(args.config)
     if wl.forward_only:
         print("bench.py times forward+backward; pick config 1-4", file=sys.stderr)
@@ -322,6 +326,105 @@ def run_adam(args):
         per = 22 * (h["x"].shape[0] - 1) * Hkv * D
         out["cpu_baseline"] = {"value": reps * per / el / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
                                "sample": f"cartridge 0's K ({h['x'].shape[0]} tokens), {reps} steps in {el:.1f} s"}
+    print(json.dumps(out), flush=True)
+
+
+def run_decode(args):
+    """One decode step (cas_paged_decode_fwd) of the retrieval-selected mix: a
+    pool of 256 cartridges of 1,024 tokens in 16-token pages (8 KV heads x 128,
+    bf16); 64 requests, each over its 4 retrieved cartridges (the same seeded
+    selection as the forward-only retrieval configuration) and its own 64-token
+    prompt, generating one token (4,161 keys each). HBM-bound: the algorithmic
+    bytes are every request's K and V (counted per request)."""
+    import numpy as np
+    import torch
+    import paper_2606_04557_amd as cas
+    from casgen import rng
+    P, Hkv, g, D, pool, cart_len, own = 16, 8, 4, 128, 256, 1024, 65
+    cp = cart_len // P
+    sel = [rng.choose_distinct(rng.stream_key(5, rng.TAG_SELECT, r), pool, 4) for r in range(64)]
+    own_pages = -(-own // P)
+    npages = pool * cp + 64 * own_pages
+    shape = (npages, P, Hkv, D)
+    n_el = int(np.prod(shape))
+    kp = torch.from_numpy(rng.f64_to_bf16_bits(rng.normal(rng.stream_key(5, 40), n_el, 0.5)).view(np.int16)
+                          .reshape(shape)).view(torch.bfloat16).cuda()
+    vp = torch.from_numpy(rng.f64_to_bf16_bits(rng.normal(rng.stream_key(5, 41), n_el, 0.5)).view(np.int16)
+                          .reshape(shape)).view(torch.bfloat16).cuda()
+    pages, kv_lens = [], []
+    nxt = pool * cp
+    for s_ in sel:
+        pl = [c * cp + j for c in s_ for j in range(cp)] + list(range(nxt, nxt + own_pages))
+        nxt += own_pages
+        pages.append(pl)
+        kv_lens.append(4 * cart_len + own)
+    q_counts = [1] * 64
+    Hq = Hkv * g
+    q = torch.from_numpy(rng.f64_to_bf16_bits(rng.normal(rng.stream_key(5, 42), 64 * Hq * D, 1.0)).view(np.int16)
+                         .reshape(64, Hq, D)).view(torch.bfloat16).cuda()
+    scale = float(np.float32(1.0 / np.sqrt(D)))
+    o = torch.empty_like(q)
+    lse = torch.empty((Hq, 64), dtype=torch.float32, device="cuda")
+    prob = cas.DecodeProblem(q_counts, kv_lens, pages, npages, P, Hkv, g, D, scale)
+    import ctypes
+    n = ctypes.c_size_t(0)
+    cas._check(cas.load().cas_paged_decode_workspace_size(ctypes.byref(prob.c), ctypes.byref(n)))
+    ws = torch.empty(max(n.value, 1), dtype=torch.uint8, device="cuda")
+
+    def step():
+        cas.paged_decode_fwd(q, kp, vp, q_counts, kv_lens, pages, Hkv, g, scale, o=o, lse=lse, workspace=ws,
+                             problem=prob)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    cas.timing_reset()
+    cas.timing_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    cas.timing_enable(False)
+    kt = cas.timing_read()
+    ms = (t1 - t0) * 1e3 / args.steps
+    kv_bytes = sum(kv_lens) * Hkv * D * 2 * 2
+    dn, dtot = kt["decode"]
+    avg = dtot / dn
+    gpu_ms = avg + (kt["decode_merge"][1] / kt["decode_merge"][0] if "decode_merge" in kt else 0.0)
+    achieved = kv_bytes / (avg * 1e-3) / 1e9
+    out = {
+        "metric": "paged decode step over retrieved cartridges, HBM GB/s of K/V (64 requests x 4 x 1K-token cartridges)",
+        "value": kv_bytes / (ms * 1e-3) / 1e9, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded Gaussian pages and queries; seeded retrieval selection)",
+        "config": {"workload": "Cartridge-RAG decode: 64 requests, 4 of 256 cartridges of 1,024 tokens + "
+                               "64-token prompt, 1 new token each", "page_size": P, "kv_len": kv_lens[0],
+                   "num_q_heads": Hq, "num_kv_heads": Hkv, "head_dim": D, "parallelism": "single GPU"},
+        "tokens_per_s": 64 / (ms * 1e-3),
+        "gpu_ms": gpu_ms,
+        "kernels": {k: {"launches": c, "avg_ms": t / c} for k, (c, t) in kt.items()},
+        "roofline": {"bound": "hbm", "kernel": "decode", "achieved": achieved, "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": None, "avg_launch_ms": avg,
+                     "bytes_per_launch": kv_bytes},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        # The first 8 requests, over a compact copy of just their pages.
+        used = sorted({pg for pl in pages[:8] for pg in pl})
+        remap = {pg: i for i, pg in enumerate(used)}
+        idx = torch.tensor(used, device="cuda")
+        kpn = kp.index_select(0, idx).float().cpu().numpy()
+        vpn = vp.index_select(0, idx).float().cpu().numpy()
+        qh = q[:8].float().cpu().numpy()
+        t0 = time.perf_counter()
+        oracle.paged_decode_forward(qh, kpn, vpn, q_counts[:8], kv_lens[:8],
+                                    [[remap[pg] for pg in pl] for pl in pages[:8]], scale, g)
+        el = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": sum(kv_lens[:8]) * Hkv * D * 4 / el / 1e9, "unit": "GB/s", "cores": 1,
+                               "kind": "oracle", "sample": f"8 of the 64 requests, {el:.1f} s"}
     print(json.dumps(out), flush=True)
 
 

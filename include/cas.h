@@ -248,6 +248,50 @@ cas_status_t cas_cartridge_adam(const cas_adam_cartridge_t *carts, int32_t n, in
                                 int32_t head_dim, const cas_adam_config_t *cfg, void *workspace,
                                 size_t ws_bytes, void *hip_stream);
 
+/*
+ * Short-query / decode attention over paged cartridges (paper: Section
+ * "Inference" and paragraph "Cartridge RAG": the top-k retrieved cartridges'
+ * KV caches are concatenated ahead of the prompt; appendix on cartridge
+ * sizes: cartridges are whole 16-token pages of the serving engine's paged
+ * KV cache). Forward only.
+ *
+ * K and V live in a page pool: k_pages, v_pages are bf16 device tensors
+ * [num_pages, page_size, num_kv_heads, head_dim], contiguous. Request b owns
+ * kv_lens[b] keys, stored in the pages page_ids[page_offsets[b] ..
+ * page_offsets[b+1]) in key order (ceil(kv_lens[b] / page_size) pages; the
+ * last may be partly filled): typically the pages of its selected cartridges
+ * (shared with other requests, never copied) followed by the pages of its
+ * own prompt and generated tokens. Its n_b = q_offsets[b+1] - q_offsets[b]
+ * queries (1 <= n_b <= kv_lens[b]; n_b = 1 for a decode step) are the last
+ * n_b positions of that key sequence: query i sees keys 0 .. kv_lens[b] -
+ * n_b + i (causal among the new tokens). q and o are [Tq, Hq, head_dim]
+ * (Tq = q_offsets[batch]), lse is [Hq, Tq] fp32 (may be NULL); query head h
+ * reads kv head h / group_size. page_size is 16, 32, 64 or 128; head_dim 64
+ * or 128; page ids lie in [0, num_pages). The key axis of each request is
+ * split over several workgroups when the requests alone would not fill the
+ * GPU (partials merged by their LSE). Validation before anything is
+ * enqueued; on error nothing runs and the outputs are untouched.
+ */
+typedef struct {
+  int32_t batch;
+  int32_t num_kv_heads;
+  int32_t group_size;
+  int32_t head_dim;
+  float softmax_scale;
+  int32_t page_size;
+  int64_t num_pages;
+  const int32_t *q_offsets;    /* host, batch+1 */
+  const int32_t *kv_lens;      /* host, batch */
+  const int32_t *page_offsets; /* host, batch+1 */
+  const int32_t *page_ids;     /* host, page_offsets[batch] entries */
+} cas_decode_problem_t;
+
+cas_status_t cas_paged_decode_workspace_size(const cas_decode_problem_t *p, size_t *bytes);
+
+cas_status_t cas_paged_decode_fwd(const cas_decode_problem_t *p, const void *q, const void *k_pages,
+                                  const void *v_pages, void *o, float *lse, void *workspace,
+                                  size_t ws_bytes, void *hip_stream);
+
 /* Static description of a status code. */
 const char *cas_status_string(cas_status_t s);
 /* Message of the last failed call on this thread ("" if none). */

@@ -15,6 +15,8 @@ from .attention import (  # noqa: F401
     packed_forward,
     packed_key_grads_many,
     packed_rows_forward_backward,
+    paged_decode_forward,
+    paged_keys,
     row_keys,
     rows_forward_backward,
     visible_mask,

@@ -377,3 +377,39 @@ def packed_key_grads_many(q, k_self, v_self, cart_k, cart_v, rows, q_offsets, sc
             out[i][0][:] += dk
             out[i][1][:] += dv
     return out
+
+
+# ---------------------------------------------------------------------------
+# Short-query / decode attention over paged cartridges (paper: Section
+# "Inference", paragraph "Cartridge RAG", appendix on cartridge sizes: the
+# retrieved cartridges' KV caches, kept in 16-token pages, precede the
+# prompt). Request b's keys are its pages in order, cut to kv_lens[b]; its
+# n_b queries are the last n_b positions: query i sees keys 0 .. L - n + i.
+# ---------------------------------------------------------------------------
+
+def paged_keys(k_pages, v_pages, pages: Sequence[int], kv_len: int):
+    """Keys and values [kv_len, Hkv, D] of one request, gathered from its pages."""
+    K = np.concatenate([_f64(k_pages[p]) for p in pages], axis=0)[:kv_len]
+    V = np.concatenate([_f64(v_pages[p]) for p in pages], axis=0)[:kv_len]
+    return K, V
+
+
+def paged_decode_forward(q, k_pages, v_pages, q_counts: Sequence[int], kv_lens: Sequence[int],
+                         page_lists: Sequence[Sequence[int]], scale: float, group_size: int):
+    """O [Tq, Hq, D] and LSE [Hq, Tq] (q packed by request, [Tq, Hq, D])."""
+    q = _f64(q)
+    Tq, Hq, Dh = q.shape
+    O = np.zeros((Tq, Hq, Dh))
+    LSE = np.zeros((Hq, Tq))
+    q0 = 0
+    for b, n in enumerate(q_counts):
+        L = int(kv_lens[b])
+        K, V = paged_keys(k_pages, v_pages, page_lists[b], L)
+        for h in range(Hq):
+            kv = h // group_size
+            o, lse, _ = head_forward(q[q0:q0 + n, h, :], K[:, kv, :], V[:, kv, :], L - n, n,
+                                     np.arange(n), scale)
+            O[q0:q0 + n, h, :] = o
+            LSE[h, q0:q0 + n] = lse
+        q0 += n
+    return O, LSE

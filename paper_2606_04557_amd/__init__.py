@@ -17,7 +17,7 @@ from ._lib import load  # noqa: F401
 __all__ = ["Segment", "Problem", "CasError", "load", "prefix_attn_fwd", "prefix_attn_bwd",
            "workspace_size", "plan_info", "set_tuning", "get_tuning", "cartridge_stage",
            "timing_enable", "timing_reset", "timing_read", "AdamCartridge", "adam_lr_scale",
-           "cartridge_adam"]
+           "cartridge_adam", "DecodeProblem", "paged_decode_fwd"]
 
 
 class CasError(RuntimeError):
@@ -265,6 +265,60 @@ def cartridge_adam(carts: Sequence[AdamCartridge], lr: float, beta1: float = 0.9
     cfg = _lib.AdamConfig(lr, beta1, beta2, eps, warmup_steps, warmup_buckets)
     _check(load().cas_cartridge_adam(ctypes.cast(arr, P), len(carts), Hkv, D, ctypes.byref(cfg), ws.data_ptr(),
                                      ws.numel(), _stream_handle(dev, stream)))
+
+
+class DecodeProblem:
+    """Host tables of a paged decode call (cas_decode_problem_t): per request its
+    query count, key count and page list (pages of [page_size, Hkv, d])."""
+
+    def __init__(self, q_counts: Sequence[int], kv_lens: Sequence[int], page_lists: Sequence[Sequence[int]],
+                 num_pages: int, page_size: int, num_kv_heads: int, group_size: int, head_dim: int,
+                 softmax_scale: float):
+        B = len(q_counts)
+        if len(kv_lens) != B or len(page_lists) != B:
+            raise ValueError("one query count, kv_len and page list per request")
+        qo = [0]
+        for n in q_counts:
+            qo.append(qo[-1] + int(n))
+        po = [0]
+        for pl in page_lists:
+            po.append(po[-1] + len(pl))
+        ids = [int(x) for pl in page_lists for x in pl]
+        self.Tq = qo[-1]
+        self._qo = (ctypes.c_int32 * (B + 1))(*qo)
+        self._kv = (ctypes.c_int32 * max(B, 1))(*[int(x) for x in kv_lens])
+        self._po = (ctypes.c_int32 * (B + 1))(*po)
+        self._ids = (ctypes.c_int32 * max(len(ids), 1))(*ids)
+        I = ctypes.POINTER(ctypes.c_int32)
+        self.c = _lib.DecodeProblem(B, num_kv_heads, group_size, head_dim, float(softmax_scale), page_size,
+                                    int(num_pages), ctypes.cast(self._qo, I), ctypes.cast(self._kv, I),
+                                    ctypes.cast(self._po, I), ctypes.cast(self._ids, I))
+
+
+def paged_decode_fwd(q, k_pages, v_pages, q_counts: Sequence[int], kv_lens: Sequence[int],
+                     page_lists: Sequence[Sequence[int]], num_kv_heads: int, group_size: int,
+                     softmax_scale: float, o=None, lse=None, need_lse: bool = True, stream=None,
+                     workspace=None, problem: Optional[DecodeProblem] = None):
+    """Attention of each request's last q_counts[b] positions (q: [Tq, Hq, d]
+    packed by request) over its kv_lens[b] keys held in the pages page_lists[b]
+    of the pools k_pages, v_pages ([num_pages, page_size, Hkv, d] bf16).
+    Returns O [Tq, Hq, d] and LSE [Hq, Tq] (fp32). A DecodeProblem built once
+    from the same tables may be passed as ``problem`` to skip rebuilding them."""
+    import torch
+    num_pages, page_size, Hkv, D = k_pages.shape
+    prob = problem if problem is not None else DecodeProblem(q_counts, kv_lens, page_lists, num_pages, page_size,
+                                                             Hkv, group_size, D, softmax_scale)
+    if o is None:
+        o = torch.empty_like(q)
+    if lse is None and need_lse:
+        lse = torch.empty((q.shape[1], q.shape[0]), dtype=torch.float32, device=q.device)
+    n = ctypes.c_size_t(0)
+    _check(load().cas_paged_decode_workspace_size(ctypes.byref(prob.c), ctypes.byref(n)))
+    ws = workspace if workspace is not None and workspace.numel() >= n.value else _workspace(n.value, q.device)
+    _check(load().cas_paged_decode_fwd(ctypes.byref(prob.c), q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(),
+                                       o.data_ptr(), _ptr(lse), ws.data_ptr(), ws.numel(),
+                                       _stream_handle(q.device, stream)))
+    return o, lse
 
 
 def cartridge_stage(copies: Sequence[Tuple[object, object]], side_stream, done_event=None) -> None:

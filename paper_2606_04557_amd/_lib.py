@@ -23,7 +23,7 @@ EXPORTS = [
     "cas_cartridge_stage", "cas_status_string", "cas_last_error_message", "cas_abi_version",
     "cas_set_tuning", "cas_get_tuning", "cas_plan_info", "cas_timing_enable",
     "cas_timing_reset", "cas_timing_read", "cas_adam_lr_scale", "cas_cartridge_adam_workspace_size",
-    "cas_cartridge_adam",
+    "cas_cartridge_adam", "cas_paged_decode_workspace_size", "cas_paged_decode_fwd",
 ]
 
 
@@ -53,6 +53,14 @@ class AdamConfig(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
                 ("eps", ctypes.c_float), ("warmup_steps", ctypes.c_int32),
                 ("warmup_buckets", ctypes.c_int32)]
+
+
+class DecodeProblem(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("group_size", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("softmax_scale", ctypes.c_float), ("page_size", ctypes.c_int32),
+                ("num_pages", ctypes.c_int64), ("q_offsets", ctypes.POINTER(ctypes.c_int32)),
+                ("kv_lens", ctypes.POINTER(ctypes.c_int32)), ("page_offsets", ctypes.POINTER(ctypes.c_int32)),
+                ("page_ids", ctypes.POINTER(ctypes.c_int32))]
 
 
 class StageCopy(ctypes.Structure):
@@ -105,6 +113,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cas_adam_lr_scale.restype = ctypes.c_float
     lib.cas_cartridge_adam_workspace_size.argtypes = [P(AdamCartridge), i32, i32, i32, P(sz)]
     lib.cas_cartridge_adam.argtypes = [P(AdamCartridge), i32, i32, i32, P(AdamConfig), vp, sz, vp]
+    lib.cas_paged_decode_workspace_size.argtypes = [P(DecodeProblem), P(sz)]
+    lib.cas_paged_decode_fwd.argtypes = [P(DecodeProblem), vp, vp, vp, vp, vp, vp, sz, vp]
     lib.cas_set_tuning.argtypes = [P(Tuning)]
     lib.cas_get_tuning.argtypes = [P(Tuning)]
     lib.cas_plan_info.argtypes = [P(Problem), P(PlanInfo)]
@@ -114,7 +124,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     for name in ("cas_prefix_attn_workspace_size", "cas_prefix_attn_fwd", "cas_prefix_attn_bwd",
                  "cas_cartridge_stage", "cas_set_tuning", "cas_get_tuning", "cas_plan_info",
                  "cas_timing_enable", "cas_timing_reset", "cas_timing_read",
-                 "cas_cartridge_adam_workspace_size", "cas_cartridge_adam"):
+                 "cas_cartridge_adam_workspace_size", "cas_cartridge_adam",
+                 "cas_paged_decode_workspace_size", "cas_paged_decode_fwd"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib

@@ -711,6 +711,120 @@ cas_status_t check_workspace(void *ws, size_t have, size_t need) {
   return CAS_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Paged decode: validation, key-axis split planning and launch tables.
+// ---------------------------------------------------------------------------
+constexpr int kMaxDecSplits = 64;
+
+struct DecodePlan {
+  int Tq = 0, Hq = 0;
+  std::vector<DevDecodeReq> reqs;
+  std::vector<DevDecodeWork> work;
+  std::vector<int32_t> tok_req;
+  int max_split = 1;
+  size_t off_work = 0, off_pages = 0, off_tokreq = 0, off_plse = 0, off_po = 0, bytes = 0;
+};
+
+cas_status_t build_decode(const cas_decode_problem_t *p, DecodePlan &dp) {
+  if (!p) return fail(CAS_ERR_INVALID_ARGUMENT, "problem is NULL");
+  if (p->batch < 1 || p->num_kv_heads < 1 || p->group_size < 1)
+    return fail(CAS_ERR_INVALID_ARGUMENT, "batch, num_kv_heads and group_size must be >= 1");
+  if (p->head_dim != 64 && p->head_dim != 128) return fail(CAS_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (!std::isfinite(p->softmax_scale) || !(p->softmax_scale > 0.0f))
+    return fail(CAS_ERR_INVALID_ARGUMENT, "softmax_scale must be finite and > 0");
+  const int P = p->page_size;
+  if (P != 16 && P != 32 && P != 64 && P != 128) return fail(CAS_ERR_UNSUPPORTED, "page_size must be 16, 32, 64 or 128");
+  const int64_t Hq = (int64_t)p->num_kv_heads * p->group_size;
+  if (Hq > (1 << 16)) return fail(CAS_ERR_UNSUPPORTED, "num_kv_heads*group_size above 2^16");
+  if ((int64_t)P * p->num_kv_heads * p->head_dim * 2 >= ((int64_t)1 << 31))
+    return fail(CAS_ERR_UNSUPPORTED, "page larger than 2 GiB");
+  if (p->num_pages < 1) return fail(CAS_ERR_INVALID_ARGUMENT, "num_pages must be >= 1");
+  if (!p->q_offsets || !p->kv_lens || !p->page_offsets || !p->page_ids)
+    return fail(CAS_ERR_INVALID_ARGUMENT, "q_offsets, kv_lens, page_offsets and page_ids must be non-NULL");
+  if (p->q_offsets[0] != 0 || p->page_offsets[0] != 0)
+    return fail(CAS_ERR_INVALID_ARGUMENT, "q_offsets[0] and page_offsets[0] must be 0");
+  const int B = p->batch;
+  for (int b = 0; b < B; ++b) {
+    const int64_t n = (int64_t)p->q_offsets[b + 1] - p->q_offsets[b];
+    const int64_t L = p->kv_lens[b];
+    if (n < 1) return fail(CAS_ERR_INVALID_ARGUMENT, "request " + std::to_string(b) + ": no query token");
+    if (L < n) return fail(CAS_ERR_INVALID_ARGUMENT, "request " + std::to_string(b) + ": kv_len below its query count");
+    if (L > (1 << 30)) return fail(CAS_ERR_UNSUPPORTED, "request " + std::to_string(b) + ": more than 2^30 keys");
+    if ((int64_t)p->page_offsets[b + 1] - p->page_offsets[b] != ceil_div(L, P))
+      return fail(CAS_ERR_INVALID_ARGUMENT, "request " + std::to_string(b) + ": page count must be ceil(kv_len / page_size)");
+  }
+  const int64_t Tq = p->q_offsets[B];
+  if (Tq * Hq > INT32_MAX) return fail(CAS_ERR_UNSUPPORTED, "query tokens * heads above 2^31");
+  for (int32_t i = 0; i < p->page_offsets[B]; ++i)
+    if (p->page_ids[i] < 0 || p->page_ids[i] >= p->num_pages)
+      return fail(CAS_ERR_INVALID_ARGUMENT, "page id " + std::to_string(i) + " out of range");
+  dp.Tq = (int)Tq;
+  dp.Hq = (int)Hq;
+  const int g = p->group_size, Hkv = p->num_kv_heads;
+  // Split planning: about 1024 workgroups of at least 8 tiles (two per wave).
+  int64_t total = 0;
+  for (int b = 0; b < B; ++b) {
+    const int64_t n = p->q_offsets[b + 1] - p->q_offsets[b];
+    total += ceil_div(p->kv_lens[b], kDecTile) * Hkv * ceil_div(n * g, kDecRows);
+  }
+  const int64_t per_wg = std::max<int64_t>(8, ceil_div(total, 1024));
+  dp.reqs.resize(B);
+  dp.tok_req.resize(Tq);
+  struct W {
+    int64_t tiles;
+    DevDecodeWork w;
+  };
+  std::vector<W> work;
+  for (int b = 0; b < B; ++b) {
+    const int n = p->q_offsets[b + 1] - p->q_offsets[b];
+    const int64_t nt = ceil_div(p->kv_lens[b], kDecTile);
+    const int ns = (int)std::min<int64_t>(kMaxDecSplits, ceil_div(nt, per_wg));
+    DevDecodeReq &r = dp.reqs[b];
+    r.q0 = p->q_offsets[b];
+    r.n = n;
+    r.kv_len = p->kv_lens[b];
+    r.page0 = p->page_offsets[b];
+    r.nsplit = ns;
+    dp.max_split = std::max(dp.max_split, ns);
+    for (int t = 0; t < n; ++t) dp.tok_req[r.q0 + t] = b;
+    for (int kvh = 0; kvh < Hkv; ++kvh)
+      for (int row0 = 0; row0 < n * g; row0 += kDecRows)
+        for (int s = 0; s < ns; ++s) {
+          DevDecodeWork d{};
+          d.b = b;
+          d.kvh = kvh;
+          d.row0 = row0;
+          d.split = ns > 1 ? s : -1;
+          d.tile0 = (int)(nt * s / ns);
+          d.tile1 = (int)(nt * (s + 1) / ns);
+          work.push_back({d.tile1 - d.tile0, d});
+        }
+  }
+  if (work.size() > (size_t)INT32_MAX) return fail(CAS_ERR_UNSUPPORTED, "too many workgroups");
+  // Longest ranges first.
+  std::stable_sort(work.begin(), work.end(), [](const W &a, const W &b) { return a.tiles > b.tiles; });
+  dp.work.resize(work.size());
+  for (size_t i = 0; i < work.size(); ++i) dp.work[i] = work[i].w;
+  size_t off = align_up(dp.reqs.size() * sizeof(DevDecodeReq), 256);
+  dp.off_work = off;
+  off = align_up(off + dp.work.size() * sizeof(DevDecodeWork), 256);
+  dp.off_pages = off;
+  off = align_up(off + (size_t)p->page_offsets[B] * sizeof(int32_t), 256);
+  dp.off_tokreq = off;
+  off = align_up(off + (size_t)Tq * sizeof(int32_t), 256);
+  const size_t table_end = off;
+  if (dp.max_split > 1) {
+    const size_t plane = (size_t)Tq * Hq;
+    dp.off_plse = off;
+    off = align_up(off + (size_t)dp.max_split * plane * 4, 256);
+    dp.off_po = off;
+    off = align_up(off + (size_t)dp.max_split * plane * p->head_dim * 4, 256);
+  }
+  dp.bytes = off;
+  (void)table_end;
+  return CAS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -734,6 +848,73 @@ const char *cas_last_error_message(void) { return g_err.c_str(); }
 
 float cas_adam_lr_scale(int32_t step, int32_t warmup_steps, int32_t warmup_buckets) {
   return lr_scale(step, warmup_steps, warmup_buckets);
+}
+
+cas_status_t cas_paged_decode_workspace_size(const cas_decode_problem_t *p, size_t *bytes) {
+  if (!bytes) return fail(CAS_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  DecodePlan dp;
+  cas_status_t s = build_decode(p, dp);
+  if (s != CAS_OK) return s;
+  *bytes = dp.bytes;
+  return CAS_OK;
+}
+
+cas_status_t cas_paged_decode_fwd(const cas_decode_problem_t *p, const void *q, const void *k_pages,
+                                  const void *v_pages, void *o, float *lse, void *workspace,
+                                  size_t ws_bytes, void *hip_stream) {
+  DecodePlan dp;
+  cas_status_t s = build_decode(p, dp);
+  if (s != CAS_OK) return s;
+  if (!q || !k_pages || !v_pages || !o) return fail(CAS_ERR_INVALID_ARGUMENT, "q, k_pages, v_pages and o must be non-NULL");
+  if (!aligned16(q) || !aligned16(k_pages) || !aligned16(v_pages) || !aligned16(o) || ((uintptr_t)lse & 3u))
+    return fail(CAS_ERR_ALIGNMENT, "tensors must be 16-byte aligned (lse 4-byte)");
+  const uintptr_t qbytes = (uintptr_t)dp.Tq * dp.Hq * p->head_dim * 2;
+  const uintptr_t pool = (uintptr_t)p->num_pages * p->page_size * p->num_kv_heads * p->head_dim * 2;
+  std::vector<Interval> iv;
+  iv.push_back({(uintptr_t)q, (uintptr_t)q + qbytes, false, 0, "q"});
+  iv.push_back({(uintptr_t)k_pages, (uintptr_t)k_pages + pool, false, 0, "k_pages"});
+  iv.push_back({(uintptr_t)v_pages, (uintptr_t)v_pages + pool, false, 0, "v_pages"});
+  iv.push_back({(uintptr_t)o, (uintptr_t)o + qbytes, true, 1, "o"});
+  if (lse) iv.push_back({(uintptr_t)lse, (uintptr_t)lse + (uintptr_t)dp.Tq * dp.Hq * 4, true, 2, "lse"});
+  std::string msg;
+  if (!overlap_free(iv, msg)) return fail(CAS_ERR_INVALID_ARGUMENT, msg);
+  s = check_workspace(workspace, ws_bytes, dp.bytes);
+  if (s != CAS_OK) return s;
+  hipStream_t stream = (hipStream_t)hip_stream;
+  char *ws = (char *)workspace;
+  const int npage_ids = p->page_offsets[p->batch];
+  s = ring_upload(dp.off_plse ? dp.off_plse : dp.bytes, workspace, stream, [&](char *h) {
+    std::memcpy(h, dp.reqs.data(), dp.reqs.size() * sizeof(DevDecodeReq));
+    std::memcpy(h + dp.off_work, dp.work.data(), dp.work.size() * sizeof(DevDecodeWork));
+    if (npage_ids) std::memcpy(h + dp.off_pages, p->page_ids, (size_t)npage_ids * sizeof(int32_t));
+    std::memcpy(h + dp.off_tokreq, dp.tok_req.data(), dp.tok_req.size() * sizeof(int32_t));
+  });
+  if (s != CAS_OK) return s;
+  DecodeParams kp{};
+  kp.q = q;
+  kp.k_pages = k_pages;
+  kp.v_pages = v_pages;
+  kp.o = o;
+  kp.lse = lse;
+  kp.reqs = (const DevDecodeReq *)ws;
+  kp.work = (const DevDecodeWork *)(ws + dp.off_work);
+  kp.page_ids = (const int32_t *)(ws + dp.off_pages);
+  kp.tok_req = (const int32_t *)(ws + dp.off_tokreq);
+  kp.part_lse = dp.max_split > 1 ? (float *)(ws + dp.off_plse) : nullptr;
+  kp.part_o = dp.max_split > 1 ? (float *)(ws + dp.off_po) : nullptr;
+  kp.plane = (int64_t)dp.Tq * dp.Hq;
+  kp.Hkv = p->num_kv_heads;
+  kp.g = p->group_size;
+  kp.page_size = p->page_size;
+  kp.Tq = dp.Tq;
+  kp.scale_log2 = p->softmax_scale * 1.4426950408889634f;
+  hipError_t e = timed("decode", stream, [&] { return launch_decode_bf16(kp, p->head_dim, (int)dp.work.size(), stream); });
+  if (e != hipSuccess) return hip_fail("decode launch", e);
+  if (dp.max_split > 1) {
+    e = timed("decode_merge", stream, [&] { return launch_decode_merge_bf16(kp, p->head_dim, stream); });
+    if (e != hipSuccess) return hip_fail("decode_merge launch", e);
+  }
+  return CAS_OK;
 }
 
 cas_status_t cas_cartridge_adam_workspace_size(const cas_adam_cartridge_t *carts, int32_t n,

@@ -207,6 +207,40 @@ struct AdamParams {
   float eps;
 };
 
+// Paged decode: one request (its queries are tokens q0 .. q0+n-1; its keys
+// the pages page_ids[page0 ..] in order, kv_len of them) and one workgroup's
+// share: packed rows row0 .. row0+31 (row r = query r / g, head kvh*g + r % g)
+// over 32-key tiles [tile0, tile1) of the request's key axis.
+constexpr int kDecTile = 32;
+constexpr int kDecRows = 32;
+struct DevDecodeReq {
+  int32_t q0, n, kv_len, page0;
+  int32_t nsplit;        // key-axis splits of every row block of the request
+  int32_t pad_[3];
+};
+struct DevDecodeWork {
+  int32_t b, kvh, row0, split;   // split index, or -1 when the range is the whole axis
+  int32_t tile0, tile1;
+  int32_t pad_[2];
+};
+
+struct DecodeParams {
+  const void *q;
+  const void *k_pages;
+  const void *v_pages;
+  void *o;
+  float *lse;             // [Hq][Tq] or null
+  const DevDecodeReq *reqs;
+  const DevDecodeWork *work;
+  const int32_t *page_ids;
+  const int32_t *tok_req; // [Tq] request of each query token (merge)
+  float *part_o;          // [split][Tq * Hq][D] when a request is split
+  float *part_lse;        // [split][Tq * Hq]
+  int64_t plane;          // Tq * Hq
+  int32_t Hkv, g, page_size, Tq;
+  float scale_log2;
+};
+
 // Kernel launchers (defined in the .hip files).
 hipError_t launch_fwd(const FwdParams &p, DType dt, int D, hipStream_t s);
 hipError_t launch_fwd_merge(const MergeParams &p, DType dt, int D, hipStream_t s);
@@ -221,5 +255,7 @@ hipError_t launch_dq_bf16(const DqParams &p, int D, hipStream_t s);
 hipError_t launch_dkdv_bf16(const DkdvParams &p, int D, int n_wg, hipStream_t s);
 hipError_t launch_bwd_transpose_bf16(const PreParams &p, int D, hipStream_t s);
 hipError_t launch_adam_bf16(const AdamParams &p, int D, int n_chunks, hipStream_t s);
+hipError_t launch_decode_bf16(const DecodeParams &p, int D, int n_work, hipStream_t s);
+hipError_t launch_decode_merge_bf16(const DecodeParams &p, int D, hipStream_t s);
 
 }  // namespace cas

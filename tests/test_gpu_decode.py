@@ -1,0 +1,108 @@
+"""GPU parity of the paged short-query / decode attention (cas_paged_decode_fwd)
+against the fp64 oracle: requests over retrieved cartridges held in a
+paged KV pool (paper: Section "Inference", paragraph "Cartridge RAG"; the
+appendix on cartridge sizes for the 16-token pages).
+
+Bars as for the other bf16 paths: max |gpu - oracle| / max |oracle| <= 2e-2
+on O, LSE absolute error <= 1e-3; every output element is compared.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from casgen import rng
+from gpu_util import LSE_TOL, TOL, host, rel_err
+
+pytestmark = pytest.mark.gpu
+
+
+def _pool(seed, n_carts, cart_pages, P, Hkv, D, reqs, own_extra=0):
+    """A page pool: cartridge c owns pages [c * cart_pages, (c+1) * cart_pages);
+    each request's own tokens get fresh pages after them. reqs: (cartridge ids,
+    own tokens, queries). Returns pool arrays (bf16 values as float32), the
+    per-request key counts, query counts and page lists."""
+    own_pages = [-(-own // P) for _, own, _ in reqs]
+    npages = n_carts * cart_pages + sum(own_pages) + own_extra
+    shape = (npages, P, Hkv, D)
+    bits = lambda tag: rng.f64_to_bf16_bits(rng.normal(rng.stream_key(seed, tag), int(np.prod(shape)), 0.5))
+    kp = rng.bf16_bits_to_f32(bits(1)).reshape(shape)
+    vp = rng.bf16_bits_to_f32(bits(2)).reshape(shape)
+    nxt = n_carts * cart_pages
+    kv_lens, q_counts, pages = [], [], []
+    for (carts, own, n), op in zip(reqs, own_pages):
+        pl = [c * cart_pages + j for c in carts for j in range(cart_pages)]
+        pl += list(range(nxt, nxt + op))
+        nxt += op
+        pages.append(pl)
+        kv_lens.append(len(carts) * cart_pages * P + own)
+        q_counts.append(n)
+    return kp, vp, kv_lens, q_counts, pages
+
+
+def _run(kp, vp, kv_lens, q_counts, pages, Hkv, g, D, seed, scale=None):
+    import torch
+    import paper_2606_04557_amd as cas
+    Tq, Hq = sum(q_counts), Hkv * g
+    q = rng.bf16_bits_to_f32(rng.f64_to_bf16_bits(rng.normal(rng.stream_key(seed, 3), Tq * Hq * D, 1.0))).reshape(
+        Tq, Hq, D)
+    scale = scale or float(np.float32(1.0 / np.sqrt(D)))
+    dq = torch.from_numpy(q).to(torch.bfloat16).cuda()
+    dk = torch.from_numpy(kp).to(torch.bfloat16).cuda()
+    dv = torch.from_numpy(vp).to(torch.bfloat16).cuda()
+    o, lse = cas.paged_decode_fwd(dq, dk, dv, q_counts, kv_lens, pages, Hkv, g, scale)
+    torch.cuda.synchronize()
+    O, LSE = oracle.paged_decode_forward(q, kp, vp, q_counts, kv_lens, pages, scale, g)
+    e_o = rel_err(host(o), O)
+    e_l = float(np.abs(host(lse) - LSE).max())
+    print(f"decode O {e_o:.2e} LSE {e_l:.2e}")
+    assert e_o <= TOL["bf16"] and e_l <= LSE_TOL["bf16"], (e_o, e_l)
+    return o, lse
+
+
+CASES = [
+    # (page size, kv heads, group, head dim, cartridges of the pool, pages per cartridge,
+    #  requests: (cartridge ids, own tokens, queries))
+    dict(name="p16_decode", P=16, Hkv=8, g=4, D=128, n_carts=6, cart_pages=8,
+         reqs=[([0, 3], 1, 1), ([5], 17, 1), ([1, 2, 4, 0], 40, 1), ([], 9, 1), ([2], 100, 3)]),
+    # 9 queries x 4 heads = 36 rows: two row blocks; an own part that starts mid-page
+    dict(name="p16_multirow", P=16, Hkv=2, g=4, D=128, n_carts=3, cart_pages=20,
+         reqs=[([0, 1, 2], 61, 9), ([1], 8, 8), ([2, 0], 33, 2)]),
+    dict(name="p32_d64", P=32, Hkv=2, g=2, D=64, n_carts=4, cart_pages=5,
+         reqs=[([3, 1], 31, 1), ([0], 1, 1), ([2, 3, 0, 1], 64, 5)]),
+    dict(name="p64_g8", P=64, Hkv=1, g=8, D=128, n_carts=2, cart_pages=3,
+         reqs=[([1, 0], 70, 4), ([0], 2, 2)]),
+    dict(name="p128", P=128, Hkv=4, g=4, D=128, n_carts=2, cart_pages=2,
+         reqs=[([0, 1], 300, 1), ([1], 5, 5)]),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c["name"] for c in CASES])
+def test_decode_small(case):
+    c = dict(case)
+    kp, vp, kl, qc, pages = _pool(900 + len(c["name"]), c["n_carts"], c["cart_pages"], c["P"], c["Hkv"], c["D"],
+                                  c["reqs"], own_extra=3)
+    _run(kp, vp, kl, qc, pages, c["Hkv"], c["g"], c["D"], 950 + len(c["name"]))
+
+
+def test_decode_retrieval_mix_full_size():
+    """Cartridge-RAG decode step at full size: a pool of 256 cartridges of 1,024
+    tokens (16,384 pages of 16 tokens, 8 KV heads x 128); 64 requests, each over
+    4 retrieved cartridges plus its own 64-token prompt, decoding one token
+    (kv_len = 4,161). Every output is compared."""
+    sel = [rng.choose_distinct(rng.stream_key(5, 8, r), 256, 4) for r in range(64)]
+    reqs = [(s, 65, 1) for s in sel]
+    kp, vp, kl, qc, pages = _pool(77, 256, 64, 16, 8, 128, reqs)
+    _run(kp, vp, kl, qc, pages, 8, 4, 128, 78)
+
+
+def test_decode_rejects_bad_tables():
+    import torch
+    import paper_2606_04557_amd as cas
+    kp = torch.zeros((4, 16, 2, 64), dtype=torch.bfloat16, device="cuda")
+    q = torch.zeros((2, 4, 64), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(cas.CasError):       # page id out of range
+        cas.paged_decode_fwd(q, kp, kp.clone(), [1, 1], [20, 3], [[0, 4], [1]], 2, 2, 0.125)
+    with pytest.raises(cas.CasError):       # page count != ceil(kv_len / page_size)
+        cas.paged_decode_fwd(q, kp, kp.clone(), [1, 1], [20, 3], [[0], [1]], 2, 2, 0.125)
+    with pytest.raises(cas.CasError):       # more queries than keys
+        cas.paged_decode_fwd(q, kp, kp.clone(), [2, 0], [1, 3], [[0], [1]], 2, 2, 0.125)

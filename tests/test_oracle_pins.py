@@ -465,3 +465,56 @@ def test_p13_packed_block_diagonal_and_fixed_layout():
     Op, LSEp = _pfwd(f)
     assert np.allclose(Op, Of.reshape(6, 2, 4), rtol=0, atol=1e-14)
     assert np.allclose(LSEp, LSEf.transpose(1, 0, 2).reshape(2, 6), rtol=0, atol=1e-14)
+
+
+# ---------------------------------------------------------------------------
+# Paged decode (requests over page lists; the last n keys are the new tokens).
+# ---------------------------------------------------------------------------
+
+def _paged_problem(seed, P=4, npages=9, Hq=4, Hkv=2, D=4, reqs=((9, 1), (4, 3), (12, 2))):
+    r = np.random.default_rng(seed)
+    kp = r.standard_normal((npages, P, Hkv, D))
+    vp = r.standard_normal((npages, P, Hkv, D))
+    kv_lens = [L for L, _ in reqs]
+    q_counts = [n for _, n in reqs]
+    pages = [list(r.permutation(npages)[: -(-L // P)]) for L in kv_lens]
+    q = r.standard_normal((sum(q_counts), Hq, D))
+    return q, kp, vp, q_counts, kv_lens, pages
+
+
+def test_p14_paged_decode_equals_prefix_plus_self():
+    """P14: each request equals the fixed-layout problem whose single cartridge
+    is its first L - n gathered keys and whose self tokens are the last n."""
+    q, kp, vp, qc, kl, pages = _paged_problem(14)
+    O, LSE = oracle.paged_decode_forward(q, kp, vp, qc, kl, pages, 0.45, 2)
+    q0 = 0
+    for b, n in enumerate(qc):
+        K = np.concatenate([kp[p] for p in pages[b]])[: kl[b]]
+        V = np.concatenate([vp[p] for p in pages[b]])[: kl[b]]
+        L = kl[b]
+        Of, LSEf = oracle.forward(q[None, q0:q0 + n], K[None, L - n:], V[None, L - n:], [K[: L - n]],
+                                  [V[: L - n]], [[0]], 0.45, 2)
+        assert np.allclose(O[q0:q0 + n], Of[0], rtol=0, atol=1e-14)
+        assert np.allclose(LSE[:, q0:q0 + n], LSEf[0], rtol=0, atol=1e-14)
+        q0 += n
+
+
+def test_p15_paged_decode_brute_force():
+    """P15: scalar loops over the keys each query sees, with math.exp."""
+    q, kp, vp, qc, kl, pages = _paged_problem(15, P=2, npages=7, reqs=((5, 2), (3, 1)))
+    O, LSE = oracle.paged_decode_forward(q, kp, vp, qc, kl, pages, 0.8, 2)
+    q0 = 0
+    for b, n in enumerate(qc):
+        keys = [(p, j) for p in pages[b] for j in range(kp.shape[1])][: kl[b]]
+        for i in range(n):
+            for h in range(q.shape[1]):
+                kv = h // 2
+                vis = keys[: kl[b] - n + i + 1]
+                s = [0.8 * sum(q[q0 + i, h, d] * kp[p, j, kv, d] for d in range(q.shape[2])) for p, j in vis]
+                m = max(s)
+                z = sum(math.exp(x - m) for x in s)
+                assert abs(LSE[h, q0 + i] - (m + math.log(z))) < 1e-12
+                for d in range(q.shape[2]):
+                    ref = sum(math.exp(x - m) / z * vp[p, j, kv, d] for x, (p, j) in zip(s, vis))
+                    assert abs(O[q0 + i, h, d] - ref) < 1e-12
+        q0 += n
