@@ -108,6 +108,8 @@ def main():
                     help="time the cartridge Adam step over the packed layout's 20-cartridge pool")
     ap.add_argument("--decode", action="store_true",
                     help="time one paged decode step of the retrieval mix (64 requests x 4 cartridges)")
+    ap.add_argument("--pool", action="store_true",
+                    help="time training steps (packed attention fwd+bwd, Adam) through the budget manager")
     ap.add_argument("--cpu-heads", type=int, default=16, help="oracle heads timed for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "hbm_traffic_16x2k.json"),
@@ -142,6 +144,8 @@ def main():
         return run_adam(args)
     if args.decode:
         return run_decode(args)
+    if args.pool:
+        return run_pool(args)
     wl = casgen.packed() if args.packed else casgen.config(args.config)
     if wl.forward_only:
         print("bench.py times forward+backward; pick config 1-4", file=sys.stderr)
@@ -425,6 +429,80 @@ def run_decode(args):
         el = time.perf_counter() - t0
         out["cpu_baseline"] = {"value": sum(kv_lens[:8]) * Hkv * D * 4 / el / 1e9, "unit": "GB/s", "cores": 1,
                                "kind": "oracle", "sample": f"8 of the 64 requests, {el:.1f} s"}
+    print(json.dumps(out), flush=True)
+
+
+def run_pool(args):
+    """Training steps through the budget manager with the paper's settings
+    (B = 20 active of N = 60 cartridges, rotation every R = 10 steps swapping
+    phi = 0.5 of the pool, least-trained first): per step one layer's packed
+    8,192-token attention forward and backward over the active cartridges
+    (the packed layout's samples, their cartridge slots mapped onto the active
+    set), the fused Adam step, and cas_pool_end_step. The same loop with
+    phi = 0 (no rotation) gives the cost of the rotations' copies, which run
+    on the pool's stream behind the compute."""
+    import numpy as np
+    import torch
+    import casgen
+    import paper_2606_04557_amd as cas
+    from casgen import rng
+    wl = casgen.packed()
+    Hkv, g, D = wl.num_kv_heads, wl.group_size, wl.head_dim
+    lens = [wl.cart_lens[c % len(wl.cart_lens)] for c in range(60)]
+    T = casgen.make_tensors(wl, carts=[])
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    q, ks, vs, do = dev(T["q"]), dev(T["k_self"]), dev(T["v_self"]), dev(T["d_o"])
+    qo, scale = wl.q_offsets, float(wl.scale)
+    o, dq = torch.empty_like(q), torch.empty_like(q)
+    lse = torch.empty((wl.num_q_heads, sum(wl.row_lens)), dtype=torch.float32, device="cuda")
+    dks, dvs = torch.empty_like(ks), torch.empty_like(vs)
+    cfg = dict(lr=0.05, beta1=0.9, beta2=0.999, eps=1e-8, warmup_steps=20, warmup_buckets=4)
+    res = {}
+    steps = args.steps if args.steps >= 20 else 40
+    for phi in (0.5, 0.0):
+        pl = cas.CartridgePool(lens, Hkv, D, 20, 10, phi, frozen_tokens=1)
+        for c, L in enumerate(lens):
+            h = pl.host(c)
+            for i, name in enumerate(("k", "v")):
+                h[name][...] = rng.f64_to_bf16_bits(rng.normal(rng.stream_key(60, c, i), L * Hkv * D, 0.5)
+                                                    ).view(np.int16).reshape(L, Hkv, D)
+        pl.load()
+
+        def step():
+            act = pl.active()
+            views = [a for _, a in act]
+            rows = [[cas.Segment(views[i].k, views[i].v, views[i].dk, views[i].dv) for i in r] for r in wl.rows]
+            cas.prefix_attn_fwd(q, ks, vs, rows, Hkv, g, scale, o=o, lse=lse, q_offsets=qo)
+            cas.prefix_attn_bwd(q, ks, vs, rows, Hkv, g, scale, o, lse, do, dq=dq, dk_self=dks, dv_self=dvs,
+                                q_offsets=qo)
+            cas.cartridge_adam(views, **cfg)
+            pl.end_step()
+
+        for _ in range(5):
+            step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            step()
+        torch.cuda.synchronize()
+        res[phi] = (time.perf_counter() - t0) * 1e3 / steps
+        pl.flush()
+        pl.close()
+    per_cart = [L * Hkv * D * (2 * 2 + 4 * 4) for L in lens]
+    moved = 2 * 10 * (sum(per_cart) / len(per_cart))         # 10 evicted + 10 admitted per rotation
+    out = {
+        "metric": "training step through the budget manager, ms per step (packed 8K attention fwd+bwd + Adam)",
+        "value": res[0.5], "unit": "ms", "n_gpus": 1, "steps": steps, "warmup": 5, "ms_per_step": res[0.5],
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded Gaussian cartridges and samples)",
+        "config": {"workload": "N = 60 cartridges, B = 20 active, rotation every 10 steps swapping 10 "
+                               "(least-trained first); one attention layer of the packed 8,192-token layout",
+                   "parallelism": "single GPU"},
+        "ms_per_step_without_rotation": res[0.0],
+        "rotation_overhead_frac": res[0.5] / res[0.0] - 1.0,
+        "bytes_moved_per_rotation": moved,
+        "roofline": None, "cpu_baseline": None,
+    }
     print(json.dumps(out), flush=True)
 
 

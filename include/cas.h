@@ -292,6 +292,57 @@ cas_status_t cas_paged_decode_fwd(const cas_decode_problem_t *p, const void *q, 
                                   const void *v_pages, void *o, float *lse, void *workspace,
                                   size_t ws_bytes, void *hip_stream);
 
+/*
+ * Budget manager (paper: paragraphs "Budget Manager" and "Pool rotation";
+ * hyperparameter table: budget B = 20, rotation interval R = 10, swap
+ * fraction phi = 0.5, least-trained cartridges first). The pool owns a
+ * pinned host copy of every cartridge (bf16 K/V, fp32 Adam moments, step
+ * count) and B active device slots, plus floor(phi * B) staging slots into
+ * which the next rotation's cartridges are copied ahead of time on the
+ * pool's own stream while the current ones train.
+ *
+ * Rotation, after every R-th cas_pool_end_step: the n = min(floor(phi * B),
+ * N - B) active cartridges with the most optimizer steps (ties: lower id)
+ * are copied back to host (parameters and moments, after the compute
+ * stream's work so far) and leave the active set; the prefetched cartridges,
+ * the n offloaded ones with the fewest steps (ties: lower id), take their
+ * place; then the next admissions are prefetched into the freed slots.
+ * Offloaded cartridges receive no gradient. cas_pool_plan_rotation is that
+ * policy on its own (host only).
+ *
+ * Use: create; fill the host copies (cas_pool_host_cartridge: pinned views,
+ * moments zero, step 0); cas_pool_load; then per training step read the
+ * active set (cas_pool_active: device views of K/V, their gradient buffers
+ * dk/dv, moments and step counts, ready for cas_cartridge_adam) and call
+ * cas_pool_end_step after the optimizer step. cas_pool_flush copies every
+ * active cartridge back and waits, after which all host copies are current.
+ * Calls on one pool must not overlap; streams are the caller's except the
+ * pool's own copy stream (default priority).
+ */
+typedef struct cas_pool cas_pool_t;
+
+typedef struct {
+  int32_t num_cartridges;   /* N >= 1 */
+  const int64_t *lens;      /* host, N token counts (>= 1) */
+  int32_t num_kv_heads;
+  int32_t head_dim;         /* 64 or 128 */
+  int32_t budget;           /* B, 1 <= B <= N */
+  int32_t rotate_every;     /* R >= 1 */
+  float swap_fraction;      /* phi in [0, 1] */
+  int32_t frozen_tokens;    /* reported in the views (BOS: 1) */
+} cas_pool_config_t;
+
+cas_status_t cas_pool_plan_rotation(const int32_t *steps, const uint8_t *active, int32_t n, int32_t budget,
+                                    float swap_fraction, int32_t *evict, int32_t *admit, int32_t *n_swap);
+cas_status_t cas_pool_create(const cas_pool_config_t *cfg, cas_pool_t **pool);
+cas_status_t cas_pool_destroy(cas_pool_t *pool);
+cas_status_t cas_pool_host_cartridge(cas_pool_t *pool, int32_t cart, cas_adam_cartridge_t *host_view);
+cas_status_t cas_pool_load(cas_pool_t *pool, void *compute_stream);
+cas_status_t cas_pool_active(cas_pool_t *pool, int32_t *cart_ids, cas_adam_cartridge_t *views, int32_t cap,
+                             int32_t *n);
+cas_status_t cas_pool_end_step(cas_pool_t *pool, void *compute_stream);
+cas_status_t cas_pool_flush(cas_pool_t *pool, void *compute_stream);
+
 /* Static description of a status code. */
 const char *cas_status_string(cas_status_t s);
 /* Message of the last failed call on this thread ("" if none). */

@@ -22,3 +22,4 @@ from .attention import (  # noqa: F401
     visible_mask,
 )
 from . import adam  # noqa: F401,E402
+from . import pool  # noqa: F401,E402

@@ -17,7 +17,7 @@ from ._lib import load  # noqa: F401
 __all__ = ["Segment", "Problem", "CasError", "load", "prefix_attn_fwd", "prefix_attn_bwd",
            "workspace_size", "plan_info", "set_tuning", "get_tuning", "cartridge_stage",
            "timing_enable", "timing_reset", "timing_read", "AdamCartridge", "adam_lr_scale",
-           "cartridge_adam", "DecodeProblem", "paged_decode_fwd"]
+           "cartridge_adam", "DecodeProblem", "paged_decode_fwd", "plan_rotation", "CartridgePool"]
 
 
 class CasError(RuntimeError):
@@ -319,6 +319,103 @@ def paged_decode_fwd(q, k_pages, v_pages, q_counts: Sequence[int], kv_lens: Sequ
                                        o.data_ptr(), _ptr(lse), ws.data_ptr(), ws.numel(),
                                        _stream_handle(q.device, stream)))
     return o, lse
+
+
+def plan_rotation(steps: Sequence[int], active: Sequence[bool], budget: int, swap_fraction: float):
+    """The budget manager's rotation choice (cas_pool_plan_rotation): (evict, admit)."""
+    n = len(steps)
+    st = (ctypes.c_int32 * n)(*[int(x) for x in steps])
+    ac = (ctypes.c_uint8 * n)(*[1 if a else 0 for a in active])
+    ev = (ctypes.c_int32 * n)()
+    ad = (ctypes.c_int32 * n)()
+    m = ctypes.c_int32(0)
+    _check(load().cas_pool_plan_rotation(st, ac, n, int(budget), float(swap_fraction), ev, ad, ctypes.byref(m)))
+    return list(ev[:m.value]), list(ad[:m.value])
+
+
+class _DevArray:
+    """A device buffer of the pool seen by torch (__cuda_array_interface__)."""
+
+    def __init__(self, ptr: int, shape, typestr: str):
+        self.__cuda_array_interface__ = {"shape": tuple(shape), "typestr": typestr, "data": (int(ptr), False),
+                                         "version": 2, "strides": None}
+
+
+class CartridgePool:
+    """Budget manager (cas_pool_*): pinned host copies of every cartridge, B
+    active device slots and prefetched rotations."""
+
+    def __init__(self, lens: Sequence[int], num_kv_heads: int, head_dim: int, budget: int, rotate_every: int,
+                 swap_fraction: float, frozen_tokens: int = 1):
+        self.lens = [int(x) for x in lens]
+        self.Hkv, self.D = num_kv_heads, head_dim
+        self._lens = (ctypes.c_int64 * len(lens))(*self.lens)
+        cfg = _lib.PoolConfig(len(lens), ctypes.cast(self._lens, ctypes.POINTER(ctypes.c_int64)), num_kv_heads,
+                              head_dim, budget, rotate_every, swap_fraction, frozen_tokens)
+        h = ctypes.c_void_p()
+        _check(load().cas_pool_create(ctypes.byref(cfg), ctypes.byref(h)))
+        self.h = h
+
+    def close(self):
+        if self.h:
+            _check(load().cas_pool_destroy(self.h))
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def host(self, cart: int) -> dict:
+        """numpy views of cartridge `cart`'s pinned host copy: k, v (bf16 bits as
+        int16), m1_k, m2_k, m1_v, m2_v (float32), and its step count."""
+        import numpy as np
+        v = _lib.AdamCartridge()
+        _check(load().cas_pool_host_cartridge(self.h, int(cart), ctypes.byref(v)))
+        L, shp = int(v.len), (int(v.len), self.Hkv, self.D)
+        n = L * self.Hkv * self.D
+        out = {}
+        for name in ("k", "v"):
+            out[name] = np.ctypeslib.as_array(ctypes.cast(getattr(v, name), ctypes.POINTER(ctypes.c_int16)),
+                                              (n,)).reshape(shp)
+        for name in ("m1_k", "m2_k", "m1_v", "m2_v"):
+            out[name] = np.ctypeslib.as_array(ctypes.cast(getattr(v, name), ctypes.POINTER(ctypes.c_float)),
+                                              (n,)).reshape(shp)
+        out["step"] = int(v.step)
+        return out
+
+    def load(self, stream=None):
+        import torch
+        _check(load().cas_pool_load(self.h, _stream_handle(torch.device("cuda"), stream)))
+
+    def active(self):
+        """[(cartridge id, AdamCartridge of torch views over its device slot)]."""
+        import torch
+        cap = 1 << 12
+        ids = (ctypes.c_int32 * cap)()
+        views = (_lib.AdamCartridge * cap)()
+        n = ctypes.c_int32(0)
+        _check(load().cas_pool_active(self.h, ids, views, cap, ctypes.byref(n)))
+        out = []
+        for i in range(n.value):
+            v = views[i]
+            shp = (int(v.len), self.Hkv, self.D)
+            t = {}
+            for name in ("k", "v", "dk", "dv"):
+                t[name] = torch.as_tensor(_DevArray(getattr(v, name), shp, "<i2"), device="cuda").view(torch.bfloat16)
+            for name in ("m1_k", "m2_k", "m1_v", "m2_v"):
+                t[name] = torch.as_tensor(_DevArray(getattr(v, name), shp, "<f4"), device="cuda")
+            out.append((int(ids[i]), AdamCartridge(**t, step=int(v.step), frozen_tokens=int(v.frozen_tokens))))
+        return out
+
+    def end_step(self, stream=None):
+        import torch
+        _check(load().cas_pool_end_step(self.h, _stream_handle(torch.device("cuda"), stream)))
+
+    def flush(self, stream=None):
+        import torch
+        _check(load().cas_pool_flush(self.h, _stream_handle(torch.device("cuda"), stream)))
 
 
 def cartridge_stage(copies: Sequence[Tuple[object, object]], side_stream, done_event=None) -> None:

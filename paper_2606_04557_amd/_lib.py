@@ -24,6 +24,8 @@ EXPORTS = [
     "cas_set_tuning", "cas_get_tuning", "cas_plan_info", "cas_timing_enable",
     "cas_timing_reset", "cas_timing_read", "cas_adam_lr_scale", "cas_cartridge_adam_workspace_size",
     "cas_cartridge_adam", "cas_paged_decode_workspace_size", "cas_paged_decode_fwd",
+    "cas_pool_plan_rotation", "cas_pool_create", "cas_pool_destroy", "cas_pool_host_cartridge",
+    "cas_pool_load", "cas_pool_active", "cas_pool_end_step", "cas_pool_flush",
 ]
 
 
@@ -61,6 +63,13 @@ class DecodeProblem(ctypes.Structure):
                 ("num_pages", ctypes.c_int64), ("q_offsets", ctypes.POINTER(ctypes.c_int32)),
                 ("kv_lens", ctypes.POINTER(ctypes.c_int32)), ("page_offsets", ctypes.POINTER(ctypes.c_int32)),
                 ("page_ids", ctypes.POINTER(ctypes.c_int32))]
+
+
+class PoolConfig(ctypes.Structure):
+    _fields_ = [("num_cartridges", ctypes.c_int32), ("lens", ctypes.POINTER(ctypes.c_int64)),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("budget", ctypes.c_int32),
+                ("rotate_every", ctypes.c_int32), ("swap_fraction", ctypes.c_float),
+                ("frozen_tokens", ctypes.c_int32)]
 
 
 class StageCopy(ctypes.Structure):
@@ -115,6 +124,15 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cas_cartridge_adam.argtypes = [P(AdamCartridge), i32, i32, i32, P(AdamConfig), vp, sz, vp]
     lib.cas_paged_decode_workspace_size.argtypes = [P(DecodeProblem), P(sz)]
     lib.cas_paged_decode_fwd.argtypes = [P(DecodeProblem), vp, vp, vp, vp, vp, vp, sz, vp]
+    u8p = P(ctypes.c_uint8)
+    lib.cas_pool_plan_rotation.argtypes = [P(i32), u8p, i32, i32, ctypes.c_float, P(i32), P(i32), P(i32)]
+    lib.cas_pool_create.argtypes = [P(PoolConfig), P(vp)]
+    lib.cas_pool_destroy.argtypes = [vp]
+    lib.cas_pool_host_cartridge.argtypes = [vp, i32, P(AdamCartridge)]
+    lib.cas_pool_load.argtypes = [vp, vp]
+    lib.cas_pool_active.argtypes = [vp, P(i32), P(AdamCartridge), i32, P(i32)]
+    lib.cas_pool_end_step.argtypes = [vp, vp]
+    lib.cas_pool_flush.argtypes = [vp, vp]
     lib.cas_set_tuning.argtypes = [P(Tuning)]
     lib.cas_get_tuning.argtypes = [P(Tuning)]
     lib.cas_plan_info.argtypes = [P(Problem), P(PlanInfo)]
@@ -125,7 +143,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                  "cas_cartridge_stage", "cas_set_tuning", "cas_get_tuning", "cas_plan_info",
                  "cas_timing_enable", "cas_timing_reset", "cas_timing_read",
                  "cas_cartridge_adam_workspace_size", "cas_cartridge_adam",
-                 "cas_paged_decode_workspace_size", "cas_paged_decode_fwd"):
+                 "cas_paged_decode_workspace_size", "cas_paged_decode_fwd", "cas_pool_plan_rotation",
+                 "cas_pool_create", "cas_pool_destroy", "cas_pool_host_cartridge", "cas_pool_load",
+                 "cas_pool_active", "cas_pool_end_step", "cas_pool_flush"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
