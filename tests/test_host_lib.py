@@ -336,3 +336,54 @@ def test_adam_validation(lib):
     arr[0] = _adam_cart(f, step=-1)
     assert lib.cas_cartridge_adam_workspace_size(P, 3, 2, 64, ctypes.byref(n)) == _lib.CAS_ERR_INVALID_ARGUMENT
     assert lib.cas_cartridge_adam_workspace_size(P, 0, 2, 64, ctypes.byref(n)) == _lib.CAS_OK and n.value == 0
+
+
+def _decode_problem(B=2, qc=(1, 2), kv=(20, 3), pages=((0, 1), (2,)), P=16, npages=4, Hkv=2, g=2, D=64):
+    qo = [0]
+    for n in qc:
+        qo.append(qo[-1] + n)
+    po = [0]
+    for p in pages:
+        po.append(po[-1] + len(p))
+    ids = [x for p in pages for x in p]
+    keep = [(ctypes.c_int32 * len(qo))(*qo), (ctypes.c_int32 * len(kv))(*kv), (ctypes.c_int32 * len(po))(*po),
+            (ctypes.c_int32 * max(1, len(ids)))(*ids)]
+    I = ctypes.POINTER(ctypes.c_int32)
+    prob = _lib.DecodeProblem(B, Hkv, g, D, 0.125, P, npages, *[ctypes.cast(k, I) for k in keep])
+    return prob, keep
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(), _lib.CAS_OK),
+    (dict(P=24), _lib.CAS_ERR_UNSUPPORTED),
+    (dict(D=96), _lib.CAS_ERR_UNSUPPORTED),
+    (dict(pages=((0, 4), (2,))), _lib.CAS_ERR_INVALID_ARGUMENT),     # page id out of range
+    (dict(pages=((0,), (2,))), _lib.CAS_ERR_INVALID_ARGUMENT),       # 20 keys need 2 pages of 16
+    (dict(qc=(1, 4)), _lib.CAS_ERR_INVALID_ARGUMENT),                # 4 queries, 3 keys
+    (dict(qc=(0, 2)), _lib.CAS_ERR_INVALID_ARGUMENT),                # a request without a query
+])
+def test_decode_validation(lib, over, code):
+    prob, keep = _decode_problem(**over)
+    n = ctypes.c_size_t(0)
+    assert lib.cas_paged_decode_workspace_size(ctypes.byref(prob), ctypes.byref(n)) == code, _msg(lib)
+    if code == _lib.CAS_OK:
+        assert n.value > 0
+
+
+def test_pool_config_validation(lib):
+    lens = (ctypes.c_int64 * 3)(10, 20, 30)
+    P = ctypes.POINTER(ctypes.c_int64)
+    h = ctypes.c_void_p()
+    for bad in (dict(budget=0), dict(budget=4), dict(rotate_every=0), dict(swap_fraction=1.5),
+                dict(head_dim=96), dict(num_kv_heads=0)):
+        cfg = _lib.PoolConfig(3, ctypes.cast(lens, P), 2, 64, 2, 10, 0.5, 1)
+        for k, v in bad.items():
+            setattr(cfg, k, v)
+        st = lib.cas_pool_create(ctypes.byref(cfg), ctypes.byref(h))
+        assert st in (_lib.CAS_ERR_INVALID_ARGUMENT, _lib.CAS_ERR_UNSUPPORTED), (bad, st)
+        assert not h.value
+    bad_lens = (ctypes.c_int64 * 3)(10, 0, 30)
+    cfg = _lib.PoolConfig(3, ctypes.cast(bad_lens, P), 2, 64, 2, 10, 0.5, 1)
+    assert lib.cas_pool_create(ctypes.byref(cfg), ctypes.byref(h)) == _lib.CAS_ERR_INVALID_ARGUMENT
+    assert lib.cas_pool_active(None, None, None, 0, ctypes.byref(ctypes.c_int32())) == _lib.CAS_ERR_INVALID_ARGUMENT
+    assert lib.cas_pool_destroy(None) == _lib.CAS_OK
