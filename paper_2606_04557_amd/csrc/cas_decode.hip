@@ -81,7 +81,21 @@ __global__ __launch_bounds__(kDecWaves * 64) void decode_bf16_kernel(DecodeParam
   for (int i = 0; i < NI; ++i) coff[i] = ((lane % CPR) ^ swz<D>(RPI * i + lrow)) * 8;
   const int64_t row_el = (int64_t)Hkv * D;            // elements between consecutive tokens of a page
 
-  auto issue_tile = [&](int tile, int stage) __attribute__((always_inline)) {
+  // Pages of a tile's copy instructions, read one tile ahead of the copies
+  // (their scalar-load latency then never delays a copy issue).
+  struct TilePages {
+    int id[NI];
+  };
+  auto tile_pages = [&](int tile) __attribute__((always_inline)) {
+    TilePages tp;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int k0 = tile * kDecTile + RPI * i;
+      tp.id[i] = k0 < kv_len ? load_const(p.page_ids, rq.page0 + k0 / P) : 0;
+    }
+    return tp;
+  };
+  auto issue_tile = [&](int tile, const TilePages &tp, int stage) __attribute__((always_inline)) {
     char *kd = wbase + (2 * stage) * TB;
     char *vd = kd + TB;
 #pragma unroll
@@ -91,7 +105,7 @@ __global__ __launch_bounds__(kDecWaves * 64) void decode_bf16_kernel(DecodeParam
       int voff = 0;
       if (k0 < kv_len) {
         const int pidx = k0 / P;
-        const int page = load_const(p.page_ids, rq.page0 + pidx);
+        const int page = tp.id[i];
         const int valid = min(P, kv_len - pidx * P);  // tokens held by this page
         const int64_t pbase = ((int64_t)page * P * Hkv + kvh) * D;
         const int bytes = (int)(((int64_t)(valid - 1) * row_el + D) * 2);
@@ -148,11 +162,16 @@ __global__ __launch_bounds__(kDecWaves * 64) void decode_bf16_kernel(DecodeParam
   // Tiles tile0 + wave, + 4, ... ; the copy of the next one overlaps this one.
   int stage = 0;
   int t = w.tile0 + wave;
-  if (t < w.tile1) issue_tile(t, 0);
+  TilePages next{};
+  if (t < w.tile1) {
+    issue_tile(t, tile_pages(t), 0);
+    next = tile_pages(t + kDecWaves);
+  }
   for (; t < w.tile1; t += kDecWaves) {
     const int tn = t + kDecWaves;
     if (tn < w.tile1) {
-      issue_tile(tn, stage ^ 1);
+      issue_tile(tn, next, stage ^ 1);
+      next = tile_pages(tn + kDecWaves);
       wait_vmcnt<2 * NI>();
     } else {
       wait_vmcnt<0>();
