@@ -857,7 +857,7 @@ struct cas_pool {
   std::vector<size_t> hoff;
   char *dev = nullptr;
   size_t A = 0, M = 0, slot_bytes = 0;       // bf16 tensor, fp32 tensor, slot
-  std::vector<int32_t> steps, slot_of, slot_cart, active, staging, next_admit;
+  std::vector<int32_t> steps, slot_cart, active, staging, next_admit;   // slot_cart: cartridge in each slot or -1
   int64_t step_count = 0;
   bool loaded = false;
   hipStream_t side = nullptr;
@@ -1027,7 +1027,6 @@ cas_status_t cas_pool_load(cas_pool_t *p, void *compute_stream) {
   std::vector<int> order(p->N);
   for (int c = 0; c < p->N; ++c) order[c] = c;
   std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return p->steps[a] < p->steps[b]; });
-  p->slot_of.assign(p->N, -1);
   p->active.clear();
   p->staging.clear();
   for (int i = 0; i < p->B; ++i) {
