@@ -112,6 +112,9 @@ def main():
                     help="time training steps (packed attention fwd+bwd, Adam) through the budget manager")
     ap.add_argument("--cpu-heads", type=int, default=16, help="oracle heads timed for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--mfma-counters", default=os.path.join(ROOT, "profiles", "mfma_util_16x2k.json"),
+                    help="JSON of rocprofv3 MFMA counters per launch (executed MFMA work, MFMA busy cycles, "
+                         "clock); used only while the kernel sources still hash to the value recorded in it")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "hbm_traffic_16x2k.json"),
                     help="JSON of calibrated rocprofv3 FETCH_SIZE/WRITE_SIZE bytes per launch; used only "
                          "while the kernel sources still hash to the value recorded in it")
@@ -223,6 +226,23 @@ def main():
                 "avg_launch_ms": avg_ms,
                 "flops_per_launch": wl.flops(per_pair) if per_pair else None}
     kernels = {k: {"launches": n, "avg_ms": t / n} for k, (n, t) in ktimes.items()}
+    # MFMA utilisation: the MFMA work each launch executes (counted by
+    # SQ_INSTS_VALU_MFMA_MOPS_BF16, recompute and masked tile parts included)
+    # over this run's live launch time, against the dense bf16 peak; and the
+    # MFMA busy share of the SIMD cycles at the clock the counter run saw.
+    mfma_util = None
+    if args.mfma_counters and os.path.exists(args.mfma_counters) and args.config == 3 and not args.packed:
+        with open(args.mfma_counters) as fh:
+            rec = json.load(fh)
+        if rec.get("source_sha256_16") == kernel_source_hash():
+            mfma_util = {}
+            for k, c in rec["kernels"].items():
+                if k in kernels:
+                    live = c["executed_tflop"] / (kernels[k]["avg_ms"] * 1e-3)
+                    mfma_util[k] = {"executed_tflop_per_launch": c["executed_tflop"],
+                                    "executed_tflops": live, "frac_of_peak": live / peak,
+                                    "busy_frac_at_clock": c["mfma_busy_frac"],
+                                    "clock_ghz": c["clock_ghz"]}
 
     out = {
         "metric": METRIC,
@@ -252,6 +272,7 @@ def main():
         "query_tokens_per_s": sum(wl.row_lens) / (ms * 1e-3),
         "kernels": kernels,
         "roofline": roofline,
+        "mfma_util": mfma_util,
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:
