@@ -562,19 +562,44 @@ void fwd_bf16_kernel(FwdParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// dQ (query-stationary).
+// dQ (query-stationary): ping-pong between the two waves of each SIMD.
+//
+// The key axis is walked in 32-key units (half tiles of the tile table). Per
+// unit u a wave runs a matrix phase G_u (dQ^T += K_{u-1}^T dS_{u-1}^T, then
+// S_u^T = K_u Q^T and dP_u^T = V_u dO^T: 24 MFMAs for d = 128 in one
+// scheduling region) and a VALU phase X_u (P = exp2(S c - LSE2), masks,
+// dS = P (dP - D), bf16 packing of dS). Waves 0-3 (group A) run G_u while
+// waves 4-7 (group B) run X_{u-1}, and the other way round in the next phase;
+// every phase ends in a workgroup barrier, so on each SIMD one wave's MFMA
+// stream runs beside the other wave's VALU work. (32-key units keep the
+// scores, dP and dS of one unit within the 256 registers of a wave that
+// shares its SIMD.)
+//
+// LDS: four K and four V unit buffers, unit u in buffer u % 4. K_u is read by
+// G_u and G_{u+1} (up to phase 2u+3), V_u by G_u (up to phase 2u+1). Only
+// group B copies: at the start of phase 2u (a VALU phase for it) it issues
+// unit u+2 into the buffers unit u-2 left free, and at the end of phase 2u it
+// waits for unit u+1, which G_{u+1} reads from phase 2u+2 on.
 // ---------------------------------------------------------------------------
+constexpr int kDqUnit = 32;   // keys per dQ unit
+
 template <int D>
-__global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
+__global__ __launch_bounds__(kFastThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void dq_bf16_kernel(DqParams p) {
   constexpr int NSTEP = D / 16;
   constexpr int DT = D / 32;
-  constexpr int TB = kKT * D * 2;
-  __shared__ __attribute__((aligned(1024))) char kb0[TB];
-  __shared__ __attribute__((aligned(1024))) char vb0[TB];
-  __shared__ __attribute__((aligned(1024))) char kb1[TB];
-  __shared__ __attribute__((aligned(1024))) char vb1[TB];
+  constexpr int UB = kDqUnit * D * 2;   // bytes per unit buffer
+  __shared__ __attribute__((aligned(1024))) char kb0[UB];
+  __shared__ __attribute__((aligned(1024))) char kb1[UB];
+  __shared__ __attribute__((aligned(1024))) char kb2[UB];
+  __shared__ __attribute__((aligned(1024))) char kb3[UB];
+  __shared__ __attribute__((aligned(1024))) char vb0[UB];
+  __shared__ __attribute__((aligned(1024))) char vb1[UB];
+  __shared__ __attribute__((aligned(1024))) char vb2[UB];
+  __shared__ __attribute__((aligned(1024))) char vb3[UB];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2;
   const int G = lane >> 5, n = lane & 31;
   // Logical order: row block fastest, then split, batch row, KV head (the
   // KV heads split the XCDs evenly whatever the rows' lengths).
@@ -627,6 +652,10 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
       df[st] = Mma<__bf16>::zero();
     }
   }
+  // Unit copies are waited for with partial vmcnt counts, which must not
+  // include these loads.
+  wait_vmcnt<0>();
+
   f32x16 acc[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) acc[dt] = zero16();
@@ -635,95 +664,227 @@ __global__ __launch_bounds__(kFastThreads) void dq_bf16_kernel(DqParams p) {
   const int ntiles = ptiles + wg_t_hi / kKT + 1;
   const int tb = __builtin_amdgcn_readfirstlane((int)((int64_t)ntiles * split / p.splits));
   const int te = __builtin_amdgcn_readfirstlane((int)((int64_t)ntiles * (split + 1) / p.splits));
+  const int nu = 2 * (te - tb);   // units of this split
   TileTable tt;
   tt.init(p.tiles, row, kvh);
 
-  // Tile copies, issued piece by piece inside the previous tile's compute
-  // (a burst of copy instructions would stall the issuing wave): piece n is
-  // K instruction n (n < PER) or V instruction n - PER.
-  CopyLanes<D, kKT, kNW> cl;
-  cl.init(wave, lane);
-  constexpr int PER = CopyLanes<D, kKT, kNW>::PER;
-  auto piece = [&](const TileInfo &ti, char *kb, char *vb, int n) __attribute__((always_inline)) {
-    if (n < PER) cl.issue_one(kb, ti.kp, ti.st, ti.nvalid, wave, n);
-    else cl.issue_one(vb, ti.vp, ti.st, ti.nvalid, wave, n - PER);
+  // Unit u: half u % 2 of local tile u / 2.
+  struct Unit {
+    const __bf16 *kp, *vp;
+    int st, nvalid, self0;   // nvalid <= 0: no keys
   };
-  auto issue = [&](const TileInfo &ti, char *kb, char *vb) __attribute__((always_inline)) {
-#pragma unroll
-    for (int n = 0; n < 2 * PER; ++n) piece(ti, kb, vb, n);
+  auto unit_at = [&](int u) __attribute__((always_inline)) {
+    const TileInfo t = tt.at(tb + (u >> 1));
+    const int hk = (u & 1) * kDqUnit;
+    Unit x;
+    x.kp = t.kp + (int64_t)hk * t.st;
+    x.vp = t.vp + (int64_t)hk * t.st;
+    x.st = t.st;
+    x.nvalid = min(kDqUnit, t.nvalid - hk);
+    x.self0 = t.self0 < 0 ? -1 : t.self0 + hk;
+    return x;
   };
 
-  // compute(ti, ...) issues copy pieces 2h and 2h+1 of the next tile after
-  // half h's score products; with no next tile, or when this wave skips the
-  // tile, the pieces go first.
-  auto compute = [&](const TileInfo &ti, const char *kb, const char *vb, auto &&next) __attribute__((always_inline)) {
-    static_assert(2 * PER <= 4, "at most four copy pieces per tile");
-    auto at = [&](int point) __attribute__((always_inline)) {
-      if (point < 2 * PER) next(point);
-    };
-    if (!wave_active || (ti.self0 >= 0 && ti.self0 > wave_t_hi)) {
+  // Group B's share of every unit copy (4 waves): instruction k of a K or V
+  // unit moves rows cr0 + RSTEP k (16 bytes per lane, swizzled chunk ccol);
+  // the swizzle repeats every 16 rows, so one row and one chunk offset per
+  // lane serve every instruction. Rows past nvalid re-read row nvalid-1
+  // (masked later); a unit without keys goes through an empty resource.
+  constexpr int CPR = D / 8;                                 // 16-byte chunks per row
+  constexpr int kCopyInst = kDqUnit * CPR / 64 / 4;          // per wave per K or V unit
+  constexpr int RSTEP = 4 * 64 / CPR;                        // rows between a wave's instructions
+  constexpr int kPieces = 2 * kCopyInst;                     // copy instructions per VALU phase
+  static_assert(kCopyInst >= 1 && kDqUnit * CPR == kCopyInst * 4 * 64, "unit copies split evenly");
+  static_assert(RSTEP % 16 == 0, "swizzle period divides the row step");
+  static_assert(16 % kPieces == 0, "copy pieces spread over the 16 exponentials");
+  const int cpos = (wave & 3) * 64 + lane;
+  const int cr0 = cpos / CPR;
+  const int ccol = ((cpos % CPR) ^ swz<D>(cr0)) * 8;
+  auto copy_one = [&](char *buf, const BufRsrc &rs, const Unit &x, int k) __attribute__((always_inline)) {
+    dma16(rs, (min(cr0 + RSTEP * k, max(x.nvalid, 1) - 1) * x.st + ccol) * 2, buf + ((wave & 3) + 4 * k) * 1024);
+  };
+  auto unit_bytes = [&](const Unit &x, bool has) __attribute__((always_inline)) {
+    return (has && x.nvalid > 0) ? ((x.nvalid - 1) * x.st + D) * 2 : 0;
+  };
+
+  // S^T and dP^T of the unit between its G and X phases; dS^T of the unit
+  // (bf16, per 16-key step) between its X phase and the next G phase.
+  f32x16 sa = zero16(), dpa = zero16();
+  bf16x8 dsf[2];
 #pragma unroll
-      for (int n = 0; n < 2 * PER; ++n) next(n);
+  for (int s = 0; s < 2; ++s) dsf[s] = Mma<__bf16>::zero();
+
+  // Matrix phase as one software-pipelined MFMA sequence: dQ^T of the previous
+  // unit (2*DT MFMAs, K^T fragments by two transposed LDS reads each), then
+  // S^T and dP^T of this unit (2*NSTEP MFMAs, one row read each). The fragment
+  // of MFMA k+LEAD is read while MFMA k runs, into a ring of LEAD+1 registers.
+  auto matrix = [&](const char *kbp, const char *kb, const char *vb) __attribute__((always_inline)) {
+    constexpr int NQ = 2 * DT;
+    constexpr int N = NQ + 2 * NSTEP;
+    constexpr int LEAD = 4, R = LEAD + 1;
+    // MFMA k < NQ: 16-key step s = k / DT, dt = k % DT.
+    // MFMA k >= NQ: st = (k - NQ) / 2; S (even) or dP (odd).
+    auto load = [&](auto K) __attribute__((always_inline)) {
+      constexpr int k = decltype(K)::value;
+      if constexpr (k < NQ) {
+        return tr_frag_at<D>(kbp, to, 16 * (k / DT), k % DT);
+      } else {
+        constexpr int st = (k - NQ) / 2;
+        if constexpr ((k - NQ) % 2 == 0) return row_frag_at<D>(kb, ro, 0, st);
+        else return row_frag_at<D>(vb, ro, 0, st);
+      }
+    };
+    auto mma = [&](auto K, const bf16x8 &f) __attribute__((always_inline)) {
+      constexpr int k = decltype(K)::value;
+      if constexpr (k < NQ) {
+        acc[k % DT] = Mma<__bf16>::run(f, dsf[k / DT], acc[k % DT]);
+      } else {
+        // The first step starts from an inline zero accumulator.
+        constexpr int st = (k - NQ) / 2;
+        if constexpr ((k - NQ) % 2 == 0) sa = Mma<__bf16>::run(f, qf[st], st == 0 ? zero16() : sa);
+        else dpa = Mma<__bf16>::run(f, df[st], st == 0 ? zero16() : dpa);
+      }
+    };
+    bf16x8 ring[R];
+    static_for<LEAD>([&](auto K) __attribute__((always_inline)) {
+      constexpr int k = decltype(K)::value;
+      if constexpr (k < N) ring[k % R] = load(K);
+    });
+    static_for<N>([&](auto K) __attribute__((always_inline)) {
+      constexpr int k = decltype(K)::value;
+      if constexpr (k + LEAD < N) ring[(k + LEAD) % R] = load(std::integral_constant<int, k + LEAD>{});
+      mma(K, ring[k % R]);
+    });
+    static_for<LEAD>([&](auto K) __attribute__((always_inline)) {
+      constexpr int k = decltype(K)::value;
+      if constexpr (k < N) sched_ds_read<(k < NQ ? 2 : 1)>();
+    });
+    static_for<N>([&](auto K) __attribute__((always_inline)) {
+      constexpr int k = decltype(K)::value;
+      sched_mfma<1>();
+      if constexpr (k + LEAD < N) sched_ds_read<(k + LEAD < NQ ? 2 : 1)>();
+    });
+  };
+
+  // VALU phase of a live unit; piece(n), n < kPieces: copy instruction n of
+  // the phase, spread evenly over the exponentials.
+  auto dsoft = [&](auto MASK, int lim, auto &&piece) __attribute__((always_inline)) {
+    if constexpr (decltype(MASK)::value) {
+      // lim: last visible key of this lane's query within the unit (negative:
+      // none). Register j of lane group G holds key crow(j, 0) + 4G.
+      const int limg = lim - 4 * G;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) sa[j] = crow(j, 0) <= limg ? sa[j] : -INFINITY;
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      // dP accumulated from zero: dS = P (dP - D) with -D added here.
+      sa[j] = fast_exp2(fmaf(sa[j], c, -lse2r)) * (dpa[j] + ndr);
+      constexpr int EPP = 16 / kPieces;
+      if (j % EPP == EPP - 1) {
+        asm volatile("" : "+v"(sa[j]));   // keep the copies spread
+        piece(j / EPP);
+      }
+      if (j % 8 == 7) dsf[j / 8] = pack_bf16x8(sa, j / 8);
+    }
+  };
+
+  auto gphase = [&](int u, const char *kbp, const char *kb, const char *vb) __attribute__((always_inline)) {
+    if (u <= nu && wave_active) matrix(kbp, kb, vb);
+  };
+  auto xphase = [&](int u, auto &&piece) __attribute__((always_inline)) {
+    auto all_pieces = [&]() __attribute__((always_inline)) {
+#pragma unroll
+      for (int k = 0; k < kPieces; ++k) piece(k);
+    };
+    if (u < 0 || u >= nu) {
+      all_pieces();
       return;
     }
-    const bool need_mask = (ti.nvalid < kKT) || (ti.self0 >= 0 && ti.self0 + kKT - 1 > wave_t_lo);
+    const Unit x = unit_at(u);
+    if (!wave_active || x.nvalid <= 0 || (x.self0 >= 0 && x.self0 > wave_t_hi)) {
 #pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      // dP accumulates onto -D, so the MFMAs deliver dP - D.
-      f32x16 sa = zero16(), dpa;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) dpa[j] = ndr;
-#pragma unroll
-      for (int st = 0; st < NSTEP; ++st) {
-        sa = Mma<__bf16>::run(row_frag_at<D>(kb, ro, 32 * sub, st), qf[st], sa);
-        dpa = Mma<__bf16>::run(row_frag_at<D>(vb, ro, 32 * sub, st), df[st], dpa);
-      }
-      at(2 * sub);
-      at(2 * sub + 1);
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        float pv = fast_exp2(fmaf(sa[j], c, -lse2r));
-        if (need_mask) {
-          const int key = 32 * sub + crow(j, G);
-          const bool ok = key < ti.nvalid && (ti.self0 < 0 || ti.self0 + key <= my_t);
-          pv = ok ? pv : 0.0f;
-        }
-        sa[j] = pv * dpa[j];
-      }
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        const bf16x8 dsf = pack_bf16x8(sa, s);
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-          acc[dt] = Mma<__bf16>::run(tr_frag_at<D>(kb, to, 32 * sub + 16 * s, dt), dsf, acc[dt]);
-      }
+      for (int s = 0; s < 2; ++s) dsf[s] = Mma<__bf16>::zero();
+      all_pieces();
+      return;
+    }
+    if (x.nvalid < kDqUnit || (x.self0 >= 0 && x.self0 + kDqUnit - 1 > wave_t_lo)) {
+      const int lim = x.self0 < 0 ? x.nvalid - 1 : min(x.nvalid - 1, my_t - x.self0);
+      dsoft(std::true_type{}, lim, piece);
+    } else {
+      dsoft(std::false_type{}, kDqUnit - 1, piece);
     }
   };
+  auto no_piece = [](int) {};
 
-  if (tb < te) {
-    TileInfo cur = tt.at(tb);
-    issue(cur, kb0, vb0);
-    __syncthreads();
-    for (int it = tb; it < te; it += 2) {
-      // compute runs unconditionally (a branch around it would make the
-      // register allocator copy the accumulators); only the copies are
-      // conditional.
-      TileInfo nxt;
-      const bool has1 = it + 1 < te;
-      if (has1) nxt = tt.at(it + 1);
-      compute(cur, kb0, vb0, [&](int n) __attribute__((always_inline)) {
-        if (has1) piece(nxt, kb1, vb1, n);
-      });
-      __syncthreads();
-      if (!has1) break;
-      const bool has2 = it + 2 < te;
-      const TileInfo prev = nxt;
-      if (has2) cur = tt.at(it + 2);
-      compute(prev, kb1, vb1, [&](int n) __attribute__((always_inline)) {
-        if (has2) piece(cur, kb0, vb0, n);
-      });
-      __syncthreads();
+  auto issue_unit = [&](int u, char *kbn, char *vbn) __attribute__((always_inline)) {
+    const Unit x = unit_at(u);
+    const int bytes = unit_bytes(x, true);
+    const BufRsrc rk = make_rsrc(x.kp, bytes), rv = make_rsrc(x.vp, bytes);
+#pragma unroll
+    for (int k = 0; k < kCopyInst; ++k) copy_one(kbn, rk, x, k);
+#pragma unroll
+    for (int k = 0; k < kCopyInst; ++k) copy_one(vbn, rv, x, k);
+  };
+  // Phase 2u for group B: unit u+2 (through empty resources past the last
+  // unit: zeros into buffers that only G_nu's unused products read) spread
+  // over X_{u-1}; then wait for unit u+1.
+  auto even_b = [&](int u, char *kbn, char *vbn) __attribute__((always_inline)) {
+    const Unit x = unit_at(min(u + 2, nu - 1));
+    const int bytes = unit_bytes(x, u + 2 < nu);
+    const BufRsrc rk = make_rsrc(x.kp, bytes), rv = make_rsrc(x.vp, bytes);
+    xphase(u - 1, [&](int k) __attribute__((always_inline)) {
+      if (k < kCopyInst) copy_one(kbn, rk, x, k);
+      else copy_one(vbn, rv, x, k - kCopyInst);
+    });
+    wait_vmcnt<kPieces>();
+  };
+
+  if (nu > 0) {
+    // G_0 multiplies K buffer 3 by dS = 0: clear it so no stale bit pattern
+    // (a NaN) can reach dQ.
+    for (int i = tid; i < UB / 16; i += kFastThreads) reinterpret_cast<uint4 *>(kb3)[i] = uint4{0, 0, 0, 0};
+    // Prologue (group B): unit 0, then unit 1 (nu is even, so it exists).
+    if (grp == 1) {
+      issue_unit(0, kb0, vb0);
+      wait_vmcnt<0>();
+      issue_unit(1, kb1, vb1);
     }
+    lds_barrier();
+    // Eight phases per iteration (four units), so every buffer is a fixed LDS
+    // address: G_u reads K_{u-1}, K_u and V_u from buffers (u-1)%4 and u%4;
+    // the copies of phase 2u go to buffers (u+2)%4. Each group runs its own
+    // copy of the loop (straight-line phases); s_barrier pairs them.
+    auto run = [&](auto GROUP_A) __attribute__((always_inline)) {
+      constexpr bool A = decltype(GROUP_A)::value;
+      auto even = [&](int u, const char *kbp, const char *kbi, const char *vbi, char *kbn, char *vbn)
+                      __attribute__((always_inline)) {
+        if constexpr (A) gphase(u, kbp, kbi, vbi);
+        else even_b(u, kbn, vbn);
+        lds_barrier();
+      };
+      auto odd = [&](int u, const char *kbp, const char *kbi, const char *vbi) __attribute__((always_inline)) {
+        if constexpr (A) xphase(u, no_piece);
+        else gphase(u, kbp, kbi, vbi);
+        lds_barrier();
+      };
+      for (int u = 0; u <= nu; u += 4) {
+        even(u, kb3, kb0, vb0, kb2, vb2);
+        odd(u, kb3, kb0, vb0);
+        if (u + 1 > nu) break;
+        even(u + 1, kb0, kb1, vb1, kb3, vb3);
+        odd(u + 1, kb0, kb1, vb1);
+        if (u + 2 > nu) break;
+        even(u + 2, kb1, kb2, vb2, kb0, vb0);
+        odd(u + 2, kb1, kb2, vb2);
+        if (u + 3 > nu) break;
+        even(u + 3, kb2, kb3, vb3, kb1, vb1);
+        odd(u + 3, kb2, kb3, vb3);
+      }
+    };
+    if (grp == 0) run(std::true_type{});
+    else run(std::false_type{});
+    wait_vmcnt<0>();
   }
 
   if (my_row >= nrows) return;
