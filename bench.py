@@ -110,6 +110,9 @@ def main():
                     help="time one paged decode step of the retrieval mix (64 requests x 4 cartridges)")
     ap.add_argument("--pool", action="store_true",
                     help="time training steps (packed attention fwd+bwd, Adam) through the budget manager")
+    ap.add_argument("--stage", action="store_true",
+                    help="time the forward-only retrieval mix with the pool's second half staged "
+                         "host->HBM (cas_cartridge_stage) on a side stream, overlapped with compute")
     ap.add_argument("--cpu-heads", type=int, default=16, help="oracle heads timed for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mfma-counters", default=os.path.join(ROOT, "profiles", "mfma_util_16x2k.json"),
@@ -149,6 +152,8 @@ def main():
         return run_decode(args)
     if args.pool:
         return run_pool(args)
+    if args.stage:
+        return run_stage(args)
     wl = casgen.packed() if args.packed else casgen.config(args.config)
     if wl.forward_only:
         print("bench.py times forward+backward; pick config 1-4", file=sys.stderr)
@@ -450,6 +455,163 @@ def run_decode(args):
         el = time.perf_counter() - t0
         out["cpu_baseline"] = {"value": sum(kv_lens[:8]) * Hkv * D * 4 / el / 1e9, "unit": "GB/s", "cores": 1,
                                "kind": "oracle", "sample": f"8 of the 64 requests, {el:.1f} s"}
+    print(json.dumps(out), flush=True)
+
+
+def run_stage(args):
+    """The forward-only retrieval-selected inference mix with cartridge
+    staging: 64 requests of 64 causal queries (32 query / 8 KV heads x 128,
+    bf16), each over its 4 seeded selections from a pool of 256 cartridges of
+    1,024 tokens. Cartridges 0-127 are resident in HBM; 128-255 sit in pinned
+    host memory and are staged inside the timed region by cas_cartridge_stage
+    on a side stream, in 8 chunks of 16 cartridges (K and V, 64 MiB per chunk)
+    with one event each. Requests are grouped by the last chunk they need and
+    launched in that order: the resident-only group at once, every other group
+    after its chunk's event. Reported: the wall time of the whole mix, the
+    staging alone (GB/s against the host link), the compute alone, and the
+    overlap (t_copy + t_compute - t_wall) / min(t_copy, t_compute)."""
+    import ctypes
+    import numpy as np
+    import torch
+    import casgen
+    import paper_2606_04557_amd as cas
+    wl = casgen.config(5)
+    pool, L = len(wl.cart_lens), wl.cart_lens[0]
+    half, chunk = pool // 2, 16
+    B, Sq, Hq, Hkv, D, g = wl.batch, wl.q_len, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.group_size
+    used = sorted({c for r in wl.rows for c in r})
+    log(f"generating {wl.name}: {wl.description} ({len(used)} cartridges selected)")
+    T = casgen.make_tensors(wl, carts=used)
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16)
+
+    kdev = torch.zeros((pool, L, Hkv, D), dtype=torch.bfloat16, device="cuda")
+    vdev = torch.zeros_like(kdev)
+    khost = torch.zeros((pool - half, L, Hkv, D), dtype=torch.bfloat16).pin_memory()
+    vhost = torch.zeros_like(khost).pin_memory()
+    for c in used:
+        if c < half:
+            kdev[c].copy_(bf(T["cart_k"][c]))
+            vdev[c].copy_(bf(T["cart_v"][c]))
+        else:
+            khost[c - half].copy_(bf(T["cart_k"][c]))
+            vhost[c - half].copy_(bf(T["cart_v"][c]))
+    # Requests ordered by the last staged chunk they need (-1: resident only).
+    need = [max([(c - half) // chunk for c in r if c >= half], default=-1) for r in wl.rows]
+    order = sorted(range(B), key=lambda r: need[r])
+    q = bf(T["q"][order]).cuda()
+    ks = bf(T["k_self"][order]).cuda()
+    vs = bf(T["v_self"][order]).cuda()
+    o = torch.empty_like(q)
+    lse = torch.empty((B, Hq, Sq), dtype=torch.float32, device="cuda")
+    scale = float(wl.scale)
+    lib = cas.load()
+    groups = []   # (chunk waited for, problem, first row, last row, workspace)
+    r0 = 0
+    while r0 < B:
+        r1 = r0
+        while r1 < B and need[order[r1]] == need[order[r0]]:
+            r1 += 1
+        rows = [[cas.Segment(kdev[c], vdev[c]) for c in wl.rows[order[r]]] for r in range(r0, r1)]
+        prob = cas.Problem.from_tensors(q[r0:r1], rows, Hkv, g, scale, None)
+        ws = torch.empty(max(cas.workspace_size(prob, False), 1), dtype=torch.uint8, device="cuda")
+        groups.append((need[order[r0]], prob, r0, r1, ws, rows))
+        r0 = r1
+    compute = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    hs = cas._stream_handle(q.device, None)
+    nchunks = (pool - half) // chunk
+    copies = []
+    for ci in range(nchunks):
+        arr = (cas._lib.StageCopy * (2 * chunk))()
+        for j in range(chunk):
+            c = ci * chunk + j
+            for m, (h, d) in enumerate(((khost[c], kdev[half + c]), (vhost[c], vdev[half + c]))):
+                e = arr[2 * j + m]
+                e.host_src, e.dev_dst, e.bytes = h.data_ptr(), d.data_ptr(), h.numel() * 2
+        copies.append(arr)
+    stage_bytes = (pool - half) * 2 * L * Hkv * D * 2
+    events = [torch.cuda.Event() for _ in range(nchunks)]
+    for e in events:
+        e.record(side)   # torch creates its events lazily
+
+    def launch(gr):
+        _, prob, a, b_, ws, _ = gr
+        o_, lse_ = o[a:b_], lse[a:b_]
+        cas._check(lib.cas_prefix_attn_fwd(ctypes.byref(prob.c), q[a:b_].data_ptr(), ks[a:b_].data_ptr(),
+                                           vs[a:b_].data_ptr(), o_.data_ptr(), lse_.data_ptr(),
+                                           ws.data_ptr(), ws.numel(), hs))
+
+    def stage_all():
+        for ci in range(nchunks):
+            cas._check(lib.cas_cartridge_stage(ctypes.cast(copies[ci], ctypes.POINTER(cas._lib.StageCopy)),
+                                               2 * chunk, side.cuda_stream, events[ci].cuda_event))
+
+    def wall():
+        side.wait_stream(compute)
+        stage_all()
+        for gr in groups:
+            if gr[0] >= 0:
+                compute.wait_event(events[gr[0]])
+            launch(gr)
+
+    def timed(fn):
+        # Both streams start after t0 and t1 follows both (the side stream's
+        # copies are joined into the compute stream before t1).
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0.record(compute)
+        fn()
+        compute.wait_stream(side)
+        t1.record(compute)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1)
+
+    def compute_only():
+        for gr in groups:
+            launch(gr)
+
+    def copy_only():
+        side.wait_stream(compute)
+        stage_all()
+
+    for _ in range(args.warmup):
+        timed(wall)
+    cas.timing_reset()
+    cas.timing_enable(True)
+    t_comp = sorted(timed(compute_only) for _ in range(args.steps))
+    cas.timing_enable(False)
+    kt = cas.timing_read()
+    t_copy = sorted(timed(copy_only) for _ in range(args.steps))
+    t_wall = sorted(timed(wall) for _ in range(args.steps))
+    med = lambda v: v[len(v) // 2]
+    tc, tx, tw = med(t_comp), med(t_copy), med(t_wall)
+    flops = wl.flops(4)
+    fwd_n, fwd_ms = kt["fwd"]
+    achieved = flops * args.steps / (fwd_ms * 1e-3) / 1e12
+    out = {
+        "metric": "retrieval inference mix: forward TFLOP/s with host->HBM cartridge staging overlapped "
+                  "(64 requests x 4 of 256 1K-token cartridges)",
+        "value": flops / (tw * 1e-3) / 1e12, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": tw, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded Gaussian Q/K/V; seeded retrieval selection)",
+        "config": {"workload": f"{wl.name}: {wl.description}", "requests": B, "q_len": Sq,
+                   "num_q_heads": Hq, "num_kv_heads": Hkv, "head_dim": D, "pool": pool,
+                   "staged_cartridges": pool - half, "chunks": nchunks, "launch_groups": len(groups),
+                   "parallelism": "single GPU"},
+        "t_wall_ms": tw, "t_compute_ms": tc, "t_copy_ms": tx,
+        "t_wall_ms_p10_p90": [t_wall[len(t_wall) // 10], t_wall[(9 * len(t_wall)) // 10]],
+        "staging_gb_s": stage_bytes / (tx * 1e-3) / 1e9, "staging_bytes": stage_bytes,
+        "overlap": (tx + tc - tw) / min(tx, tc),
+        "compute_tflops": flops / (tc * 1e-3) / 1e12,
+        "kernels": {k: {"launches": c, "avg_ms": t / c} for k, (c, t) in kt.items()},
+        "roofline": {"bound": "mfma", "kernel": "fwd", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "avg_launch_ms": fwd_ms / fwd_n, "flops_per_launch": flops * args.steps / fwd_n},
+        "cpu_baseline": None,
+    }
     print(json.dumps(out), flush=True)
 
 
