@@ -524,12 +524,14 @@ def run_stage(args):
     nchunks = (pool - half) // chunk
     copies = []
     for ci in range(nchunks):
+        # K of the chunk's 16 cartridges, then their V: address order in both
+        # pools, so the library moves each as one transfer.
         arr = (cas._lib.StageCopy * (2 * chunk))()
-        for j in range(chunk):
-            c = ci * chunk + j
-            for m, (h, d) in enumerate(((khost[c], kdev[half + c]), (vhost[c], vdev[half + c]))):
-                e = arr[2 * j + m]
-                e.host_src, e.dev_dst, e.bytes = h.data_ptr(), d.data_ptr(), h.numel() * 2
+        for m, (hp, dp) in enumerate(((khost, kdev), (vhost, vdev))):
+            for j in range(chunk):
+                c = ci * chunk + j
+                e = arr[m * chunk + j]
+                e.host_src, e.dev_dst, e.bytes = hp[c].data_ptr(), dp[half + c].data_ptr(), hp[c].numel() * 2
         copies.append(arr)
     stage_bytes = (pool - half) * 2 * L * Hkv * D * 2
     events = [torch.cuda.Event() for _ in range(nchunks)]

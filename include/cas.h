@@ -169,6 +169,9 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
  * pinned (page-locked) host memory, else CAS_ERR_NOT_PINNED and nothing is
  * enqueued: a pageable copy would silently serialise with the host. The
  * caller keeps host_src alive and unmodified until the event completes.
+ * Consecutive entries whose source and destination both continue the
+ * previous entry's are moved as one transfer (list a pool's cartridges in
+ * address order to get large transfers); copies run in the given order.
  */
 typedef struct {
   const void *host_src;

@@ -251,3 +251,30 @@ def test_c5_forward_with_staging():
     with pytest.raises(cas.CasError) as ei:
         cas.cartridge_stage([(src, dst)], side)
     assert "CAS_ERR_NOT_PINNED" in str(ei.value)
+
+
+def test_stage_contiguous_and_scattered_copies():
+    """cas_cartridge_stage moves runs of address-contiguous entries as one
+    transfer: a list mixing such runs, gaps, zero-byte entries and a reversed
+    order must still land every byte where its entry says."""
+    import torch
+    import paper_2606_04557_amd as cas
+    n = 1 << 16
+    host = torch.arange(8 * n, dtype=torch.int32).pin_memory()
+    dev = torch.full((10 * n,), -1, dtype=torch.int32, device="cuda")
+    pieces = [(0, 0), (1, 1), (2, 2),          # one contiguous run
+              (3, 5), (4, 6),                  # a second run after a gap in the destination
+              (6, 3), (5, 4),                  # reversed: two transfers
+              (7, 9)]
+    copies = [(host[s * n:(s + 1) * n], dev[d * n:(d + 1) * n]) for s, d in pieces]
+    copies.insert(3, (host[:0], dev[:0]))      # a zero-byte entry inside the list
+    side = torch.cuda.Stream()
+    ev = torch.cuda.Event()
+    torch.cuda.synchronize()
+    cas.cartridge_stage(copies, side, ev)
+    torch.cuda.current_stream().wait_event(ev)
+    got = dev.cpu()
+    want = torch.full((10 * n,), -1, dtype=torch.int32)
+    for s, d in pieces:
+        want[d * n:(d + 1) * n] = host[s * n:(s + 1) * n]
+    assert torch.equal(got, want)
