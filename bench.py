@@ -113,6 +113,9 @@ def main():
     ap.add_argument("--stage", action="store_true",
                     help="time the forward-only retrieval mix with the pool's second half staged "
                          "host->HBM (cas_cartridge_stage) on a side stream, overlapped with compute")
+    ap.add_argument("--no-dist", action="store_true",
+                    help="skip the per-step warm/cold distribution runs after the timed region "
+                         "(profiler passes: keeps every dispatch of a kernel alike)")
     ap.add_argument("--cpu-heads", type=int, default=16, help="oracle heads timed for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mfma-counters", default=os.path.join(ROOT, "profiles", "mfma_util_16x2k.json"),
@@ -213,6 +216,30 @@ def main():
     value = flops_step / (ms * 1e-3) / 1e12
     log("kernel times", ktimes)
 
+    # Per-step distribution (HIP events around each step on the launch
+    # stream), warm and cold: before each cold step a 1 GiB buffer is
+    # rewritten, more than the 256 MiB Infinity Cache and the L2s, so the
+    # step starts from HBM. Both run after the timed region above.
+    def per_step(cold: bool):
+        scrub = torch.empty(1 << 28, dtype=torch.float32, device="cuda") if cold else None
+        out = []
+        for i in range(args.steps):
+            if cold:
+                scrub.fill_(float(i))
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            step()
+            b.record()
+            b.synchronize()
+            out.append(a.elapsed_time(b))
+        out.sort()
+        return [out[len(out) // 10], out[len(out) // 2], out[(9 * len(out)) // 10]]
+
+    warm_dist = cold_dist = None
+    if not args.no_dist:
+        warm_dist, cold_dist = per_step(False), per_step(True)
+        log("per-step ms p10/p50/p90 warm", warm_dist, "cold", cold_dist)
+
     # Dominant kernel: the one with the largest total time in the timed region.
     dom = max(ktimes, key=lambda k: ktimes[k][1])
     launches, total = ktimes[dom]
@@ -275,6 +302,9 @@ def main():
         "mfma_frac_of_step": value / peak,
         "tflops_fa14": wl.flops(14) / (ms * 1e-3) / 1e12,
         "query_tokens_per_s": sum(wl.row_lens) / (ms * 1e-3),
+        "kv_tokens_per_s": sum(wl.prefix_len(b) + wl.row_lens[b] for b in range(wl.batch)) / (ms * 1e-3),
+        "step_ms_p10_p50_p90": warm_dist,
+        "cold_step_ms_p10_p50_p90": cold_dist,
         "kernels": kernels,
         "roofline": roofline,
         "mfma_util": mfma_util,

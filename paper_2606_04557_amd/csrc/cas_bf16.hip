@@ -48,11 +48,6 @@ __device__ __forceinline__ void sched_mfma() { __builtin_amdgcn_sched_group_barr
 template <int N>
 __device__ __forceinline__ void sched_ds_read() { __builtin_amdgcn_sched_group_barrier(0x100, N, 0); }
 
-struct TileMask {
-  int nvalid;
-  int self0;
-};
-
 // Per-lane share of the direct-to-LDS copies of an R-row tile: the tile row
 // and element offset (swizzle applied) of each 16-byte chunk this lane moves
 // are fixed for the whole kernel, so a tile copy costs one multiply-add and
