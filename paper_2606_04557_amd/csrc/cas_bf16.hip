@@ -1560,17 +1560,35 @@ void dkdv_bf16_kernel(DkdvParams p) {
       wait_vmcnt<0>();
     }
 
-    if (!key_ok) return;
+    // Store through LDS: each lane holds 4-channel pieces of its key's row;
+    // staged as whole rows, every store instruction writes full 16-byte
+    // pieces of consecutive rows (whole cache lines instead of 8-byte pieces
+    // that leave lines partly written). Every wave's copies have landed
+    // (wait above), so after this barrier the arena is free.
+    __syncthreads();
     __bf16 *dst = pwave ? dvp : dkp;
     if (!dst) return;
     const float sc = pwave ? 1.0f : p.scale;
-    const int64_t krow = (int64_t)(key0 + my_key) * st;
+    constexpr int SRS = (D + 8) * 2;                 // staged row bytes (padded against bank conflicts)
+    char *const stg = smem + wave * 32 * SRS;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj)
-        store4(dst + krow + dt * 32 + jj * 8 + G * 4, acc[dt][jj * 4 + 0] * sc, acc[dt][jj * 4 + 1] * sc,
-               acc[dt][jj * 4 + 2] * sc, acc[dt][jj * 4 + 3] * sc);
+        store4(reinterpret_cast<__bf16 *>(stg + n * SRS) + dt * 32 + jj * 8 + G * 4, acc[dt][jj * 4 + 0] * sc,
+               acc[dt][jj * 4 + 1] * sc, acc[dt][jj * 4 + 2] * sc, acc[dt][jj * 4 + 3] * sc);
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes are done
+    asm volatile("" ::: "memory");
+    constexpr int CPR = D / 8;                       // 16-byte pieces per row
+    constexpr int RPI = 64 / CPR;                    // rows per store instruction
+    const int nrow = min(32, nk - 32 * q);           // valid keys of this wave
+    const int pr = lane / CPR, pc = lane % CPR;
+#pragma unroll
+    for (int i = 0; i < 32 / RPI; ++i) {
+      const int r = RPI * i + pr;
+      const uint4 v = *reinterpret_cast<const uint4 *>(stg + r * SRS + pc * 16);
+      if (r < nrow) *reinterpret_cast<uint4 *>(dst + (int64_t)(key0 + 32 * q + r) * st + pc * 8) = v;
+    }
 
   };
   if (pwave) body(std::true_type{});
