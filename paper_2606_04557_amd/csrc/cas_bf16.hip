@@ -20,7 +20,7 @@ constexpr int kFastThreads = kNW * 64;
 constexpr int kKT = 64;                // keys per tile (forward, dQ)
 constexpr int kFastRowsPerWave = 32;
 constexpr int kFastRowsPerWg = kNW * kFastRowsPerWave;   // 256
-constexpr int kDkdvLead = 4;           // dK/dV: LDS fragments in flight ahead of their MFMA
+constexpr int kDkdvLead = 6;           // dK/dV: LDS fragments in flight ahead of their MFMA
 constexpr int kDkdvPrio = 1;           // dK/dV: wave priority in a matrix phase (0 in VALU phases)
 constexpr int kRefMargin = 64;         // forward: row sums below 2^kRefMargin need no exact pass
 
