@@ -107,8 +107,11 @@ def head_backward(qh: np.ndarray, K: np.ndarray, V: np.ndarray, n_prefix: int, q
 
 
 def forward(q, k_self, v_self, cart_k: Sequence, cart_v: Sequence, rows: Sequence[Sequence[int]],
-            scale: float, group_size: int):
-    """O [B, Sq, Hq, D] and LSE [B, Hq, Sq] over [cartridges of the row || causal self]."""
+            scale: float, group_size: int, kv_heads: Optional[Sequence[int]] = None):
+    """O [B, Sq, Hq, D] and LSE [B, Hq, Sq] over [cartridges of the row || causal self].
+
+    With ``kv_heads`` given, only the query heads of those KV heads' groups
+    are evaluated (every other head's O and LSE stay zero)."""
     q = _f64(q)
     B, Sq, Hq, Dh = q.shape
     O = np.zeros((B, Sq, Hq, Dh))
@@ -117,6 +120,8 @@ def forward(q, k_self, v_self, cart_k: Sequence, cart_v: Sequence, rows: Sequenc
     for b in range(B):
         for h in range(Hq):
             kv = h // group_size
+            if kv_heads is not None and kv not in kv_heads:
+                continue
             K, V, npre = row_keys(cart_k, cart_v, rows[b], k_self[b], v_self[b], kv)
             o, lse, _ = head_forward(q[b, :, h, :], K, V, npre, Sq, t_all, scale)
             O[b, :, h, :] = o
@@ -125,18 +130,24 @@ def forward(q, k_self, v_self, cart_k: Sequence, cart_v: Sequence, rows: Sequenc
 
 
 def backward(q, k_self, v_self, cart_k: Sequence, cart_v: Sequence, rows: Sequence[Sequence[int]],
-             scale: float, group_size: int, d_o, O=None, LSE=None):
+             scale: float, group_size: int, d_o, O=None, LSE=None,
+             kv_heads: Optional[Sequence[int]] = None):
     """Gradients of sum(dO * O).
 
     Returns dq, dk_self, dv_self, dcart_k, dcart_v; dcart_* hold one entry per
     cartridge tensor (None for cartridges no row references) and sum over all
-    references of that cartridge."""
+    references of that cartridge.
+
+    With ``kv_heads`` given, only those KV heads (and the query heads of
+    their groups) are evaluated; every other head's gradients stay zero. The
+    gradients of a KV head depend on its own group's queries only, so the
+    evaluated heads are complete."""
     q = _f64(q)
     d_o = _f64(d_o)
     B, Sq, Hq, Dh = q.shape
     Hkv = np.asarray(k_self).shape[2]
     if O is None or LSE is None:
-        O, LSE = forward(q, k_self, v_self, cart_k, cart_v, rows, scale, group_size)
+        O, LSE = forward(q, k_self, v_self, cart_k, cart_v, rows, scale, group_size, kv_heads)
     dq = np.zeros_like(q)
     dk_self = np.zeros((B, Sq, Hkv, Dh))
     dv_self = np.zeros((B, Sq, Hkv, Dh))
@@ -152,6 +163,8 @@ def backward(q, k_self, v_self, cart_k: Sequence, cart_v: Sequence, rows: Sequen
     for b in range(B):
         for h in range(Hq):
             kv = h // group_size
+            if kv_heads is not None and kv not in kv_heads:
+                continue
             K, V, npre = row_keys(cart_k, cart_v, rows[b], k_self[b], v_self[b], kv)
             dQh, dK, dV = head_backward(q[b, :, h, :], K, V, npre, Sq, t_all, scale,
                                         d_o[b, :, h, :], O[b, :, h, :], LSE[b, h, :])

@@ -6,12 +6,10 @@ hyperparameter table's 8,192-token packed sequences) against the fp64 oracle.
 Bars as in test_gpu_parity: max |gpu - oracle| / max |oracle| <= 1e-5 (fp32)
 or 2e-2 (bf16) per tensor, LSE absolute error <= 1e-5 / 1e-3.
 """
-import numpy as np
 import pytest
 
 import casgen
-import oracle
-from gpu_util import GpuCase, LSE_TOL, TOL, host, rel_err
+from gpu_util import GpuCase
 from test_gpu_parity import _check_full
 
 pytestmark = pytest.mark.gpu
@@ -90,56 +88,16 @@ def test_packed_equal_lengths_match_fixed_layout():
         assert torch.equal(b.dk[c], d1[c][0]) and torch.equal(b.dv[c], d1[c][1])
 
 
-def test_packed_8k_sampled():
+def test_packed_8k_full():
     """The 8,192-token packed training layout (20-cartridge pool, target plus up
-    to 10 distractors per sample): sampled rows and keys against the oracle,
+    to 10 distractors per sample): every output element against the oracle,
     and the whole-tensor identity that every query row's P sums to one, so the
     dV of all keys (each cartridge once, all self keys) adds up to the dO of
     every query row of the group."""
-    import torch
     wl = casgen.packed()
     case = GpuCase(wl)
-    o, lse = case.fwd()
-    dq, dks, dvs = case.bwd(o, lse)
-    _sync()
-    q, ks, vs, ck, cv, rows, scale, g = case.oracle_args()
-    d_o = case.oracle_do()
-    qo = wl.q_offsets
-    rng = np.random.default_rng(8)
-    picks = []
-    for _ in range(24):
-        b = int(rng.integers(wl.batch))
-        picks.append((b, int(rng.integers(wl.num_q_heads)), int(rng.integers(wl.q_lens[b]))))
-    picks += [(0, 0, 0), (wl.batch - 1, wl.num_q_heads - 1, wl.q_lens[-1] - 1)]
-    go, gl, gq = host(o), host(lse), host(dq)
-    vo, vl, vq, ro, rl, rq = [], [], [], [], [], []
-    for b, h, t in picks:
-        oo, ll, dd = oracle.packed_rows_forward_backward(q, ks, vs, ck, cv, rows, qo, scale, g, b, h, [t], d_o)
-        ro.append(oo[0]); rl.append(ll[0]); rq.append(dd[0])
-        vo.append(go[qo[b] + t, h]); vl.append(gl[h, qo[b] + t]); vq.append(gq[qo[b] + t, h])
-    tol = TOL["bf16"]
-    e_o, e_q = rel_err(np.array(vo), np.array(ro)), rel_err(np.array(vq), np.array(rq))
-    e_l = float(np.abs(np.array(vl) - np.array(rl)).max())
-    print("P8K sampled O", f"{e_o:.2e}", "LSE", f"{e_l:.2e}", "dQ", f"{e_q:.2e}")
-    assert e_o <= tol and e_l <= LSE_TOL["bf16"] and e_q <= tol
-    # Keys: the cartridge used by the most samples, one used once, self keys.
-    uses = {c: sum(c in r for r in rows) for c in range(len(wl.cart_lens))}
-    busy = max(uses, key=uses.get)
-    once = min((c for c in uses if uses[c] > 0), key=uses.get)
-    kv = 3
-    targets = [(busy, [0, wl.cart_lens[busy] - 1]), (once, [wl.cart_lens[once] // 2]), (-1, [0, 5]),
-               (-wl.batch, [wl.q_lens[-1] - 1])]
-    res = oracle.packed_key_grads_many(q, ks, vs, ck, cv, rows, qo, scale, g, d_o, kv, targets)
-    for (cart, toks), (rk, rv) in zip(targets, res):
-        if cart >= 0:
-            gk, gv = host(case.dk[cart][toks, kv]), host(case.dv[cart][toks, kv])
-        else:
-            b = -cart - 1
-            gk = host(dks[[qo[b] + t for t in toks], kv])
-            gv = host(dvs[[qo[b] + t for t in toks], kv])
-        ek, ev = rel_err(gk, rk), rel_err(gv, rv)
-        print(f"P8K kv{kv} cart{cart} ({uses.get(cart, 1)} uses) dK {ek:.2e} dV {ev:.2e}")
-        assert ek <= tol and ev <= tol
+    _, _, (dq, dks, dvs) = _check_full(case, "P8K")
+    g = wl.group_size
     tot = dvs.float().sum(0)
     for c in case.dv:
         tot = tot + case.dv[c].float().sum(0)

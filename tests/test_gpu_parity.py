@@ -3,9 +3,10 @@ seeded input bits.
 
 Bars: max |gpu - oracle| / max |oracle| <= 1e-5 for fp32 inputs and <= 2e-2
 for bf16 inputs, per output tensor (per cartridge for dK/dV); LSE absolute
-error <= 1e-5 (fp32) / 1e-3 (bf16). Small cases compare every element; the
-benchmark-size cases compare sampled rows and keys the oracle evaluates one by
-one, plus whole-tensor properties.
+error <= 1e-5 (fp32) / 1e-3 (bf16). Small cases and the 4 x 1024-cartridge
+configuration compare every element; the 16 x 2048 and ragged 64-cartridge
+configurations compare two whole KV heads element by element, plus sampled
+rows and tile-edge keys on the other heads and whole-tensor properties.
 """
 import numpy as np
 import pytest
@@ -48,7 +49,7 @@ def _check_full(case, label=""):
     for (kind, c), base in case.bases.items():
         if base.dim() == 2 and base.shape[1] > wl.num_kv_heads * wl.head_dim:
             assert torch.isnan(base[:, wl.num_kv_heads * wl.head_dim:].float()).all(), (kind, c)
-    return o, lse
+    return o, lse, (dq, dks, dvs)
 
 
 def test_c1_fp32_full():
@@ -115,14 +116,17 @@ def test_small_forced_splits(spec):
         cas.set_tuning(0, 0)
 
 
-def _sampled_check(case, n_rows=24, key_targets=None, seed=0, forward_only=False):
+def _sampled_check(case, n_rows=24, key_targets=None, seed=0, forward_only=False, results=None):
     """Oracle evaluated on sampled query rows (O, LSE, dQ) and sampled keys (dK, dV)."""
     wl = case.wl
-    o, lse = case.fwd()
-    grads = None
-    if not forward_only:
-        grads = case.bwd(o, lse)
-    _sync()
+    if results is None:
+        o, lse = case.fwd()
+        grads = None
+        if not forward_only:
+            grads = case.bwd(o, lse)
+        _sync()
+    else:
+        o, lse, grads = results
     args = case.oracle_args()
     d_o = None if forward_only else case.oracle_do()
     rng = np.random.default_rng(seed)
@@ -162,59 +166,131 @@ def _sampled_check(case, n_rows=24, key_targets=None, seed=0, forward_only=False
     return o, lse, grads
 
 
-def _gradient_sums(case, grads):
-    """Whole-tensor property: per (row, kv head) with no cartridge shared between
-    rows, the dV rows over all visible keys sum to the sum of dO over the group's
-    query rows (softmax rows sum to one)."""
+def _check_heads(case, kv_heads):
+    """Whole KV heads compared element by element: O, LSE and dQ of every query
+    row of their GQA groups, and the self dK/dV and every cartridge's dK/dV at
+    those heads (every token). Returns the library's results for further
+    checks on the other heads."""
     import torch
+    wl = case.wl
+    o, lse = case.fwd()
+    grads = case.bwd(o, lse)
+    _sync()
+    args = case.oracle_args()
+    O, LSE = oracle.forward(*args, kv_heads=kv_heads)
+    rdq, rdks, rdvs, rdck, rdcv = oracle.backward(*args, case.oracle_do(), O=O, LSE=LSE,
+                                                  kv_heads=kv_heads)
+    g = wl.group_size
+    qh = [h for h in range(wl.num_q_heads) if h // g in kv_heads]
+    kvi = torch.tensor(kv_heads, device=o.device)
+    qhi = torch.tensor(qh, device=o.device)
+    tol = TOL[wl.dtype]
+    errs = {
+        "o": rel_err(host(o.index_select(2, qhi)), O[:, :, qh]),
+        "lse": float(np.abs(host(lse.index_select(1, qhi)) - LSE[:, qh]).max()),
+        "dq": rel_err(host(grads[0].index_select(2, qhi)), rdq[:, :, qh]),
+        "dk_self": rel_err(host(grads[1].index_select(2, kvi)), rdks[:, :, kv_heads]),
+        "dv_self": rel_err(host(grads[2].index_select(2, kvi)), rdvs[:, :, kv_heads]),
+    }
+    for c in case.dk:
+        errs[f"dk[{c}]"] = rel_err(host(case.dk[c].index_select(1, kvi)), rdck[c][:, kv_heads])
+        errs[f"dv[{c}]"] = rel_err(host(case.dv[c].index_select(1, kvi)), rdcv[c][:, kv_heads])
+    worst = max((v, k) for k, v in errs.items() if k != "lse")
+    print(wl.name, f"kv heads {kv_heads} in full:", {k: f"{v:.2e}" for k, v in errs.items()
+                                                    if k in ("o", "lse", "dq", "dk_self", "dv_self")},
+          f"worst {worst[1]} {worst[0]:.2e} over {len(case.dk)} cartridges")
+    for k, v in errs.items():
+        lim = LSE_TOL[wl.dtype] if k == "lse" else tol
+        assert v <= lim, (wl.name, k, v)
+    return o, lse, grads
+
+
+def _gradient_sums(case, grads):
+    """Whole-tensor properties per (row, kv head) when no cartridge is shared
+    between rows: (a) the dV of all visible keys sums to the dO of the group's
+    query rows (each softmax row sums to one); (b) the dK of all visible keys
+    sums to zero (each row of dS sums to zero), measured against the sum of
+    |dK|."""
     wl = case.wl
     g = wl.group_size
     do = case.d_o.float()
     for b in range(wl.batch):
         tot = grads[2][b].float().sum(0)                      # [Hkv, D]
+        tk = grads[1][b].float().sum(0)
+        ak = grads[1][b].float().abs().sum(0)
         for c in wl.rows[b]:
             tot = tot + case.dv[c].float().sum(0)
+            tk = tk + case.dk[c].float().sum(0)
+            ak = ak + case.dk[c].float().abs().sum(0)
         exp = do[b].view(wl.q_len, wl.num_kv_heads, g, wl.head_dim).sum((0, 2))
         err = (tot - exp).abs().max().item() / exp.abs().max().item()
-        print(wl.name, "sum dV rel err", f"{err:.2e}")
+        errk = (tk.abs() / ak).max().item()
+        print(wl.name, f"row {b} sum dV rel err {err:.2e}, |sum dK| / sum |dK| {errk:.2e}")
         assert err <= 2e-2
+        assert errk <= 2e-3
 
 
-def test_c2_full_size_sampled():
+def _edge_tokens(L):
+    """Tile-edge tokens of a length-L key block (64-key tiles, 128-key dK/dV
+    workgroups) plus the last one."""
+    return sorted({t for t in (0, 1, 63, 64, 127, 128, L // 2, L - 2, L - 1) if 0 <= t < L})
+
+
+def test_c2_full_size():
+    """4 rows x 4 x 1024-token cartridges: every output element against the oracle."""
     case = GpuCase(casgen.config(2))
-    targets = {3: [(0, [0, 511, 1023]), (13, [5, 1000]), (-1, [0, 1023]), (-4, [512])]}
-    o, lse, grads = _sampled_check(case, key_targets=targets)
+    _, _, grads = _check_full(case, "C2")
     _gradient_sums(case, grads)
 
 
-def test_c3_full_size_sampled():
-    """The headline 16 x 2048-cartridge configuration in the launch plan the bench times."""
-    case = GpuCase(casgen.config(3))
-    targets = {5: [(0, [0, 2047]), (17, [1000]), (-1, [0, 2047]), (-2, [1024])]}
-    o, lse, grads = _sampled_check(case, n_rows=32, key_targets=targets, seed=3)
-    _gradient_sums(case, grads)
+def test_c3_full_size():
+    """The headline 16 x 2048-cartridge configuration in the launch plan the
+    bench times: KV heads 0 and 7 (the first and last XCD range of the
+    forward and dQ order) in full; on every other head, sampled query rows and
+    tile-edge keys of a cartridge of each row and of the self keys."""
+    wl = casgen.config(3)
+    case = GpuCase(wl)
+    res = _check_heads(case, [0, 7])
+    targets = {}
+    for kv in range(1, 7):
+        b = kv % 2
+        c0, c1 = wl.rows[b][kv], wl.rows[b][15 - kv]
+        targets[kv] = [(c0, _edge_tokens(2048)), (c1, [1000, 1024, 1535, 1536]),
+                       (-b - 1, _edge_tokens(wl.q_len))]
+    _sampled_check(case, n_rows=32, key_targets=targets, seed=3, results=res)
+    _gradient_sums(case, res[2])
 
 
-def test_c4_full_size_sampled():
+def test_c4_full_size():
     """64 cartridges of U[256, 4096] tokens in separate allocations with padded and
-    head-major layouts; B = 1 forces key-axis splits in the forward and dQ."""
+    head-major layouts; B = 1 forces key-axis splits in the forward and dQ.
+    KV heads 2 and 6 in full; on every other head, tile-edge keys of two
+    cartridges of each layout kind and of the self keys."""
     import paper_2606_04557_amd as cas
     wl = casgen.config(4)
     case = GpuCase(wl)
     prob = cas.Problem.from_tensors(case.q, case.rows, wl.num_kv_heads, wl.group_size, float(wl.scale))
     info = cas.plan_info(prob)
     assert info["fwd_splits"] > 1 and info["dq_splits"] > 1
-    last = len(wl.cart_lens) - 1
-    targets = {2: [(0, [0, wl.cart_lens[0] - 1]), (37, [wl.cart_lens[37] // 2]),
-                   (last, [wl.cart_lens[last] - 1]), (-1, [0, 511])]}
-    o, lse, grads = _sampled_check(case, n_rows=32, key_targets=targets, seed=4)
-    _gradient_sums(case, grads)
+    res = _check_heads(case, [2, 6])
+    targets = {}
+    for kv in (0, 1, 3, 4, 5, 7):
+        picks = []
+        for kind in ("tok", "padded", "head"):
+            ids = [c for c in range(64) if wl.layouts[c] == kind]
+            c = ids[(kv * 5) % len(ids)]
+            picks.append((c, _edge_tokens(wl.cart_lens[c])))
+        picks.append((-1, _edge_tokens(wl.q_len)))
+        targets[kv] = picks
+    _sampled_check(case, n_rows=32, key_targets=targets, seed=4, results=res)
+    _gradient_sums(case, res[2])
 
 
 def test_c5_forward_with_staging():
     """Retrieval-style inference mix: 64 requests each over 4 cartridges of a
     256-cartridge pool; the pool's second half is staged host -> HBM with
-    cas_cartridge_stage on a side stream, and the forward waits on its events."""
+    cas_cartridge_stage on a side stream, and the forward waits on its events.
+    Every O and LSE element is compared with the oracle."""
     import torch
     import paper_2606_04557_amd as cas
     wl = casgen.config(5)
@@ -244,7 +320,12 @@ def test_c5_forward_with_staging():
         events.append(ev)
     for ev in events:
         torch.cuda.current_stream().wait_event(ev)
-    _sampled_check(case, n_rows=40, forward_only=True, seed=5)
+    o, lse = case.fwd()
+    _sync()
+    O, LSE, _ = full_oracle(case, backward=False)
+    e_o, e_l = rel_err(host(o), O), float(np.abs(host(lse) - LSE).max())
+    print("C5 every element: O", f"{e_o:.2e}", "LSE", f"{e_l:.2e}")
+    assert e_o <= TOL["bf16"] and e_l <= LSE_TOL["bf16"]
     # A pageable source is refused before anything is enqueued.
     src = torch.zeros(1024, dtype=torch.bfloat16)
     dst = torch.zeros(1024, dtype=torch.bfloat16, device="cuda")

@@ -380,6 +380,58 @@ def test_sampled_paths_match_full():
             assert np.abs(dv - ev).max() <= 1e-13
 
 
+def test_key_grads_many_matches_full():
+    """key_grads_many against the full backward: several targets per call, one
+    cartridge named by two targets, a cartridge referenced by every row and
+    twice within one row, a cartridge used by one row only, zero-length and
+    one-token cartridges, and self targets of every row, on each KV head."""
+    p = _problem(43, B=3, Sq=5, Hq=4, Hkv=2, D=3, lens=(3, 2, 0, 1, 4),
+                 rows=((0, 1, 0), (2, 0, 3), (4, 0, 1)))
+    dq, dks, dvs, dck, dcv = _bwd(p)
+    args = (p["q"], p["k_self"], p["v_self"], p["cart_k"], p["cart_v"], p["rows"], p["scale"],
+            p["group_size"])
+    targets = [(0, [2, 0, 1]), (1, [1]), (0, [1]), (3, [0]), (4, [3, 0, 2]), (2, []),
+               (-1, [4, 0]), (-2, [0, 1, 2, 3, 4]), (-3, [2])]
+    for kv in range(2):
+        res = oracle.key_grads_many(*args, p["d_o"], kv=kv, targets=targets)
+        assert len(res) == len(targets)
+        for (cart, toks), (dk, dv) in zip(targets, res):
+            if cart >= 0:
+                ek, ev = dck[cart][toks, kv], dcv[cart][toks, kv]
+            else:
+                ek, ev = dks[-cart - 1, toks, kv], dvs[-cart - 1, toks, kv]
+            assert dk.shape == ek.shape and dv.shape == ev.shape
+            assert np.abs(dk - ek).max(initial=0) <= 1e-13, (kv, cart, toks)
+            assert np.abs(dv - ev).max(initial=0) <= 1e-13, (kv, cart, toks)
+
+
+def test_kv_head_restriction_matches_full():
+    """forward/backward restricted to some KV heads equal the full evaluation
+    on those heads' outputs and leave every other head at zero."""
+    p = _problem(47, B=2, Sq=4, Hq=6, Hkv=3, D=3, lens=(2, 3), rows=((0, 1), (1, 0, 1)))
+    O, LSE = _fwd(p)
+    full = _bwd(p)
+    args = (p["q"], p["k_self"], p["v_self"], p["cart_k"], p["cart_v"], p["rows"], p["scale"],
+            p["group_size"])
+    for sel in ([0], [2], [0, 2]):
+        Or, Lr = oracle.forward(*args, kv_heads=sel)
+        part = oracle.backward(*args, p["d_o"], kv_heads=sel)
+        qh = [h for h in range(6) if h // 2 in sel]
+        qo = [h for h in range(6) if h // 2 not in sel]
+        ko = [k for k in range(3) if k not in sel]
+        assert np.array_equal(Or[:, :, qh], O[:, :, qh]) and not Or[:, :, qo].any()
+        assert np.array_equal(Lr[:, qh], LSE[:, qh]) and not Lr[:, qo].any()
+        assert np.abs(part[0][:, :, qh] - full[0][:, :, qh]).max() <= 1e-13
+        assert not part[0][:, :, qo].any()
+        for i in (1, 2):
+            assert np.abs(part[i][:, :, sel] - full[i][:, :, sel]).max() <= 1e-13
+            assert not part[i][:, :, ko].any()
+        for i in (3, 4):
+            for c in range(2):
+                assert np.abs(part[i][c][:, sel] - full[i][c][:, sel]).max() <= 1e-13
+                assert not part[i][c][:, ko].any()
+
+
 # ---------------------------------------------------------------------------
 # Packed samples (one token axis, per-sample cartridges, block-diagonal self).
 # ---------------------------------------------------------------------------
@@ -465,6 +517,44 @@ def test_p13_packed_block_diagonal_and_fixed_layout():
     Op, LSEp = _pfwd(f)
     assert np.allclose(Op, Of.reshape(6, 2, 4), rtol=0, atol=1e-14)
     assert np.allclose(LSEp, LSEf.transpose(1, 0, 2).reshape(2, 6), rtol=0, atol=1e-14)
+
+
+def test_packed_sampled_paths_match_full():
+    """packed_rows_forward_backward at every (sample, head, position) and
+    packed_key_grads_many for every cartridge (one shared by two samples and
+    referenced twice by one, one seen only by an empty sample) and for the
+    self keys of every sample, against packed_forward / packed_backward."""
+    p = _packed_problem(15, q_lens=(3, 0, 2, 1), Hq=4, Hkv=2)
+    args = (p["q"], p["k_self"], p["v_self"], p["cart_k"], p["cart_v"], p["rows"], p["q_offsets"],
+            p["scale"], p["group_size"])
+    O, LSE = oracle.packed_forward(*args)
+    dq, dks, dvs, dck, dcv = oracle.packed_backward(*args, p["d_o"])
+    qo = p["q_offsets"]
+    for b in range(len(p["rows"])):
+        n = qo[b + 1] - qo[b]
+        for h in range(4):
+            if n == 0:
+                continue
+            t_idx = list(range(n))[::-1]
+            o, lse, d = oracle.packed_rows_forward_backward(*args, b, h, t_idx, p["d_o"])
+            glob = [qo[b] + t for t in t_idx]
+            assert np.abs(o - O[glob, h]).max() <= 1e-13
+            assert np.abs(lse - LSE[h, glob]).max() <= 1e-13
+            assert np.abs(d - dq[glob, h]).max() <= 1e-13
+    targets = [(0, [1, 0]), (1, [0]), (2, [2, 0]), (0, [1]), (-1, [2, 0, 1]), (-3, [1, 0]),
+               (-4, [0])]
+    for kv in range(2):
+        res = oracle.packed_key_grads_many(*args, p["d_o"], kv, targets)
+        for (cart, toks), (dk, dv) in zip(targets, res):
+            if cart >= 0:
+                ek, ev = dck[cart][toks, kv], dcv[cart][toks, kv]
+            else:
+                glob = [qo[-cart - 1] + t for t in toks]
+                ek, ev = dks[glob, kv], dvs[glob, kv]
+            assert np.abs(dk - ek).max() <= 1e-13, (kv, cart, toks)
+            assert np.abs(dv - ev).max() <= 1e-13, (kv, cart, toks)
+    # Cartridge 2 belongs to the empty sample only: its gradient is exactly zero.
+    assert not dck[2].any()
 
 
 # ---------------------------------------------------------------------------
