@@ -39,7 +39,10 @@
 extern "C" {
 #endif
 
-#define CAS_ABI_VERSION 2
+#define CAS_ABI_VERSION 3
+
+/* Bytes of the device scratch each GPU holds for cas_prefix_attn_fwd_noalloc. */
+#define CAS_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
 
 typedef enum {
   CAS_OK = 0,
@@ -159,6 +162,30 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
                                  const void *v_self, const void *o, const float *lse,
                                  const void *d_o, void *dq, void *dk_self, void *dv_self,
                                  void *workspace, size_t ws_bytes, void *hip_stream);
+
+/*
+ * The forward without any allocation, for callers that cannot allocate
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc). Same problem, tensors, results and error rules as
+ * cas_prefix_attn_fwd, without the workspace arguments: the workspace is a
+ * static device array of CAS_NOALLOC_SCRATCH_BYTES that the library holds on
+ * every GPU it runs on until the process ends, and the launch tables reach it
+ * as kernel arguments (no pinned staging buffer). The call allocates nothing:
+ * no hipMalloc, hipHostMalloc, hipFree or event creation (the first call on a
+ * device only looks up that device's scratch address).
+ *
+ * When the forward would split the key axis into more partials than the
+ * scratch holds, fewer splits are used (the result changes only in rounding
+ * order). A problem whose launch tables alone exceed the scratch returns
+ * CAS_ERR_UNSUPPORTED before anything is enqueued.
+ *
+ * All calls on one GPU share its scratch: calls that may overlap on that GPU
+ * (different streams without ordering, or several host threads) race and
+ * give wrong results; calls ordered on one stream are safe. Nothing in the
+ * scratch needs clearing between calls.
+ */
+cas_status_t cas_prefix_attn_fwd_noalloc(const cas_problem_t *p, const void *q, const void *k_self,
+                                         const void *v_self, void *o, float *lse, void *hip_stream);
 
 /*
  * Cartridge staging (paper: Budget Manager and Pool rotation paragraphs,

@@ -14,7 +14,8 @@ from typing import List, Optional, Sequence, Tuple
 from . import _lib
 from ._lib import load  # noqa: F401
 
-__all__ = ["Segment", "Problem", "CasError", "load", "prefix_attn_fwd", "prefix_attn_bwd",
+__all__ = ["Segment", "Problem", "CasError", "load", "prefix_attn_fwd", "prefix_attn_fwd_noalloc",
+           "prefix_attn_bwd",
            "workspace_size", "plan_info", "set_tuning", "get_tuning", "cartridge_stage",
            "timing_enable", "timing_reset", "timing_read", "AdamCartridge", "adam_lr_scale",
            "cartridge_adam", "DecodeProblem", "paged_decode_fwd", "plan_rotation", "CartridgePool"]
@@ -179,6 +180,18 @@ def prefix_attn_fwd(q, k_self, v_self, rows: Sequence[Sequence[Segment]], num_kv
                                       v_self.data_ptr(), o.data_ptr(), _ptr(lse), ws.data_ptr(),
                                       ws.numel(), _stream_handle(q.device, stream)))
     return o, lse
+
+
+def prefix_attn_fwd_noalloc(q, k_self, v_self, rows: Sequence[Sequence[Segment]], num_kv_heads: int,
+                            group_size: int, softmax_scale: float, o, lse, stream=None,
+                            q_offsets: Optional[Sequence[int]] = None) -> None:
+    """The forward through cas_prefix_attn_fwd_noalloc: writes the caller's
+    ``o`` (and ``lse`` unless None) using the library's static device scratch
+    instead of a workspace; nothing is allocated."""
+    prob = Problem.from_tensors(q, rows, num_kv_heads, group_size, softmax_scale, q_offsets)
+    _check(load().cas_prefix_attn_fwd_noalloc(ctypes.byref(prob.c), q.data_ptr(), k_self.data_ptr(),
+                                              v_self.data_ptr(), o.data_ptr(), _ptr(lse),
+                                              _stream_handle(q.device, stream)))
 
 
 def prefix_attn_bwd(q, k_self, v_self, rows: Sequence[Sequence[Segment]], num_kv_heads: int,

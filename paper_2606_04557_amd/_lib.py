@@ -26,6 +26,7 @@ EXPORTS = [
     "cas_cartridge_adam", "cas_paged_decode_workspace_size", "cas_paged_decode_fwd",
     "cas_pool_plan_rotation", "cas_pool_create", "cas_pool_destroy", "cas_pool_host_cartridge",
     "cas_pool_load", "cas_pool_active", "cas_pool_end_step", "cas_pool_flush",
+    "cas_prefix_attn_fwd_noalloc",
 ]
 
 
@@ -92,7 +93,7 @@ class KernelTime(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 48), ("launches", ctypes.c_int32), ("total_ms", ctypes.c_double)]
 
 
-ABI_VERSION = 2   # CAS_ABI_VERSION of include/cas.h (cas_problem_t with q_offsets)
+ABI_VERSION = 3   # CAS_ABI_VERSION of include/cas.h (q_offsets; the no-allocation forward)
 
 _lib = None
 
@@ -110,6 +111,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cas_prefix_attn_workspace_size.argtypes = [P(Problem), ctypes.c_int, P(sz)]
     lib.cas_prefix_attn_fwd.argtypes = [P(Problem), vp, vp, vp, vp, vp, vp, sz, vp]
     lib.cas_prefix_attn_bwd.argtypes = [P(Problem), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.cas_prefix_attn_fwd_noalloc.argtypes = [P(Problem), vp, vp, vp, vp, vp, vp]
     lib.cas_cartridge_stage.argtypes = [P(StageCopy), i32, vp, vp]
     lib.cas_status_string.argtypes = [ctypes.c_int]
     lib.cas_status_string.restype = ctypes.c_char_p
@@ -140,6 +142,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cas_timing_reset.argtypes = []
     lib.cas_timing_read.argtypes = [P(KernelTime), i32, P(i32)]
     for name in ("cas_prefix_attn_workspace_size", "cas_prefix_attn_fwd", "cas_prefix_attn_bwd",
+                 "cas_prefix_attn_fwd_noalloc",
                  "cas_cartridge_stage", "cas_set_tuning", "cas_get_tuning", "cas_plan_info",
                  "cas_timing_enable", "cas_timing_reset", "cas_timing_read",
                  "cas_cartridge_adam_workspace_size", "cas_cartridge_adam",

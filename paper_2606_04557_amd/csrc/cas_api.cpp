@@ -120,8 +120,9 @@ int auto_splits(int64_t base_wgs, int64_t min_row_tiles) {
 }
 
 // Shapes, segment table and planning. `bwd` additionally folds aliases and
-// builds the dK/dV work list. Pure host code.
-cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
+// builds the dK/dV work list. A positive `fwd_split_cap` bounds the forward's
+// key-axis splits. Pure host code.
+cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl, int fwd_split_cap = 0) {
   if (!p) return fail(CAS_ERR_INVALID_ARGUMENT, "problem is NULL");
   if (p->dtype != CAS_DTYPE_BF16 && p->dtype != CAS_DTYPE_FP32)
     return fail(CAS_ERR_INVALID_ARGUMENT, "unknown dtype");
@@ -270,6 +271,7 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl) {
     base_dq += Hkv * ceil_div((int64_t)pl.len[b] * pl.g, rpw_dq);
   }
   pl.fwd_splits = tu.fwd_splits > 0 ? std::min(tu.fwd_splits, kMaxSplits) : auto_splits(base_fwd, min_row_tiles);
+  if (fwd_split_cap > 0) pl.fwd_splits = std::min(pl.fwd_splits, fwd_split_cap);
   pl.dq_splits = tu.dq_splits > 0 ? std::min(tu.dq_splits, kMaxSplits) : auto_splits(base_dq, min_row_tiles);
   if ((int64_t)pl.B * Hkv * pl.nqblk_fwd * pl.fwd_splits > INT32_MAX ||
       (int64_t)pl.B * Hkv * pl.nqblk_dq * pl.dq_splits > INT32_MAX)
@@ -536,17 +538,21 @@ cas_status_t ring_upload(size_t bytes, void *ws, hipStream_t stream, Fill &&fill
   return CAS_OK;
 }
 
+// Writes the launch tables, laid out as in the workspace, to host memory h
+// (table_bytes, zeroed by the caller).
+void fill_tables(const Plan &pl, bool bwd, char *h) {
+  if (!pl.segs.empty()) std::memcpy(h + pl.off_segs, pl.segs.data(), pl.segs.size() * sizeof(DevSeg));
+  std::memcpy(h + pl.off_rows, pl.rows.data(), pl.rows.size() * sizeof(DevRow));
+  if (!pl.tiles.empty()) std::memcpy(h + pl.off_tiles, pl.tiles.data(), pl.tiles.size() * sizeof(DevTile));
+  if (bwd) {
+    if (!pl.carts.empty()) std::memcpy(h + pl.off_carts, pl.carts.data(), pl.carts.size() * sizeof(DevCart));
+    if (!pl.uses.empty()) std::memcpy(h + pl.off_uses, pl.uses.data(), pl.uses.size() * sizeof(int32_t));
+    if (!pl.order.empty()) std::memcpy(h + pl.off_order, pl.order.data(), pl.order.size() * sizeof(DevWg));
+  }
+}
+
 cas_status_t upload_tables(const Plan &pl, bool bwd, void *ws, hipStream_t stream) {
-  return ring_upload(pl.table_bytes, ws, stream, [&](char *h) {
-    if (!pl.segs.empty()) std::memcpy(h + pl.off_segs, pl.segs.data(), pl.segs.size() * sizeof(DevSeg));
-    std::memcpy(h + pl.off_rows, pl.rows.data(), pl.rows.size() * sizeof(DevRow));
-    if (!pl.tiles.empty()) std::memcpy(h + pl.off_tiles, pl.tiles.data(), pl.tiles.size() * sizeof(DevTile));
-    if (bwd) {
-      if (!pl.carts.empty()) std::memcpy(h + pl.off_carts, pl.carts.data(), pl.carts.size() * sizeof(DevCart));
-      if (!pl.uses.empty()) std::memcpy(h + pl.off_uses, pl.uses.data(), pl.uses.size() * sizeof(int32_t));
-      if (!pl.order.empty()) std::memcpy(h + pl.off_order, pl.order.data(), pl.order.size() * sizeof(DevWg));
-    }
-  });
+  return ring_upload(pl.table_bytes, ws, stream, [&](char *h) { fill_tables(pl, bwd, h); });
 }
 
 // ---------------------------------------------------------------------------
@@ -847,6 +853,119 @@ int plan_rotation(const int32_t *steps, const uint8_t *active, int N, int B, flo
 }
 
 }  // namespace
+
+namespace cas {
+
+cas_status_t prefix_attn_fwd_run(const cas_problem_t *p, const void *q, const void *k_self,
+                                 const void *v_self, void *o, float *lse, void *workspace,
+                                 size_t ws_bytes, hipStream_t stream, ScratchAddressFn scratch) {
+  Plan pl;
+  cas_status_t s = build_plan(p, false, pl);
+  if (s != CAS_OK) return s;
+  if (scratch) {
+    // The workspace is the fixed scratch: fewer key-axis splits (smaller
+    // partials) until it fits. Only the rounding order of the merge changes.
+    while (pl.ws_fwd > ws_bytes && pl.fwd_splits > 1) {
+      // Bytes per split (partials and flags) from this plan; the rebuilt
+      // plan is checked again since each region is rounded up to 256 bytes.
+      const size_t per_split = (pl.ws_fwd - pl.table_bytes) / (size_t)pl.fwd_splits;
+      const size_t room = ws_bytes > pl.table_bytes ? ws_bytes - pl.table_bytes : 0;
+      size_t cap = per_split ? room / per_split : 1;
+      cap = std::max<size_t>(1, std::min<size_t>(cap, (size_t)pl.fwd_splits - 1));
+      pl = Plan{};
+      s = build_plan(p, false, pl, (int)cap);
+      if (s != CAS_OK) return s;
+    }
+    if (pl.ws_fwd > ws_bytes)
+      return fail(CAS_ERR_UNSUPPORTED, "launch tables need " + std::to_string(pl.ws_fwd) +
+                                           " bytes, above the " + std::to_string(ws_bytes) +
+                                           "-byte scratch of the no-allocation forward");
+  }
+  if (!q || !k_self || !v_self || !o) return fail(CAS_ERR_INVALID_ARGUMENT, "q, k_self, v_self and o must be non-NULL");
+  if (!aligned16(q) || !aligned16(k_self) || !aligned16(v_self) || !aligned16(o) || ((uintptr_t)lse & 3u))
+    return fail(CAS_ERR_ALIGNMENT, "tensors must be 16-byte aligned (lse 4-byte)");
+  const uintptr_t qbytes = (uintptr_t)pl.T * pl.Hq * pl.D * pl.esize;
+  const uintptr_t kvbytes = (uintptr_t)pl.T * pl.Hkv * pl.D * pl.esize;
+  std::vector<Interval> iv;
+  iv.push_back({(uintptr_t)q, (uintptr_t)q + qbytes, false, 0, "q"});
+  iv.push_back({(uintptr_t)k_self, (uintptr_t)k_self + kvbytes, false, 0, "k_self"});
+  iv.push_back({(uintptr_t)v_self, (uintptr_t)v_self + kvbytes, false, 0, "v_self"});
+  iv.push_back({(uintptr_t)o, (uintptr_t)o + qbytes, true, (uintptr_t)o, "o"});
+  if (lse) iv.push_back({(uintptr_t)lse, (uintptr_t)lse + (uintptr_t)pl.T * pl.Hq * 4, true, (uintptr_t)lse, "lse"});
+  add_segment_intervals(pl, p, false, iv);
+  std::string msg;
+  if (!overlap_free(iv, msg)) return fail(CAS_ERR_INVALID_ARGUMENT, msg);
+  if (scratch) {
+    // Everything is validated: only now touch the device.
+    hipError_t e = scratch(&workspace);
+    if (e != hipSuccess) return hip_fail("hipGetSymbolAddress (no-allocation scratch)", e);
+  } else {
+    s = check_workspace(workspace, ws_bytes, pl.ws_fwd);
+    if (s != CAS_OK) return s;
+  }
+
+  bind_self_tiles(pl, k_self, v_self);
+  if (scratch) {
+    // No pinned staging ring: the tables travel as kernel arguments.
+    std::vector<char> h(pl.table_bytes, 0);
+    fill_tables(pl, false, h.data());
+    hipError_t e = launch_table_upload(h.data(), pl.table_bytes, workspace, stream);
+    if (e != hipSuccess) return hip_fail("table upload launch", e);
+  } else {
+    s = upload_tables(pl, false, workspace, stream);
+    if (s != CAS_OK) return s;
+  }
+  // Kernel timing records pooled events, which the no-allocation path must
+  // not create: it launches directly.
+  auto launch = [&](const char *name, auto &&f) -> hipError_t {
+    return scratch ? f() : timed(name, stream, f);
+  };
+  char *ws = (char *)workspace;
+  FwdParams fp{};
+  fp.q = q;
+  fp.k_self = k_self;
+  fp.v_self = v_self;
+  fp.o = o;
+  fp.lse = lse;
+  fp.part_o = pl.fwd_splits > 1 ? (float *)(ws + pl.off_part_o) : nullptr;
+  fp.part_lse = pl.fwd_splits > 1 ? (float *)(ws + pl.off_part_lse) : nullptr;
+  fp.segs = (const DevSeg *)(ws + pl.off_segs);
+  fp.rows = (const DevRow *)(ws + pl.off_rows);
+  fp.tiles = (const DevTile *)(ws + pl.off_tiles);
+  fp.ovf_flag = pl.dt == kBF16 ? (int32_t *)(ws + pl.off_ovf) : nullptr;
+  fp.plane = pl.T * pl.Hq;
+  fp.B = pl.B;
+  fp.Smax = pl.Smax;
+  fp.Hkv = pl.Hkv;
+  fp.g = pl.g;
+  fp.nrows_max = pl.nrows_max;
+  fp.nqblk = pl.nqblk_fwd;
+  fp.splits = pl.fwd_splits;
+  fp.lse_hs = pl.packed ? (int32_t)pl.T : pl.Sq;
+  fp.scale_log2 = pl.scale * 1.4426950408889634f;
+  hipError_t e = launch("fwd", [&] { return launch_fwd(fp, pl.dt, pl.D, stream); });
+  if (e != hipSuccess) return hip_fail("fwd launch", e);
+  if (pl.fwd_splits > 1) {
+    MergeParams mp{};
+    mp.part_o = fp.part_o;
+    mp.part_lse = fp.part_lse;
+    mp.o = o;
+    mp.lse = lse;
+    mp.rows = fp.rows;
+    mp.plane = fp.plane;
+    mp.B = pl.B;
+    mp.Hkv = pl.Hkv;
+    mp.g = pl.g;
+    mp.nrows_max = pl.nrows_max;
+    mp.splits = pl.fwd_splits;
+    mp.lse_hs = fp.lse_hs;
+    e = launch("fwd_merge", [&] { return launch_fwd_merge(mp, pl.dt, pl.D, stream); });
+    if (e != hipSuccess) return hip_fail("fwd_merge launch", e);
+  }
+  return CAS_OK;
+}
+
+}  // namespace cas
 
 struct cas_pool {
   int N = 0, Hkv = 0, D = 0, B = 0, R = 1, S = 0, frozen = 0;
@@ -1278,73 +1397,8 @@ cas_status_t cas_plan_info(const cas_problem_t *p, cas_plan_info_t *out) {
 cas_status_t cas_prefix_attn_fwd(const cas_problem_t *p, const void *q, const void *k_self,
                                  const void *v_self, void *o, float *lse, void *workspace,
                                  size_t ws_bytes, void *hip_stream) {
-  Plan pl;
-  cas_status_t s = build_plan(p, false, pl);
-  if (s != CAS_OK) return s;
-  if (!q || !k_self || !v_self || !o) return fail(CAS_ERR_INVALID_ARGUMENT, "q, k_self, v_self and o must be non-NULL");
-  if (!aligned16(q) || !aligned16(k_self) || !aligned16(v_self) || !aligned16(o) || ((uintptr_t)lse & 3u))
-    return fail(CAS_ERR_ALIGNMENT, "tensors must be 16-byte aligned (lse 4-byte)");
-  const uintptr_t qbytes = (uintptr_t)pl.T * pl.Hq * pl.D * pl.esize;
-  const uintptr_t kvbytes = (uintptr_t)pl.T * pl.Hkv * pl.D * pl.esize;
-  std::vector<Interval> iv;
-  iv.push_back({(uintptr_t)q, (uintptr_t)q + qbytes, false, 0, "q"});
-  iv.push_back({(uintptr_t)k_self, (uintptr_t)k_self + kvbytes, false, 0, "k_self"});
-  iv.push_back({(uintptr_t)v_self, (uintptr_t)v_self + kvbytes, false, 0, "v_self"});
-  iv.push_back({(uintptr_t)o, (uintptr_t)o + qbytes, true, (uintptr_t)o, "o"});
-  if (lse) iv.push_back({(uintptr_t)lse, (uintptr_t)lse + (uintptr_t)pl.T * pl.Hq * 4, true, (uintptr_t)lse, "lse"});
-  add_segment_intervals(pl, p, false, iv);
-  std::string msg;
-  if (!overlap_free(iv, msg)) return fail(CAS_ERR_INVALID_ARGUMENT, msg);
-  s = check_workspace(workspace, ws_bytes, pl.ws_fwd);
-  if (s != CAS_OK) return s;
-
-  hipStream_t stream = (hipStream_t)hip_stream;
-  bind_self_tiles(pl, k_self, v_self);
-  s = upload_tables(pl, false, workspace, stream);
-  if (s != CAS_OK) return s;
-  char *ws = (char *)workspace;
-  FwdParams fp{};
-  fp.q = q;
-  fp.k_self = k_self;
-  fp.v_self = v_self;
-  fp.o = o;
-  fp.lse = lse;
-  fp.part_o = pl.fwd_splits > 1 ? (float *)(ws + pl.off_part_o) : nullptr;
-  fp.part_lse = pl.fwd_splits > 1 ? (float *)(ws + pl.off_part_lse) : nullptr;
-  fp.segs = (const DevSeg *)(ws + pl.off_segs);
-  fp.rows = (const DevRow *)(ws + pl.off_rows);
-  fp.tiles = (const DevTile *)(ws + pl.off_tiles);
-  fp.ovf_flag = pl.dt == kBF16 ? (int32_t *)(ws + pl.off_ovf) : nullptr;
-  fp.plane = pl.T * pl.Hq;
-  fp.B = pl.B;
-  fp.Smax = pl.Smax;
-  fp.Hkv = pl.Hkv;
-  fp.g = pl.g;
-  fp.nrows_max = pl.nrows_max;
-  fp.nqblk = pl.nqblk_fwd;
-  fp.splits = pl.fwd_splits;
-  fp.lse_hs = pl.packed ? (int32_t)pl.T : pl.Sq;
-  fp.scale_log2 = pl.scale * 1.4426950408889634f;
-  hipError_t e = timed("fwd", stream, [&] { return launch_fwd(fp, pl.dt, pl.D, stream); });
-  if (e != hipSuccess) return hip_fail("fwd launch", e);
-  if (pl.fwd_splits > 1) {
-    MergeParams mp{};
-    mp.part_o = fp.part_o;
-    mp.part_lse = fp.part_lse;
-    mp.o = o;
-    mp.lse = lse;
-    mp.rows = fp.rows;
-    mp.plane = fp.plane;
-    mp.B = pl.B;
-    mp.Hkv = pl.Hkv;
-    mp.g = pl.g;
-    mp.nrows_max = pl.nrows_max;
-    mp.splits = pl.fwd_splits;
-    mp.lse_hs = fp.lse_hs;
-    e = timed("fwd_merge", stream, [&] { return launch_fwd_merge(mp, pl.dt, pl.D, stream); });
-    if (e != hipSuccess) return hip_fail("fwd_merge launch", e);
-  }
-  return CAS_OK;
+  return prefix_attn_fwd_run(p, q, k_self, v_self, o, lse, workspace, ws_bytes, (hipStream_t)hip_stream,
+                             nullptr);
 }
 
 cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const void *k_self,

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/cas.h"
+
 namespace cas {
 
 // Work decomposition (gfx950: 64-lane waves, 4 SIMDs per CU).
@@ -240,6 +242,23 @@ struct DecodeParams {
   int32_t Hkv, g, page_size, Tq;
   float scale_log2;
 };
+
+// Forward shared by cas_prefix_attn_fwd (scratch == nullptr: the caller's
+// workspace, tables through the pinned staging ring) and the no-allocation
+// forward (scratch != nullptr: after validation, scratch() yields the device
+// address of the library's static scratch of ws_bytes; the forward's key
+// splits are lowered until its workspace fits, tables go up as kernel
+// arguments, and no timing events are recorded).
+using ScratchAddressFn = hipError_t (*)(void **);
+cas_status_t prefix_attn_fwd_run(const cas_problem_t *p, const void *q, const void *k_self,
+                                 const void *v_self, void *o, float *lse, void *workspace,
+                                 size_t ws_bytes, hipStream_t stream, ScratchAddressFn scratch);
+
+// Copies `bytes` (a multiple of 16) of host memory to device memory `dst` on
+// stream s as the kernel arguments of a copy kernel, kTableArgChunk bytes per
+// launch: no host or device allocation.
+constexpr int kTableArgChunk = 2048;
+hipError_t launch_table_upload(const void *host, size_t bytes, void *dst, hipStream_t s);
 
 // Kernel launchers (defined in the .hip files).
 hipError_t launch_fwd(const FwdParams &p, DType dt, int D, hipStream_t s);

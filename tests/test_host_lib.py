@@ -27,7 +27,7 @@ def test_exports_match_header(lib):
     assert declared == sorted(_lib.EXPORTS)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.cas_abi_version() == _lib.ABI_VERSION == 2
+    assert lib.cas_abi_version() == _lib.ABI_VERSION == 3
     assert lib.cas_status_string(_lib.CAS_ERR_NOT_PINNED) == b"CAS_ERR_NOT_PINNED"
 
 
@@ -387,3 +387,26 @@ def test_pool_config_validation(lib):
     assert lib.cas_pool_create(ctypes.byref(cfg), ctypes.byref(h)) == _lib.CAS_ERR_INVALID_ARGUMENT
     assert lib.cas_pool_active(None, None, None, 0, ctypes.byref(ctypes.c_int32())) == _lib.CAS_ERR_INVALID_ARGUMENT
     assert lib.cas_pool_destroy(None) == _lib.CAS_OK
+
+
+def test_noalloc_forward_validation(lib):
+    """The no-allocation forward validates like the forward, before it touches
+    the device: bad shapes, NULL or misaligned tensors, overlapping outputs,
+    and launch tables larger than its fixed scratch are refused."""
+    def call(f, **over):
+        a = dict(q=f.q, ks=f.ks, vs=f.vs, o=f.o, lse=f.lse)
+        a.update(over)
+        return lib.cas_prefix_attn_fwd_noalloc(ctypes.byref(f.p), a["q"], a["ks"], a["vs"], a["o"],
+                                               a["lse"], None)
+    f = Fake()
+    f.p.head_dim = 96
+    assert call(f) == _lib.CAS_ERR_UNSUPPORTED
+    f = Fake()
+    assert call(f, q=None) == _lib.CAS_ERR_INVALID_ARGUMENT
+    assert call(f, o=f.o + 8) == _lib.CAS_ERR_ALIGNMENT
+    assert call(f, o=f.q) == _lib.CAS_ERR_INVALID_ARGUMENT
+    assert call(f, lse=f.o) == _lib.CAS_ERR_INVALID_ARGUMENT
+    # 2^25 prefix tokens: 2^19 tiles of 32 bytes = 16 MiB of tables alone.
+    f = Fake(rows=((1 << 25,),), grads=False)
+    assert call(f) == _lib.CAS_ERR_UNSUPPORTED
+    assert "scratch" in _msg(lib)
