@@ -26,15 +26,55 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-PEAK_BF16_TFLOPS = 2516.6     # 256 CUs x 2.4 GHz x 4096 dense bf16 FLOP/clk/CU
+# MI355X published dense peaks (bf16 MFMA 2.5 PFLOP/s; fp32 matrix; HBM3E).
+PEAK_BF16_TFLOPS = 2500.0
 PEAK_FP32_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 
 METRIC = "prefix-attn fwd+bwd TFLOP/s & MFMA util, 8B GQA shape, 16×2K cartridges"
 
-# FLOPs per visible (query, key) pair per query head, in units of head_dim,
-# that each kernel must execute for its own outputs.
-KERNEL_FLOPS_PER_PAIR = {"fwd": 4, "dkdv": 8, "dq": 6}
+# Algorithmic FLOPs per visible (query, key) pair per query head, in units of
+# head_dim, that each kernel owns: forward QK^T and PV; dK/dV pass dV, dP and
+# dK; dQ pass dQ (together 12d per pair). The fused backward owns dV, dP, dK
+# and dQ.
+KERNEL_FLOPS_PER_PAIR = {"fwd": 4, "dkdv": 6, "dq": 2, "dkdvq": 8}
+# What each kernel executes, recomputation included (S in every backward
+# kernel, dP again in the dQ pass).
+KERNEL_EXEC_FLOPS_PER_PAIR = {"fwd": 4, "dkdv": 8, "dq": 6, "dkdvq": 10}
+
+
+def kernel_hbm_bytes(wl, kernel: str):
+    """Compulsory HBM bytes of one launch: every tensor the kernel must read
+    once and every result it writes once (the algorithmic traffic; re-reads
+    and workspace copies are not counted)."""
+    es = 2 if wl.dtype == "bf16" else 4
+    T = sum(wl.row_lens)
+    qb = T * wl.num_q_heads * wl.head_dim * es                     # Q, O, dO or dQ
+    kvs = T * wl.num_kv_heads * wl.head_dim * es                   # self K or V
+    used = sorted({c for r in wl.rows for c in r})
+    kvc = sum(wl.cart_lens[c] for c in used) * wl.num_kv_heads * wl.head_dim * es
+    stat = T * wl.num_q_heads * 4                                  # one fp32 per query row
+    if kernel == "fwd":       # Q, K, V in; O, LSE out
+        return qb + 2 * (kvc + kvs) + qb + stat
+    if kernel == "dkdv":      # Q, dO, K, V, LSE, D in; dK, dV out
+        return 2 * qb + 2 * (kvc + kvs) + 2 * stat + 2 * (kvc + kvs)
+    if kernel == "dq":        # Q, dO, K, V, LSE, D in; dQ out
+        return 2 * qb + 2 * (kvc + kvs) + 2 * stat + qb
+    if kernel == "dkdvq":     # the dK/dV pass plus dQ out
+        return 2 * qb + 2 * (kvc + kvs) + 2 * stat + 2 * (kvc + kvs) + qb
+    return None
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
 
 
 def log(*a):
@@ -67,9 +107,14 @@ def cpu_baseline(wl, T, heads: int = 1):
     import oracle
     try:
         from threadpoolctl import threadpool_info
-        cores = sum(i.get("num_threads", 1) for i in threadpool_info()) or 1
+        cores = max(i.get("num_threads", 1) for i in threadpool_info()) or 1
     except Exception:
         cores = 1
+    try:
+        # BLAS may start more threads than the CPUs this process may run on.
+        cores = min(cores, len(os.sched_getaffinity(0)))
+    except (AttributeError, OSError):
+        pass
     f = lambda a: None if a is None else casgen.to_float(a, wl.dtype)
     # Batch row 0's query tokens in either layout.
     row0 = (lambda a: a[0:wl.row_lens[0]]) if wl.packed else (lambda a: a[0])
@@ -92,6 +137,7 @@ def cpu_baseline(wl, T, heads: int = 1):
         pairs += Sq * npre + Sq * (Sq + 1) // 2
     tflops = 12.0 * wl.head_dim * pairs / elapsed / 1e12
     return {"value": tflops, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
             "sample": f"batch row 0, {heads} of {wl.num_q_heads} query heads: full fp64 forward+backward "
                       f"({Sq} queries x {npre + Sq} keys each), {elapsed:.1f} s"}
 
@@ -245,6 +291,7 @@ def main():
     launches, total = ktimes[dom]
     avg_ms = total / launches
     per_pair = KERNEL_FLOPS_PER_PAIR.get(dom)
+    exec_pair = KERNEL_EXEC_FLOPS_PER_PAIR.get(dom)
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
     achieved = wl.flops(per_pair) / (avg_ms * 1e-3) / 1e12 if per_pair else None
     traffic = None
@@ -253,11 +300,29 @@ def main():
             rec = json.load(fh)
         if rec.get("source_sha256_16") == kernel_source_hash():
             traffic = rec["kernels"].get(dom, {}).get("bytes")
+    algo_bytes = kernel_hbm_bytes(wl, dom)
     roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                 "frac": (achieved / peak) if achieved else None, "traffic": traffic,
                 "avg_launch_ms": avg_ms,
-                "flops_per_launch": wl.flops(per_pair) if per_pair else None}
-    kernels = {k: {"launches": n, "avg_ms": t / n} for k, (n, t) in ktimes.items()}
+                "flops_per_launch": wl.flops(per_pair) if per_pair else None,
+                "flops_per_pair": f"{per_pair}d" if per_pair else None,
+                # recomputation included: what the matrix cores execute
+                "executed_flops_per_launch": wl.flops(exec_pair) if exec_pair else None,
+                "executed_tflops": wl.flops(exec_pair) / (avg_ms * 1e-3) / 1e12 if exec_pair else None,
+                "hbm": {"algorithmic_bytes": algo_bytes,
+                        "algorithmic_gbs": algo_bytes / (avg_ms * 1e-3) / 1e9 if algo_bytes else None,
+                        "measured_bytes": traffic,
+                        "measured_gbs": traffic / (avg_ms * 1e-3) / 1e9 if traffic else None,
+                        "measured_frac_of_peak": traffic / (avg_ms * 1e-3) / 1e9 / PEAK_HBM_GBS
+                        if traffic else None,
+                        "peak_gbs": PEAK_HBM_GBS}}
+    kernels = {}
+    for k, (n, t) in ktimes.items():
+        kernels[k] = {"launches": n, "avg_ms": t / n}
+        if k in KERNEL_FLOPS_PER_PAIR:
+            a = wl.flops(KERNEL_FLOPS_PER_PAIR[k]) / (t / n * 1e-3) / 1e12
+            kernels[k]["algorithmic_tflops"] = a
+            kernels[k]["frac_of_peak"] = a / peak
     # MFMA utilisation: the MFMA work each launch executes (counted by
     # SQ_INSTS_VALU_MFMA_MOPS_BF16, recompute and masked tile parts included)
     # over this run's live launch time, against the dense bf16 peak; and the

@@ -4,12 +4,12 @@ TEST INFRASTRUCTURE ONLY. Nothing in the library's product path may import,
 call or execute this module; only the tests and the bench's CPU-baseline leg
 use it. It shares no code with the HIP library.
 
-What is computed (paper: Section "Optimization Dynamics", paragraph
-"Optimizer": Adam with fp32 optimizer state and bf16 weights; paragraph
-"Per-cartridge LR warmup": a cartridge that has received s optimizer steps
-uses eta_t * min(1, s / W_c), bucketed into N_b levels so that few distinct
-learning rates occur per step; the hyperparameter table: W_c = 20, one
-frozen (BOS) token). Adam itself is Algorithm 1 of Kingma and Ba, "Adam: A
+What is computed (paper: Section "Optimization Dynamics", paragraphs
+"Optimizer" and "Per-cartridge LR warmup"; the hyperparameter table):
+Adam on bf16 cartridge weights with fp32 state. Each cartridge ramps its own
+learning rate: with s the number of steps it has been trained so far, its
+rate is the global rate times min(1, s / W_c), quantised to N_b levels so a
+step sees only a handful of distinct rates (W_c = 20; one frozen BOS token). Adam itself is Algorithm 1 of Kingma and Ba, "Adam: A
 Method for Stochastic Optimization" (ICLR 2015):
 
     t  = s + 1

@@ -5,11 +5,11 @@ call or execute this module; only the tests use it. It shares no code with
 the HIP library.
 
 What is computed (paper: paragraphs "Budget Manager" and "Pool rotation";
-hyperparameter table: B = 20, R = 10, phi = 0.5, "prioritize least
-trained"): a GPU pool holds B of the N cartridges; every R optimizer steps a
-fraction phi of the pool is evicted and replaced by offloaded cartridges,
-preferring those that have received the fewest optimizer steps. Offloaded
-cartridges receive no gradient.
+hyperparameter table: B = 20, R = 10, phi = 0.5, least-trained priority):
+B of the N cartridges sit on the GPU at a time. After every R optimizer
+steps, phi B of them go back to host memory and as many offloaded ones come
+in, the ones trained least so far first. A cartridge off the GPU gets no
+gradient while it is away.
 
 Readings where the paper is silent: n = min(floor(phi B), N - B) cartridges
 swap per rotation; the evicted ones are the active cartridges with the most
