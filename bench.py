@@ -156,6 +156,8 @@ def main():
                     help="time one paged decode step of the retrieval mix (64 requests x 4 cartridges)")
     ap.add_argument("--pool", action="store_true",
                     help="time training steps (packed attention fwd+bwd, Adam) through the budget manager")
+    ap.add_argument("--moment-dir", default=None,
+                    help="--pool: directory of the moment file tier (default: the temporary directory)")
     ap.add_argument("--stage", action="store_true",
                     help="time the forward-only retrieval mix with the pool's second half staged "
                          "host->HBM (cas_cartridge_stage) on a side stream, overlapped with compute")
@@ -720,7 +722,10 @@ def run_pool(args):
     (the packed layout's samples, their cartridge slots mapped onto the active
     set), the fused Adam step, and cas_pool_end_step. The same loop with
     phi = 0 (no rotation) gives the cost of the rotations' copies, which run
-    on the pool's stream behind the compute."""
+    on the pool's stream behind the compute. The rotating loop runs twice:
+    with the offloaded cartridges' Adam moments in pinned host memory, and
+    with them in a file under --moment-dir (the NVMe tier; its reads and
+    writes run on the pool's thread)."""
     import numpy as np
     import torch
     import casgen
@@ -737,10 +742,14 @@ def run_pool(args):
     lse = torch.empty((wl.num_q_heads, sum(wl.row_lens)), dtype=torch.float32, device="cuda")
     dks, dvs = torch.empty_like(ks), torch.empty_like(vs)
     cfg = dict(lr=0.05, beta1=0.9, beta2=0.999, eps=1e-8, warmup_steps=20, warmup_buckets=4)
+    import tempfile
+    mdir = args.moment_dir or tempfile.gettempdir()
     res = {}
     steps = args.steps if args.steps >= 20 else 40
-    for phi in (0.5, 0.0):
-        pl = cas.CartridgePool(lens, Hkv, D, 20, 10, phi, frozen_tokens=1)
+    for key in ("file", 0.5, 0.0):
+        phi = 0.5 if key == "file" else key
+        pl = cas.CartridgePool(lens, Hkv, D, 20, 10, phi, frozen_tokens=1,
+                               moment_dir=mdir if key == "file" else None)
         for c, L in enumerate(lens):
             h = pl.host(c)
             for i, name in enumerate(("k", "v")):
@@ -765,9 +774,10 @@ def run_pool(args):
         for _ in range(steps):
             step()
         torch.cuda.synchronize()
-        res[phi] = (time.perf_counter() - t0) * 1e3 / steps
+        res[key] = (time.perf_counter() - t0) * 1e3 / steps
         pl.flush()
         pl.close()
+        log(f"pool {key}: {res[key]:.3f} ms per step")
     per_cart = [L * Hkv * D * (2 * 2 + 4 * 4) for L in lens]
     moved = 2 * 10 * (sum(per_cart) / len(per_cart))         # 10 evicted + 10 admitted per rotation
     out = {
@@ -781,6 +791,12 @@ def run_pool(args):
         "ms_per_step_without_rotation": res[0.0],
         "rotation_overhead_frac": res[0.5] / res[0.0] - 1.0,
         "bytes_moved_per_rotation": moved,
+        "moment_file_tier": {"ms_per_step": res["file"], "overhead_frac": res["file"] / res[0.0] - 1.0,
+                             "directory": mdir,
+                             "file_bytes_per_rotation": 2 * 10 * sum(L * Hkv * D * 16 for L in lens) / len(lens),
+                             "pinned_host_bytes": {"host_tier": sum(per_cart),
+                                                   "file_tier": sum(L * Hkv * D * 4 for L in lens)
+                                                   + 3 * 10 * 4 * max(lens) * Hkv * D * 4}},
         "roofline": None, "cpu_baseline": None,
     }
     print(json.dumps(out), flush=True)

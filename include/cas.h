@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define CAS_ABI_VERSION 3
+#define CAS_ABI_VERSION 4
 
 /* Bytes of the device scratch each GPU holds for cas_prefix_attn_fwd_noalloc. */
 #define CAS_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
@@ -51,7 +51,8 @@ typedef enum {
   CAS_ERR_ALIGNMENT = 3,        /* pointer or stride not a multiple of 16 bytes */
   CAS_ERR_NOT_PINNED = 4,       /* staging source is pageable host memory */
   CAS_ERR_WORKSPACE = 5,        /* workspace NULL or smaller than the size query returned */
-  CAS_ERR_HIP = 6               /* a HIP runtime call failed; see cas_last_error_message */
+  CAS_ERR_HIP = 6,              /* a HIP runtime call failed; see cas_last_error_message */
+  CAS_ERR_IO = 7                /* a file operation of the pool's moment tier failed */
 } cas_status_t;
 
 typedef enum {
@@ -325,11 +326,24 @@ cas_status_t cas_paged_decode_fwd(const cas_decode_problem_t *p, const void *q, 
 /*
  * Budget manager (paper: paragraphs "Budget Manager" and "Pool rotation";
  * hyperparameter table: budget B = 20, rotation interval R = 10, swap
- * fraction phi = 0.5, least-trained cartridges first). The pool owns a
- * pinned host copy of every cartridge (bf16 K/V, fp32 Adam moments, step
- * count) and B active device slots, plus floor(phi * B) staging slots into
- * which the next rotation's cartridges are copied ahead of time on the
- * pool's own stream while the current ones train.
+ * fraction phi = 0.5, least-trained cartridges first, Adam moments of
+ * CPU-resident cartridges offloaded to NVMe). The pool owns a pinned host
+ * copy of every cartridge's bf16 K/V and step count, and B active device
+ * slots, plus floor(phi * B) staging slots into which the next rotation's
+ * cartridges are copied ahead of time on the pool's own stream while the
+ * current ones train.
+ *
+ * The fp32 Adam moments of the cartridges that are not on the GPU live in
+ * one of two tiers: pinned host memory next to their K/V (moment_dir NULL),
+ * or a file on a local (NVMe) file system (moment_dir names its directory:
+ * the pool creates an unnamed file there, removed when the pool is
+ * destroyed or the process ends, and keeps in pinned memory only two sets
+ * of floor(phi * B) (at least one) moment buffers for the cartridges in
+ * transit). The file tier's reads and writes run on a pool thread: an
+ * eviction's moments are written after their copy back has landed, and the
+ * next admissions' moments are read and copied to the GPU ahead of the
+ * rotation that admits them, overlapped with the training steps between
+ * rotations.
  *
  * Rotation, after every R-th cas_pool_end_step: the n = min(floor(phi * B),
  * N - B) active cartridges with the most optimizer steps (ties: lower id)
@@ -345,9 +359,11 @@ cas_status_t cas_paged_decode_fwd(const cas_decode_problem_t *p, const void *q, 
  * active set (cas_pool_active: device views of K/V, their gradient buffers
  * dk/dv, moments and step counts, ready for cas_cartridge_adam) and call
  * cas_pool_end_step after the optimizer step. cas_pool_flush copies every
- * active cartridge back and waits, after which all host copies are current.
- * Calls on one pool must not overlap; streams are the caller's except the
- * pool's own copy stream (default priority).
+ * active cartridge back and waits, after which all host copies (and the
+ * moment file) are current. Calls on one pool must not overlap; streams are
+ * the caller's except the pool's own copy stream (default priority). A
+ * failed file read or write of the moment tier is reported as CAS_ERR_IO by
+ * the next call on the pool; the pool is then unusable except for destroy.
  */
 typedef struct cas_pool cas_pool_t;
 
@@ -360,18 +376,31 @@ typedef struct {
   int32_t rotate_every;     /* R >= 1 */
   float swap_fraction;      /* phi in [0, 1] */
   int32_t frozen_tokens;    /* reported in the views (BOS: 1) */
+  const char *moment_dir;   /* NULL: moments in pinned host memory; else the file tier's directory */
 } cas_pool_config_t;
 
 cas_status_t cas_pool_plan_rotation(const int32_t *steps, const uint8_t *active, int32_t n, int32_t budget,
                                     float swap_fraction, int32_t *evict, int32_t *admit, int32_t *n_swap);
 cas_status_t cas_pool_create(const cas_pool_config_t *cfg, cas_pool_t **pool);
 cas_status_t cas_pool_destroy(cas_pool_t *pool);
+/* Pinned host views of cartridge cart: k, v, step and frozen tokens, and
+ * with the host moment tier its moments (NULL with the file tier: use
+ * cas_pool_read_moments). */
 cas_status_t cas_pool_host_cartridge(cas_pool_t *pool, int32_t cart, cas_adam_cartridge_t *host_view);
 cas_status_t cas_pool_load(cas_pool_t *pool, void *compute_stream);
 cas_status_t cas_pool_active(cas_pool_t *pool, int32_t *cart_ids, cas_adam_cartridge_t *views, int32_t cap,
                              int32_t *n);
 cas_status_t cas_pool_end_step(cas_pool_t *pool, void *compute_stream);
 cas_status_t cas_pool_flush(cas_pool_t *pool, void *compute_stream);
+/*
+ * Copies cartridge cart's fp32 moments, m1_k, m2_k, m1_v, m2_v (each
+ * [len, num_kv_heads, head_dim], contiguous), into the host buffer dst
+ * (4 * len * num_kv_heads * head_dim floats), from whichever tier holds
+ * them. Current for every cartridge before cas_pool_load and after
+ * cas_pool_flush; during training an active cartridge's copy is the one of
+ * its last admission. Waits for the pool's pending file I/O.
+ */
+cas_status_t cas_pool_read_moments(cas_pool_t *pool, int32_t cart, float *dst);
 
 /* Static description of a status code. */
 const char *cas_status_string(cas_status_t s);

@@ -355,16 +355,19 @@ class _DevArray:
 
 
 class CartridgePool:
-    """Budget manager (cas_pool_*): pinned host copies of every cartridge, B
-    active device slots and prefetched rotations."""
+    """Budget manager (cas_pool_*): pinned host copies of every cartridge's
+    K/V, B active device slots and prefetched rotations. The Adam moments of
+    offloaded cartridges stay in pinned host memory, or with ``moment_dir``
+    in a file in that directory (the NVMe tier)."""
 
     def __init__(self, lens: Sequence[int], num_kv_heads: int, head_dim: int, budget: int, rotate_every: int,
-                 swap_fraction: float, frozen_tokens: int = 1):
+                 swap_fraction: float, frozen_tokens: int = 1, moment_dir: Optional[str] = None):
         self.lens = [int(x) for x in lens]
         self.Hkv, self.D = num_kv_heads, head_dim
         self._lens = (ctypes.c_int64 * len(lens))(*self.lens)
         cfg = _lib.PoolConfig(len(lens), ctypes.cast(self._lens, ctypes.POINTER(ctypes.c_int64)), num_kv_heads,
-                              head_dim, budget, rotate_every, swap_fraction, frozen_tokens)
+                              head_dim, budget, rotate_every, swap_fraction, frozen_tokens,
+                              None if moment_dir is None else str(moment_dir).encode())
         h = ctypes.c_void_p()
         _check(load().cas_pool_create(ctypes.byref(cfg), ctypes.byref(h)))
         self.h = h
@@ -381,8 +384,9 @@ class CartridgePool:
             pass
 
     def host(self, cart: int) -> dict:
-        """numpy views of cartridge `cart`'s pinned host copy: k, v (bf16 bits as
-        int16), m1_k, m2_k, m1_v, m2_v (float32), and its step count."""
+        """Cartridge `cart` on the host: numpy views of its pinned k and v (bf16
+        bits as int16; writable), a copy of its moments m1_k, m2_k, m1_v, m2_v
+        (float32, from whichever tier holds them), and its step count."""
         import numpy as np
         v = _lib.AdamCartridge()
         _check(load().cas_pool_host_cartridge(self.h, int(cart), ctypes.byref(v)))
@@ -392,9 +396,10 @@ class CartridgePool:
         for name in ("k", "v"):
             out[name] = np.ctypeslib.as_array(ctypes.cast(getattr(v, name), ctypes.POINTER(ctypes.c_int16)),
                                               (n,)).reshape(shp)
-        for name in ("m1_k", "m2_k", "m1_v", "m2_v"):
-            out[name] = np.ctypeslib.as_array(ctypes.cast(getattr(v, name), ctypes.POINTER(ctypes.c_float)),
-                                              (n,)).reshape(shp)
+        m = np.empty(4 * n, dtype=np.float32)
+        _check(load().cas_pool_read_moments(self.h, int(cart), m.ctypes.data_as(ctypes.POINTER(ctypes.c_float))))
+        for i, name in enumerate(("m1_k", "m2_k", "m1_v", "m2_v")):
+            out[name] = m[i * n:(i + 1) * n].reshape(shp)
         out["step"] = int(v.step)
         return out
 

@@ -13,6 +13,7 @@ CAS_ERR_ALIGNMENT = 3
 CAS_ERR_NOT_PINNED = 4
 CAS_ERR_WORKSPACE = 5
 CAS_ERR_HIP = 6
+CAS_ERR_IO = 7
 
 CAS_DTYPE_BF16 = 0
 CAS_DTYPE_FP32 = 1
@@ -26,7 +27,7 @@ EXPORTS = [
     "cas_cartridge_adam", "cas_paged_decode_workspace_size", "cas_paged_decode_fwd",
     "cas_pool_plan_rotation", "cas_pool_create", "cas_pool_destroy", "cas_pool_host_cartridge",
     "cas_pool_load", "cas_pool_active", "cas_pool_end_step", "cas_pool_flush",
-    "cas_prefix_attn_fwd_noalloc",
+    "cas_prefix_attn_fwd_noalloc", "cas_pool_read_moments",
 ]
 
 
@@ -70,7 +71,7 @@ class PoolConfig(ctypes.Structure):
     _fields_ = [("num_cartridges", ctypes.c_int32), ("lens", ctypes.POINTER(ctypes.c_int64)),
                 ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("budget", ctypes.c_int32),
                 ("rotate_every", ctypes.c_int32), ("swap_fraction", ctypes.c_float),
-                ("frozen_tokens", ctypes.c_int32)]
+                ("frozen_tokens", ctypes.c_int32), ("moment_dir", ctypes.c_char_p)]
 
 
 class StageCopy(ctypes.Structure):
@@ -93,7 +94,7 @@ class KernelTime(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 48), ("launches", ctypes.c_int32), ("total_ms", ctypes.c_double)]
 
 
-ABI_VERSION = 3   # CAS_ABI_VERSION of include/cas.h (q_offsets; the no-allocation forward)
+ABI_VERSION = 4   # CAS_ABI_VERSION of include/cas.h (q_offsets, no-allocation forward, moment file tier)
 
 _lib = None
 
@@ -135,6 +136,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.cas_pool_active.argtypes = [vp, P(i32), P(AdamCartridge), i32, P(i32)]
     lib.cas_pool_end_step.argtypes = [vp, vp]
     lib.cas_pool_flush.argtypes = [vp, vp]
+    lib.cas_pool_read_moments.argtypes = [vp, i32, P(ctypes.c_float)]
     lib.cas_set_tuning.argtypes = [P(Tuning)]
     lib.cas_get_tuning.argtypes = [P(Tuning)]
     lib.cas_plan_info.argtypes = [P(Problem), P(PlanInfo)]
@@ -148,7 +150,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                  "cas_cartridge_adam_workspace_size", "cas_cartridge_adam",
                  "cas_paged_decode_workspace_size", "cas_paged_decode_fwd", "cas_pool_plan_rotation",
                  "cas_pool_create", "cas_pool_destroy", "cas_pool_host_cartridge", "cas_pool_load",
-                 "cas_pool_active", "cas_pool_end_step", "cas_pool_flush"):
+                 "cas_pool_active", "cas_pool_end_step", "cas_pool_flush", "cas_pool_read_moments"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib

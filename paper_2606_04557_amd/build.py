@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libcas.so")
-SOURCES = ["cas_api.cpp", "cas_fwd.hip", "cas_bwd.hip", "cas_bf16.hip", "cas_adam.hip", "cas_decode.hip",
+SOURCES = ["cas_api.cpp", "cas_pool.cpp", "cas_fwd.hip", "cas_bwd.hip", "cas_bf16.hip", "cas_adam.hip", "cas_decode.hip",
            "cas_noalloc.hip"]
 ARCH = "gfx950"
 

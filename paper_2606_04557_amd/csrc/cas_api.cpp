@@ -16,6 +16,7 @@
 #include <vector>
 
 #include "../../include/cas.h"
+#include "cas_host.h"
 #include "cas_internal.h"
 
 using namespace cas;
@@ -832,29 +833,40 @@ cas_status_t build_decode(const cas_decode_problem_t *p, DecodePlan &dp) {
   return CAS_OK;
 }
 
-// ---------------------------------------------------------------------------
-// Budget manager: the rotation policy and the pool's memory and copies.
-// ---------------------------------------------------------------------------
-// Evict the n active cartridges with the most steps, admit the n offloaded
-// ones with the fewest (ties: lower id), n = min(floor(phi * B), offloaded).
-int plan_rotation(const int32_t *steps, const uint8_t *active, int N, int B, float phi, int32_t *evict,
-                  int32_t *admit) {
-  std::vector<int> act, off;
-  for (int c = 0; c < N; ++c) (active[c] ? act : off).push_back(c);
-  const int n = std::min<int>((int)std::floor((double)phi * B + 1e-9), (int)off.size());
-  std::stable_sort(act.begin(), act.end(), [&](int a, int b) { return steps[a] > steps[b]; });
-  std::stable_sort(off.begin(), off.end(), [&](int a, int b) { return steps[a] < steps[b]; });
-  const int m = std::min<int>(n, (int)act.size());
-  for (int i = 0; i < m; ++i) {
-    if (evict) evict[i] = act[i];
-    if (admit) admit[i] = off[i];
-  }
-  return m;
-}
-
 }  // namespace
 
 namespace cas {
+
+cas_status_t set_error(cas_status_t s, const std::string &msg) { return fail(s, msg); }
+
+cas_status_t set_hip_error(const char *what, hipError_t e) { return hip_fail(what, e); }
+
+hipError_t enqueue_copies(const HostCopy *c, int n, hipMemcpyKind kind, hipStream_t s) {
+  const char *run_src = nullptr;
+  char *run_dst = nullptr;
+  size_t run_bytes = 0;
+  auto flush = [&]() -> hipError_t {
+    hipError_t e = hipSuccess;
+    if (run_bytes) e = hipMemcpyAsync(run_dst, run_src, run_bytes, kind, s);
+    run_bytes = 0;
+    return e;
+  };
+  for (int i = 0; i < n; ++i) {
+    if (c[i].bytes == 0) continue;
+    const char *src = (const char *)c[i].src;
+    char *dst = (char *)c[i].dst;
+    if (run_bytes && src == run_src + run_bytes && dst == run_dst + run_bytes) {
+      run_bytes += c[i].bytes;
+      continue;
+    }
+    hipError_t e = flush();
+    if (e != hipSuccess) return e;
+    run_src = src;
+    run_dst = dst;
+    run_bytes = c[i].bytes;
+  }
+  return flush();
+}
 
 cas_status_t prefix_attn_fwd_run(const cas_problem_t *p, const void *q, const void *k_self,
                                  const void *v_self, void *o, float *lse, void *workspace,
@@ -967,62 +979,6 @@ cas_status_t prefix_attn_fwd_run(const cas_problem_t *p, const void *q, const vo
 
 }  // namespace cas
 
-struct cas_pool {
-  int N = 0, Hkv = 0, D = 0, B = 0, R = 1, S = 0, frozen = 0;
-  float phi = 0.0f;
-  std::vector<int64_t> lens;
-  int64_t max_len = 0, tok_el = 0;
-  char *host = nullptr;
-  std::vector<size_t> hoff;
-  char *dev = nullptr;
-  size_t A = 0, M = 0, slot_bytes = 0;       // bf16 tensor, fp32 tensor, slot
-  std::vector<int32_t> steps, slot_cart, active, staging, next_admit;   // slot_cart: cartridge in each slot or -1
-  int64_t step_count = 0;
-  bool loaded = false;
-  hipStream_t side = nullptr;
-  hipEvent_t ev_compute = nullptr, ev_admit = nullptr;
-
-  char *slot_ptr(int slot, int part) const {   // 0 K, 1 V, 2 dK, 3 dV, 4.. moments m1k, m2k, m1v, m2v
-    char *b = dev + (size_t)slot * slot_bytes;
-    return part < 4 ? b + part * A : b + 4 * A + (part - 4) * M;
-  }
-  char *host_ptr(int c, int part) const {     // 0 K, 1 V, 2.. moments
-    const size_t a = (size_t)lens[c] * tok_el * 2, m = (size_t)lens[c] * tok_el * 4;
-    char *b = host + hoff[c];
-    return part < 2 ? b + part * a : b + 2 * a + (part - 2) * m;
-  }
-  // Parameters and moments of cartridge c between its host copy and a slot.
-  hipError_t move(int c, int slot, bool to_device) {
-    const size_t a = (size_t)lens[c] * tok_el * 2, m = (size_t)lens[c] * tok_el * 4;
-    static const int dparts[6] = {0, 1, 4, 5, 6, 7};
-    for (int i = 0; i < 6; ++i) {
-      void *d = slot_ptr(slot, dparts[i]);
-      void *h = host_ptr(c, i);
-      const size_t n = i < 2 ? a : m;
-      hipError_t e = to_device ? hipMemcpyAsync(d, h, n, hipMemcpyHostToDevice, side)
-                               : hipMemcpyAsync(h, d, n, hipMemcpyDeviceToHost, side);
-      if (e != hipSuccess) return e;
-    }
-    return hipSuccess;
-  }
-  // Copies the next admissions into the staging slots (after everything
-  // already queued on the pool's stream) and records ev_admit.
-  hipError_t prefetch() {
-    std::vector<uint8_t> act(N, 0);
-    for (int sl : active) act[slot_cart[sl]] = 1;
-    next_admit.assign(S, -1);
-    const int n = plan_rotation(steps.data(), act.data(), N, B, phi, nullptr, next_admit.data());
-    next_admit.resize(n);
-    for (int i = 0; i < n; ++i) {
-      const int c = next_admit[i], sl = staging[i];
-      slot_cart[sl] = c;
-      hipError_t e = move(c, sl, true);
-      if (e != hipSuccess) return e;
-    }
-    return hipEventRecord(ev_admit, side);
-  }
-};
-
 extern "C" {
 
 int32_t cas_abi_version(void) { return CAS_ABI_VERSION; }
@@ -1036,6 +992,7 @@ const char *cas_status_string(cas_status_t s) {
     case CAS_ERR_NOT_PINNED: return "CAS_ERR_NOT_PINNED";
     case CAS_ERR_WORKSPACE: return "CAS_ERR_WORKSPACE";
     case CAS_ERR_HIP: return "CAS_ERR_HIP";
+    case CAS_ERR_IO: return "CAS_ERR_IO";
   }
   return "CAS_ERR_UNKNOWN";
 }
@@ -1044,204 +1001,6 @@ const char *cas_last_error_message(void) { return g_err.c_str(); }
 
 float cas_adam_lr_scale(int32_t step, int32_t warmup_steps, int32_t warmup_buckets) {
   return lr_scale(step, warmup_steps, warmup_buckets);
-}
-
-cas_status_t cas_pool_plan_rotation(const int32_t *steps, const uint8_t *active, int32_t n, int32_t budget,
-                                    float swap_fraction, int32_t *evict, int32_t *admit, int32_t *n_swap) {
-  if (!steps || !active || !n_swap || n < 1 || budget < 1 || !(swap_fraction >= 0.0f && swap_fraction <= 1.0f))
-    return fail(CAS_ERR_INVALID_ARGUMENT, "bad rotation query");
-  *n_swap = plan_rotation(steps, active, n, budget, swap_fraction, evict, admit);
-  return CAS_OK;
-}
-
-cas_status_t cas_pool_create(const cas_pool_config_t *cfg, cas_pool_t **out) {
-  if (!cfg || !out) return fail(CAS_ERR_INVALID_ARGUMENT, "cfg or out is NULL");
-  *out = nullptr;
-  if (cfg->num_cartridges < 1 || !cfg->lens) return fail(CAS_ERR_INVALID_ARGUMENT, "need >= 1 cartridge and lens");
-  if (cfg->num_kv_heads < 1) return fail(CAS_ERR_INVALID_ARGUMENT, "num_kv_heads must be >= 1");
-  if (cfg->head_dim != 64 && cfg->head_dim != 128) return fail(CAS_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
-  if (cfg->budget < 1 || cfg->budget > cfg->num_cartridges)
-    return fail(CAS_ERR_INVALID_ARGUMENT, "budget must lie in [1, num_cartridges]");
-  if (cfg->rotate_every < 1 || !(cfg->swap_fraction >= 0.0f && cfg->swap_fraction <= 1.0f) || cfg->frozen_tokens < 0)
-    return fail(CAS_ERR_INVALID_ARGUMENT, "rotate_every >= 1, swap_fraction in [0, 1], frozen_tokens >= 0");
-  std::unique_ptr<cas_pool> p(new cas_pool());
-  p->N = cfg->num_cartridges;
-  p->Hkv = cfg->num_kv_heads;
-  p->D = cfg->head_dim;
-  p->B = cfg->budget;
-  p->R = cfg->rotate_every;
-  p->phi = cfg->swap_fraction;
-  p->frozen = cfg->frozen_tokens;
-  p->tok_el = (int64_t)p->Hkv * p->D;
-  p->S = std::min<int>((int)std::floor((double)p->phi * p->B + 1e-9), p->N - p->B);
-  size_t hb = 0;
-  for (int c = 0; c < p->N; ++c) {
-    const int64_t L = cfg->lens[c];
-    if (L < 1 || L > (1 << 30)) return fail(CAS_ERR_INVALID_ARGUMENT, "cartridge lengths must lie in [1, 2^30]");
-    p->lens.push_back(L);
-    p->max_len = std::max(p->max_len, L);
-    p->hoff.push_back(hb);
-    hb += align_up((size_t)L * p->tok_el * (2 * 2 + 4 * 4), 256);
-  }
-  p->A = align_up((size_t)p->max_len * p->tok_el * 2, 256);
-  p->M = align_up((size_t)p->max_len * p->tok_el * 4, 256);
-  p->slot_bytes = 4 * p->A + 4 * p->M;
-  hipError_t e = hipHostMalloc((void **)&p->host, hb, hipHostMallocDefault);
-  if (e != hipSuccess) { p->host = nullptr; return hip_fail("hipHostMalloc", e); }
-  std::memset(p->host, 0, hb);
-  e = hipMalloc((void **)&p->dev, p->slot_bytes * (size_t)(p->B + p->S));
-  if (e != hipSuccess) { p->dev = nullptr; hipHostFree(p->host); p->host = nullptr; return hip_fail("hipMalloc", e); }
-  auto cleanup = [&]() {
-    if (p->side) hipStreamDestroy(p->side);
-    if (p->ev_compute) hipEventDestroy(p->ev_compute);
-    if (p->ev_admit) hipEventDestroy(p->ev_admit);
-    hipFree(p->dev);
-    hipHostFree(p->host);
-  };
-  if ((e = hipStreamCreateWithFlags(&p->side, hipStreamNonBlocking)) != hipSuccess ||
-      (e = hipEventCreateWithFlags(&p->ev_compute, hipEventDisableTiming)) != hipSuccess ||
-      (e = hipEventCreateWithFlags(&p->ev_admit, hipEventDisableTiming)) != hipSuccess) {
-    cleanup();
-    return hip_fail("pool stream/event", e);
-  }
-  p->steps.assign(p->N, 0);
-  p->slot_cart.assign(p->B + p->S, -1);
-  *out = p.release();
-  return CAS_OK;
-}
-
-cas_status_t cas_pool_destroy(cas_pool_t *p) {
-  if (!p) return CAS_OK;
-  if (p->side) (void)hipStreamSynchronize(p->side);
-  if (p->side) hipStreamDestroy(p->side);
-  if (p->ev_compute) hipEventDestroy(p->ev_compute);
-  if (p->ev_admit) hipEventDestroy(p->ev_admit);
-  if (p->dev) hipFree(p->dev);
-  if (p->host) hipHostFree(p->host);
-  delete p;
-  return CAS_OK;
-}
-
-cas_status_t cas_pool_host_cartridge(cas_pool_t *p, int32_t c, cas_adam_cartridge_t *v) {
-  if (!p || !v || c < 0 || c >= p->N) return fail(CAS_ERR_INVALID_ARGUMENT, "bad pool, view or cartridge");
-  *v = cas_adam_cartridge_t{};
-  v->k = p->host_ptr(c, 0);
-  v->v = p->host_ptr(c, 1);
-  v->m1_k = (float *)p->host_ptr(c, 2);
-  v->m2_k = (float *)p->host_ptr(c, 3);
-  v->m1_v = (float *)p->host_ptr(c, 4);
-  v->m2_v = (float *)p->host_ptr(c, 5);
-  v->len = p->lens[c];
-  v->stride_tok = p->tok_el;
-  v->stride_head = p->D;
-  v->step = p->steps[c];
-  v->frozen_tokens = p->frozen;
-  return CAS_OK;
-}
-
-cas_status_t cas_pool_load(cas_pool_t *p, void *compute_stream) {
-  if (!p) return fail(CAS_ERR_INVALID_ARGUMENT, "pool is NULL");
-  if (p->loaded) return fail(CAS_ERR_INVALID_ARGUMENT, "pool already loaded");
-  // Active set: the B least-trained cartridges (ties: lower id).
-  std::vector<int> order(p->N);
-  for (int c = 0; c < p->N; ++c) order[c] = c;
-  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return p->steps[a] < p->steps[b]; });
-  p->active.clear();
-  p->staging.clear();
-  for (int i = 0; i < p->B; ++i) {
-    p->slot_cart[i] = order[i];
-    p->active.push_back(i);
-    hipError_t e = p->move(order[i], i, true);
-    if (e != hipSuccess) return hip_fail("pool load", e);
-  }
-  for (int i = 0; i < p->S; ++i) p->staging.push_back(p->B + i);
-  hipError_t e = hipEventRecord(p->ev_compute, p->side);   // active set landed
-  if (e != hipSuccess) return hip_fail("hipEventRecord", e);
-  e = hipStreamWaitEvent((hipStream_t)compute_stream, p->ev_compute, 0);
-  if (e != hipSuccess) return hip_fail("hipStreamWaitEvent", e);
-  e = p->prefetch();
-  if (e != hipSuccess) return hip_fail("pool prefetch", e);
-  p->loaded = true;
-  return CAS_OK;
-}
-
-cas_status_t cas_pool_active(cas_pool_t *p, int32_t *cart_ids, cas_adam_cartridge_t *views, int32_t cap, int32_t *n) {
-  if (!p || !n || !p->loaded) return fail(CAS_ERR_INVALID_ARGUMENT, "pool is NULL or not loaded");
-  *n = (int32_t)p->active.size();
-  for (int i = 0; i < (int)p->active.size() && i < cap; ++i) {
-    const int sl = p->active[i], c = p->slot_cart[sl];
-    if (cart_ids) cart_ids[i] = c;
-    if (!views) continue;
-    cas_adam_cartridge_t &v = views[i];
-    v = cas_adam_cartridge_t{};
-    v.k = p->slot_ptr(sl, 0);
-    v.v = p->slot_ptr(sl, 1);
-    v.dk = p->slot_ptr(sl, 2);
-    v.dv = p->slot_ptr(sl, 3);
-    v.m1_k = (float *)p->slot_ptr(sl, 4);
-    v.m2_k = (float *)p->slot_ptr(sl, 5);
-    v.m1_v = (float *)p->slot_ptr(sl, 6);
-    v.m2_v = (float *)p->slot_ptr(sl, 7);
-    v.len = p->lens[c];
-    v.stride_tok = p->tok_el;
-    v.stride_head = p->D;
-    v.step = p->steps[c];
-    v.frozen_tokens = p->frozen;
-  }
-  return CAS_OK;
-}
-
-cas_status_t cas_pool_end_step(cas_pool_t *p, void *compute_stream) {
-  if (!p || !p->loaded) return fail(CAS_ERR_INVALID_ARGUMENT, "pool is NULL or not loaded");
-  for (int sl : p->active) ++p->steps[p->slot_cart[sl]];
-  ++p->step_count;
-  if (p->S == 0 || p->step_count % p->R != 0) return CAS_OK;
-  hipStream_t cs = (hipStream_t)compute_stream;
-  // Evict after the compute stream's last use of the active set.
-  std::vector<uint8_t> act(p->N, 0);
-  for (int sl : p->active) act[p->slot_cart[sl]] = 1;
-  std::vector<int32_t> ev(p->S);
-  const int n = plan_rotation(p->steps.data(), act.data(), p->N, p->B, p->phi, ev.data(), nullptr);
-  if (n != (int)p->next_admit.size()) return fail(CAS_ERR_INVALID_ARGUMENT, "rotation size changed");
-  hipError_t e = hipEventRecord(p->ev_compute, cs);
-  if (e == hipSuccess) e = hipStreamWaitEvent(p->side, p->ev_compute, 0);
-  if (e != hipSuccess) return hip_fail("pool rotation sync", e);
-  std::vector<int32_t> freed;
-  for (int i = 0; i < n; ++i) {
-    const int c = ev[i];
-    int sl = -1;
-    for (int a : p->active)
-      if (p->slot_cart[a] == c) sl = a;
-    e = p->move(c, sl, false);
-    if (e != hipSuccess) return hip_fail("pool eviction", e);
-    p->slot_cart[sl] = -1;
-    freed.push_back(sl);
-  }
-  // The prefetched cartridges join the active set once their copies landed.
-  std::vector<int32_t> next_active;
-  for (int a : p->active)
-    if (std::find(freed.begin(), freed.end(), a) == freed.end()) next_active.push_back(a);
-  for (int i = 0; i < n; ++i) next_active.push_back(p->staging[i]);
-  e = hipStreamWaitEvent(cs, p->ev_admit, 0);
-  if (e != hipSuccess) return hip_fail("hipStreamWaitEvent", e);
-  std::vector<int32_t> next_staging = freed;
-  for (int i = n; i < (int)p->staging.size(); ++i) next_staging.push_back(p->staging[i]);
-  p->active = next_active;
-  p->staging = next_staging;
-  e = p->prefetch();   // queued after the evictions on the pool's stream
-  if (e != hipSuccess) return hip_fail("pool prefetch", e);
-  return CAS_OK;
-}
-
-cas_status_t cas_pool_flush(cas_pool_t *p, void *compute_stream) {
-  if (!p || !p->loaded) return fail(CAS_ERR_INVALID_ARGUMENT, "pool is NULL or not loaded");
-  hipError_t e = hipEventRecord(p->ev_compute, (hipStream_t)compute_stream);
-  if (e == hipSuccess) e = hipStreamWaitEvent(p->side, p->ev_compute, 0);
-  for (int sl : p->active)
-    if (e == hipSuccess) e = p->move(p->slot_cart[sl], sl, false);
-  if (e == hipSuccess) e = hipStreamSynchronize(p->side);
-  if (e != hipSuccess) return hip_fail("pool flush", e);
-  return CAS_OK;
 }
 
 cas_status_t cas_paged_decode_workspace_size(const cas_decode_problem_t *p, size_t *bytes) {
@@ -1565,36 +1324,11 @@ cas_status_t cas_cartridge_stage(const cas_stage_copy_t *copies, int32_t n, void
       return fail(CAS_ERR_INVALID_ARGUMENT, "copy " + std::to_string(i) + ": dev_dst is not device memory");
     }
   }
-  // Runs of consecutive entries that continue both the previous source and
-  // the previous destination go out as one transfer (fewer, larger DMA
-  // transfers keep the host link busier); the order of the bytes is unchanged.
+  std::vector<HostCopy> list((size_t)n);
+  for (int i = 0; i < n; ++i) list[i] = {copies[i].host_src, copies[i].dev_dst, copies[i].bytes};
   hipStream_t s = (hipStream_t)side_stream;
-  const char *run_src = nullptr;
-  char *run_dst = nullptr;
-  size_t run_bytes = 0;
-  auto flush = [&]() -> hipError_t {
-    hipError_t e = hipSuccess;
-    if (run_bytes) e = hipMemcpyAsync(run_dst, run_src, run_bytes, hipMemcpyHostToDevice, s);
-    run_bytes = 0;
-    return e;
-  };
-  for (int i = 0; i < n; ++i) {
-    const cas_stage_copy_t &c = copies[i];
-    if (c.bytes == 0) continue;
-    const char *src = (const char *)c.host_src;
-    char *dst = (char *)c.dev_dst;
-    if (run_bytes && src == run_src + run_bytes && dst == run_dst + run_bytes) {
-      run_bytes += c.bytes;
-      continue;
-    }
-    hipError_t e = flush();
-    if (e != hipSuccess) return hip_fail("hipMemcpyAsync", e);
-    run_src = src;
-    run_dst = dst;
-    run_bytes = c.bytes;
-  }
   {
-    hipError_t e = flush();
+    hipError_t e = enqueue_copies(list.data(), n, hipMemcpyHostToDevice, s);
     if (e != hipSuccess) return hip_fail("hipMemcpyAsync", e);
   }
   if (done_event) {

@@ -27,7 +27,7 @@ def test_exports_match_header(lib):
     assert declared == sorted(_lib.EXPORTS)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.cas_abi_version() == _lib.ABI_VERSION == 3
+    assert lib.cas_abi_version() == _lib.ABI_VERSION == 4
     assert lib.cas_status_string(_lib.CAS_ERR_NOT_PINNED) == b"CAS_ERR_NOT_PINNED"
 
 
@@ -387,6 +387,14 @@ def test_pool_config_validation(lib):
     assert lib.cas_pool_create(ctypes.byref(cfg), ctypes.byref(h)) == _lib.CAS_ERR_INVALID_ARGUMENT
     assert lib.cas_pool_active(None, None, None, 0, ctypes.byref(ctypes.c_int32())) == _lib.CAS_ERR_INVALID_ARGUMENT
     assert lib.cas_pool_destroy(None) == _lib.CAS_OK
+    # The moment file tier: a directory that cannot hold the file is refused
+    # (before any device call) with CAS_ERR_IO.
+    cfg = _lib.PoolConfig(3, ctypes.cast(lens, P), 2, 64, 2, 10, 0.5, 1, b"/nonexistent/cas-moments")
+    assert lib.cas_pool_create(ctypes.byref(cfg), ctypes.byref(h)) == _lib.CAS_ERR_IO
+    assert "/nonexistent/cas-moments" in _msg(lib) and not h.value
+    assert lib.cas_status_string(_lib.CAS_ERR_IO) == b"CAS_ERR_IO"
+    buf = (ctypes.c_float * 4)()
+    assert lib.cas_pool_read_moments(None, 0, buf) == _lib.CAS_ERR_INVALID_ARGUMENT
 
 
 def test_noalloc_forward_validation(lib):
