@@ -4,7 +4,9 @@ from __future__ import annotations
 import ctypes
 import os
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcas.so")
+# The in-tree build; CAS_LIB names another build of the same library (the
+# host-sanitized one that the host-side tests can run against).
+LIB_PATH = os.environ.get("CAS_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcas.so")
 
 CAS_OK = 0
 CAS_ERR_INVALID_ARGUMENT = 1

@@ -1,6 +1,15 @@
 """Build libcas.so (HIP for gfx950) in-tree with hipcc.
 
     python -m paper_2606_04557_amd.build
+    python -m paper_2606_04557_amd.build --sanitize
+
+--sanitize builds _build_san/libcas_san.so with AddressSanitizer and
+UndefinedBehaviorSanitizer on the host code only (device code is compiled as
+usual), for running the host-side tests (validation, planning) under the
+sanitizers without a GPU:
+
+    CAS_LIB=_build_san/libcas_san.so LD_PRELOAD=<clang asan runtime>:$LD_PRELOAD \
+        ASAN_OPTIONS=detect_leaks=0 python -m pytest tests/test_host_lib.py
 """
 from __future__ import annotations
 
@@ -16,6 +25,12 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libcas.so")
+SAN_DIR = os.path.join(ROOT, "_build_san")
+SAN_LIB_PATH = os.path.join(SAN_DIR, "libcas_san.so")
+# Host-only sanitizers: each -fsanitize= goes to the host compilation alone.
+SAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+             "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer",
+             "-O1", "-g"]
 SOURCES = ["cas_api.cpp", "cas_pool.cpp", "cas_fwd.hip", "cas_bwd.hip", "cas_bf16.hip", "cas_adam.hip", "cas_decode.hip",
            "cas_noalloc.hip"]
 ARCH = "gfx950"
@@ -54,27 +69,33 @@ def _run(cmd):
     return out
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source and link libcas.so; returns its path."""
+def build(verbose: bool = False, sanitize: bool = False) -> str:
+    """Compile every source and link libcas.so (or, with sanitize, the
+    host-sanitized _build_san/libcas_san.so); returns its path."""
     cc = hipcc()
-    os.makedirs(BUILD_DIR, exist_ok=True)
+    bdir, lib = (SAN_DIR, SAN_LIB_PATH) if sanitize else (BUILD_DIR, LIB_PATH)
+    extra = SAN_FLAGS if sanitize else []
+    os.makedirs(bdir, exist_ok=True)
     objs = []
     jobs = []
     for src in SOURCES:
-        obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
+        obj = os.path.join(bdir, os.path.splitext(src)[0] + ".o")
         objs.append(obj)
-        jobs.append([cc, *COMMON_FLAGS, *FILE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj])
+        jobs.append([cc, *COMMON_FLAGS, *FILE_FLAGS.get(src, []), *extra, "-c", os.path.join(CSRC, src),
+                     "-o", obj])
     with concurrent.futures.ThreadPoolExecutor(max_workers=len(jobs)) as ex:
         for out in ex.map(_run, jobs):
             if verbose and out.strip():
                 print(out)
-    tmp = LIB_PATH + ".tmp"
-    out = _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
+    tmp = lib + ".tmp"
+    link_extra = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                  "-shared-libasan"] if sanitize else []
+    out = _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *link_extra, "-o", tmp, *objs])
     if verbose and out.strip():
         print(out)
-    os.replace(tmp, LIB_PATH)
-    return LIB_PATH
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, sanitize="--sanitize" in sys.argv))

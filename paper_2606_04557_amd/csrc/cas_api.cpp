@@ -102,6 +102,7 @@ struct Plan {
   int64_t order_cap = 0;          // order entries with every self tile
   int64_t max_prefix = 0;
   int fwd_splits = 1, dq_splits = 1;
+  int xcds = 8;                   // XCDs of the device (workgroup order of the bf16 kernels)
   int nqblk_fwd = 0, nqblk_dq = 0;
   int cart_tiles = 0;
   bool want_self_grad = false;
@@ -111,11 +112,41 @@ struct Plan {
   size_t off_nd = 0, off_lse2 = 0, off_part_dq = 0, off_qT = 0, off_doT = 0, ws_bwd = 0;
 };
 
-constexpr int kTargetWgs = 512;   // two workgroups per CU on a 256-CU MI355X
+// Compute units and XCDs of the current device, looked up once per device.
+// gfx950 has 32 CUs per XCD (256 and 8 on a whole MI355X; a partition shows
+// fewer). Without a device (planning-only use) the whole MI355X is assumed.
+struct Topology {
+  int cus = 256, xcds = 8;
+};
+std::mutex g_topo_mu;
+std::map<int, Topology> g_topo;
+Topology device_topology() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return Topology{};
+  }
+  std::lock_guard<std::mutex> lk(g_topo_mu);
+  auto it = g_topo.find(dev);
+  if (it != g_topo.end()) return it->second;
+  Topology t;
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0) {
+    t.cus = cus;
+    t.xcds = std::max(1, cus / 32);
+  } else {
+    (void)hipGetLastError();
+  }
+  g_topo.emplace(dev, t);
+  return t;
+}
 
-int auto_splits(int64_t base_wgs, int64_t min_row_tiles) {
-  if (base_wgs >= (kTargetWgs * 3) / 4) return 1;
-  int64_t s = ceil_div(kTargetWgs, std::max<int64_t>(1, base_wgs));
+// Key-axis splits for a grid of base_wgs workgroups: aim at two workgroups
+// per compute unit.
+int auto_splits(int64_t base_wgs, int64_t min_row_tiles, int cus) {
+  const int64_t target = 2 * (int64_t)cus;
+  if (base_wgs >= (target * 3) / 4) return 1;
+  int64_t s = ceil_div(target, std::max<int64_t>(1, base_wgs));
   s = std::min<int64_t>(s, std::max<int64_t>(1, min_row_tiles / 8));
   return (int)std::max<int64_t>(1, std::min<int64_t>(s, kMaxSplits));
 }
@@ -125,7 +156,12 @@ int auto_splits(int64_t base_wgs, int64_t min_row_tiles) {
 // key-axis splits. Pure host code.
 cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl, int fwd_split_cap = 0) {
   if (!p) return fail(CAS_ERR_INVALID_ARGUMENT, "problem is NULL");
-  if (p->dtype != CAS_DTYPE_BF16 && p->dtype != CAS_DTYPE_FP32)
+  // The caller may pass any integer through the C ABI: read the field's
+  // bits as an integer (loading an out-of-range enumerator is undefined).
+  int32_t dtype_raw = 0;
+  static_assert(sizeof(p->dtype) == sizeof(dtype_raw), "cas_dtype_t is 32-bit");
+  std::memcpy(&dtype_raw, &p->dtype, sizeof(dtype_raw));
+  if (dtype_raw != CAS_DTYPE_BF16 && dtype_raw != CAS_DTYPE_FP32)
     return fail(CAS_ERR_INVALID_ARGUMENT, "unknown dtype");
   if (p->batch < 1 || p->num_kv_heads < 1 || p->group_size < 1 || p->head_dim < 1)
     return fail(CAS_ERR_INVALID_ARGUMENT, "batch, num_kv_heads, group_size and head_dim must be >= 1");
@@ -178,8 +214,8 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl, int fwd_spli
   if (nent > (1 << 20)) return fail(CAS_ERR_UNSUPPORTED, "more than 2^20 segment entries");
   if (nent > 0 && !p->segments) return fail(CAS_ERR_INVALID_ARGUMENT, "segments is NULL");
 
-  pl.dt = p->dtype == CAS_DTYPE_BF16 ? kBF16 : kFP32;
-  pl.esize = p->dtype == CAS_DTYPE_BF16 ? 2 : 4;
+  pl.dt = dtype_raw == CAS_DTYPE_BF16 ? kBF16 : kFP32;
+  pl.esize = dtype_raw == CAS_DTYPE_BF16 ? 2 : 4;
   pl.B = p->batch;
   pl.Hkv = p->num_kv_heads;
   pl.g = p->group_size;
@@ -271,9 +307,12 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl, int fwd_spli
     base_fwd += Hkv * ceil_div((int64_t)pl.len[b] * pl.g, rpw_fwd);
     base_dq += Hkv * ceil_div((int64_t)pl.len[b] * pl.g, rpw_dq);
   }
-  pl.fwd_splits = tu.fwd_splits > 0 ? std::min(tu.fwd_splits, kMaxSplits) : auto_splits(base_fwd, min_row_tiles);
+  const Topology topo = device_topology();
+  pl.xcds = topo.xcds;
+  pl.fwd_splits = tu.fwd_splits > 0 ? std::min(tu.fwd_splits, kMaxSplits)
+                                    : auto_splits(base_fwd, min_row_tiles, topo.cus);
   if (fwd_split_cap > 0) pl.fwd_splits = std::min(pl.fwd_splits, fwd_split_cap);
-  pl.dq_splits = tu.dq_splits > 0 ? std::min(tu.dq_splits, kMaxSplits) : auto_splits(base_dq, min_row_tiles);
+  pl.dq_splits = tu.dq_splits > 0 ? std::min(tu.dq_splits, kMaxSplits) : auto_splits(base_dq, min_row_tiles, topo.cus);
   if ((int64_t)pl.B * Hkv * pl.nqblk_fwd * pl.fwd_splits > INT32_MAX ||
       (int64_t)pl.B * Hkv * pl.nqblk_dq * pl.dq_splits > INT32_MAX)
     return fail(CAS_ERR_UNSUPPORTED, "grid too large");
@@ -954,6 +993,7 @@ cas_status_t prefix_attn_fwd_run(const cas_problem_t *p, const void *q, const vo
   fp.nqblk = pl.nqblk_fwd;
   fp.splits = pl.fwd_splits;
   fp.lse_hs = pl.packed ? (int32_t)pl.T : pl.Sq;
+  fp.xcds = pl.xcds;
   fp.scale_log2 = pl.scale * 1.4426950408889634f;
   hipError_t e = launch("fwd", [&] { return launch_fwd(fp, pl.dt, pl.D, stream); });
   if (e != hipSuccess) return hip_fail("fwd launch", e);
@@ -1273,6 +1313,7 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
     dp.nrows_max = pl.nrows_max;
     dp.nqblk = pl.nqblk_dq;
     dp.splits = pl.dq_splits;
+    dp.xcds = pl.xcds;
     dp.scale_log2 = scale_log2;
     dp.scale = pl.scale;
     e = timed("dq", stream, [&] { return launch_dq(dp, pl.dt, pl.D, stream); });

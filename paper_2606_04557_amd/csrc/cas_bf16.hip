@@ -97,18 +97,18 @@ __device__ __forceinline__ void fence_regs(T (&v)[N]) {
 }
 
 // XCD-aware workgroup order. Consecutive workgroup ids are dispatched
-// round-robin over the 8 XCDs (each with its own L2); this remaps them so
-// that each XCD receives one contiguous range of logical ids. Workgroups that
+// round-robin over the XCDs (8 on a whole MI355X, each with its own L2);
+// this remaps them so that each XCD receives one contiguous range of
+// logical ids. Workgroups that
 // stream the same K/V tiles (same batch row and KV head, adjacent logical
 // ids) then share one L2 instead of fetching every tile once per XCD. With
 // the KV head as the slowest logical index, each XCD gets whole KV heads
-// (when their count is a multiple of 8): the same work on every XCD even
+// (when their count is a multiple of the XCD count): the same work on every XCD even
 // when the batch rows differ in length.
-constexpr int kXcds = 8;
-__device__ __forceinline__ int xcd_order(int bid, int n) {
-  const int per = n / kXcds;
-  if (bid >= per * kXcds) return bid;   // the remainder keeps its id
-  return (bid % kXcds) * per + bid / kXcds;
+__device__ __forceinline__ int xcd_order(int bid, int n, int xcds) {
+  const int per = n / xcds;
+  if (bid >= per * xcds) return bid;   // the remainder keeps its id
+  return (bid % xcds) * per + bid / xcds;
 }
 
 // Workgroup barrier that orders LDS use: this wave's LDS reads have returned,
@@ -198,7 +198,7 @@ void fwd_bf16_kernel(FwdParams p) {
   const int G = lane >> 5, n = lane & 31;
   // Logical order: row block fastest, then split, batch row, KV head (the
   // KV heads split the XCDs evenly whatever the rows' lengths).
-  int bid = xcd_order(blockIdx.x, gridDim.x);
+  int bid = xcd_order(blockIdx.x, gridDim.x, p.xcds);
   const int qblk = __builtin_amdgcn_readfirstlane(bid % p.nqblk);
   bid /= p.nqblk;
   const int split = __builtin_amdgcn_readfirstlane(bid % p.splits);
@@ -598,7 +598,7 @@ void dq_bf16_kernel(DqParams p) {
   const int G = lane >> 5, n = lane & 31;
   // Logical order: row block fastest, then split, batch row, KV head (the
   // KV heads split the XCDs evenly whatever the rows' lengths).
-  int bid = xcd_order(blockIdx.x, gridDim.x);
+  int bid = xcd_order(blockIdx.x, gridDim.x, p.xcds);
   const int qblk = __builtin_amdgcn_readfirstlane(bid % p.nqblk);
   bid /= p.nqblk;
   const int split = __builtin_amdgcn_readfirstlane(bid % p.splits);

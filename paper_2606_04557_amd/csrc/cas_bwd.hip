@@ -1,4 +1,7 @@
-// Backward of multi-cartridge prefix attention on gfx950.
+// Backward of multi-cartridge prefix attention on gfx950: the statistics
+// pass for both dtypes, the fp32 dK/dV and dQ passes (v_mfma_f32_32x32x2f32,
+// no down-conversion; bf16 runs the kernels of cas_bf16.hip) and the dQ
+// split reduction for both dtypes.
 //
 // Three passes, all recomputing P from the stored row LSE:
 //   bwd_pre:  D = rowsum(dO * O) and LSE*log2(e) per packed row (fp32).
@@ -10,7 +13,7 @@
 //               S = Q K^T, dP = dO V^T        (K, V held in registers)
 //               P = exp2(S c - LSE2), dS = P (dP - D)
 //               dV^T += dO^T P, dK^T += Q^T dS  (P, dS straight from the C
-//                                                registers; Q/dO octet tiles)
+//                                                registers; Q/dO from LDS)
 //             The sums stay in registers, so each key's gradient is written
 //             once, to the owning segment's buffer, with no atomics; a
 //             cartridge referenced by several rows accumulates all of them.
@@ -56,8 +59,9 @@ __global__ __launch_bounds__(kThreads) void bwd_pre_kernel(PreParams p) {
   }
 }
 
-template <typename T, int D>
+template <int D>
 __global__ __launch_bounds__(kThreads) void dkdv_kernel(DkdvParams p) {
+  using T = float;
   using M = Mma<T>;
   using Frag = typename M::Frag;
   constexpr int NSTEP = D / M::kStep;
@@ -65,13 +69,9 @@ __global__ __launch_bounds__(kThreads) void dkdv_kernel(DkdvParams p) {
   constexpr int QSUB = QB / 32;
   constexpr int DT = D / 32;
   constexpr int RS = lds_row_stride<T, D>();
-  constexpr bool BF16 = sizeof(T) == 2;
-  constexpr int OSZ = BF16 ? QB * D : 8;
 
   __shared__ __attribute__((aligned(16))) T q_row[QB * RS];
   __shared__ __attribute__((aligned(16))) T do_row[QB * RS];
-  __shared__ __attribute__((aligned(16))) T q_oct[OSZ];
-  __shared__ __attribute__((aligned(16))) T do_oct[OSZ];
   __shared__ float lse2_l[QB];
   __shared__ float nd_l[QB];
 
@@ -160,13 +160,8 @@ __global__ __launch_bounds__(kThreads) void dkdv_kernel(DkdvParams p) {
         return dob_base + ((int64_t)t * Hq + (rr - t * g)) * D;
       };
       __syncthreads();
-      if constexpr (BF16) {
-        load_octets<D, QB, true>((__bf16 *)q_oct, (__bf16 *)q_row, qptr, nv, tid);
-        load_octets<D, QB, true>((__bf16 *)do_oct, (__bf16 *)do_row, doptr, nv, tid);
-      } else {
-        load_rows<T, D, QB>(q_row, qptr, nv, tid);
-        load_rows<T, D, QB>(do_row, doptr, nv, tid);
-      }
+      load_rows<T, D, QB>(q_row, qptr, nv, tid);
+      load_rows<T, D, QB>(do_row, doptr, nv, tid);
       if (tid < QB) {
         const int rr = r0 + tid;
         lse2_l[tid] = rr < nrows ? lse2_b[rr] : INFINITY;
@@ -196,30 +191,13 @@ __global__ __launch_bounds__(kThreads) void dkdv_kernel(DkdvParams p) {
           sa[j] = pv;
           dpa[j] = ds;
         }
-        if constexpr (BF16) {
 #pragma unroll
-          for (int s = 0; s < 2; ++s) {
-            Frag pf, dsf;
+        for (int s = 0; s < 16; ++s)
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              pf[e] = (__bf16)sa[8 * s + e];
-              dsf[e] = (__bf16)dpa[8 * s + e];
-            }
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-              dv[dt] = M::run(octet_frag<D>((const __bf16 *)do_oct, qs, s, G, dt * 32 + n), pf, dv[dt]);
-              dk[dt] = M::run(octet_frag<D>((const __bf16 *)q_oct, qs, s, G, dt * 32 + n), dsf, dk[dt]);
-            }
+          for (int dt = 0; dt < DT; ++dt) {
+            dv[dt] = M::run(trans_frag_f32<D>(do_row, qs, s, G, dt * 32 + n), sa[s], dv[dt]);
+            dk[dt] = M::run(trans_frag_f32<D>(q_row, qs, s, G, dt * 32 + n), dpa[s], dk[dt]);
           }
-        } else {
-#pragma unroll
-          for (int s = 0; s < 16; ++s)
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-              dv[dt] = M::run(trans_frag_f32<D>((const float *)do_row, qs, s, G, dt * 32 + n), sa[s], dv[dt]);
-              dk[dt] = M::run(trans_frag_f32<D>((const float *)q_row, qs, s, G, dt * 32 + n), dpa[s], dk[dt]);
-            }
-        }
       }
     }
   }
@@ -240,8 +218,9 @@ __global__ __launch_bounds__(kThreads) void dkdv_kernel(DkdvParams p) {
     }
 }
 
-template <typename T, int D>
+template <int D>
 __global__ __launch_bounds__(kThreads) void dq_kernel(DqParams p) {
+  using T = float;
   using M = Mma<T>;
   using Frag = typename M::Frag;
   constexpr int NSTEP = D / M::kStep;
@@ -250,12 +229,9 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(DqParams p) {
   constexpr int NSUB = KT / 32;
   constexpr int DT = D / 32;
   constexpr int RS = lds_row_stride<T, D>();
-  constexpr bool BF16 = sizeof(T) == 2;
-  constexpr int OSZ = BF16 ? KT * D : 8;
 
   __shared__ __attribute__((aligned(16))) T k_row[KT * RS];
   __shared__ __attribute__((aligned(16))) T v_row[KT * RS];
-  __shared__ __attribute__((aligned(16))) T k_oct[OSZ];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int G = lane >> 5, n = lane & 31;
@@ -344,12 +320,7 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(DqParams p) {
       nvalid = min(KT, len - self0);
     }
     __syncthreads();
-    if constexpr (BF16) {
-      load_octets<D, KT, true>((__bf16 *)k_oct, (__bf16 *)k_row, [&](int r) { return kp + r * st; },
-                               nvalid, tid);
-    } else {
-      load_rows<T, D, KT>(k_row, [&](int r) { return kp + r * st; }, nvalid, tid);
-    }
+    load_rows<T, D, KT>(k_row, [&](int r) { return kp + r * st; }, nvalid, tid);
     load_rows<T, D, KT>(v_row, [&](int r) { return vp + r * st; }, nvalid, tid);
     __syncthreads();
 
@@ -389,31 +360,14 @@ __global__ __launch_bounds__(kThreads) void dq_kernel(DqParams p) {
           sa[qs][j] = pv * (dpa[qs][j] + ndr[qs]);
         }
       }
-      if constexpr (BF16) {
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          Frag dsf[QS];
+      for (int s = 0; s < 16; ++s)
 #pragma unroll
-          for (int qs = 0; qs < QS; ++qs)
+        for (int dt = 0; dt < DT; ++dt) {
+          const float a = trans_frag_f32<D>(k_row, sub, s, G, dt * 32 + n);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) dsf[qs][e] = (__bf16)sa[qs][8 * s + e];
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) {
-            const Frag a = octet_frag<D>((const __bf16 *)k_oct, sub, s, G, dt * 32 + n);
-#pragma unroll
-            for (int qs = 0; qs < QS; ++qs) acc[dt][qs] = M::run(a, dsf[qs], acc[dt][qs]);
-          }
+          for (int qs = 0; qs < QS; ++qs) acc[dt][qs] = M::run(a, sa[qs][s], acc[dt][qs]);
         }
-      } else {
-#pragma unroll
-        for (int s = 0; s < 16; ++s)
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) {
-            const float a = trans_frag_f32<D>((const float *)k_row, sub, s, G, dt * 32 + n);
-#pragma unroll
-            for (int qs = 0; qs < QS; ++qs) acc[dt][qs] = M::run(a, sa[qs][s], acc[dt][qs]);
-          }
-      }
     }
   }
 
@@ -481,27 +435,27 @@ hipError_t launch_bwd_pre(const PreParams &p, DType dt, int D, hipStream_t s) {
   return D == 64 ? launch_pre_t<float, 64>(p, s) : launch_pre_t<float, 128>(p, s);
 }
 
-template <typename T, int D>
+template <int D>
 static hipError_t launch_dkdv_t(const DkdvParams &p, int n_wg, hipStream_t s) {
-  hipLaunchKernelGGL((dkdv_kernel<T, D>), dim3((unsigned)n_wg), dim3(kThreads), 0, s, p);
+  hipLaunchKernelGGL((dkdv_kernel<D>), dim3((unsigned)n_wg), dim3(kThreads), 0, s, p);
   return hipGetLastError();
 }
 
 hipError_t launch_dkdv(const DkdvParams &p, DType dt, int D, int n_wg, hipStream_t s) {
   if (dt == kBF16) return launch_dkdv_bf16(p, D, n_wg, s);
-  return D == 64 ? launch_dkdv_t<float, 64>(p, n_wg, s) : launch_dkdv_t<float, 128>(p, n_wg, s);
+  return D == 64 ? launch_dkdv_t<64>(p, n_wg, s) : launch_dkdv_t<128>(p, n_wg, s);
 }
 
-template <typename T, int D>
+template <int D>
 static hipError_t launch_dq_t(const DqParams &p, hipStream_t s) {
   const int64_t grid = (int64_t)p.nqblk * p.Hkv * p.splits * p.B;
-  hipLaunchKernelGGL((dq_kernel<T, D>), dim3((unsigned)grid), dim3(kThreads), 0, s, p);
+  hipLaunchKernelGGL((dq_kernel<D>), dim3((unsigned)grid), dim3(kThreads), 0, s, p);
   return hipGetLastError();
 }
 
 hipError_t launch_dq(const DqParams &p, DType dt, int D, hipStream_t s) {
   if (dt == kBF16) return launch_dq_bf16(p, D, s);
-  return D == 64 ? launch_dq_t<float, 64>(p, s) : launch_dq_t<float, 128>(p, s);
+  return D == 64 ? launch_dq_t<64>(p, s) : launch_dq_t<128>(p, s);
 }
 
 template <typename T, int D>

@@ -103,23 +103,6 @@ __device__ __forceinline__ typename Mma<T>::Frag global_frag(const T *rowp, int 
   }
 }
 
-// Octet layout (bf16 only): a tile of R rows (R a multiple of 32) and D
-// channels stored as [R/8 octets][D][8]. Octet o = 4*sub + 2*s + G of 32-row
-// subtile `sub` holds rows 32*sub + 16*s + 4*G + {0,1,2,3,8,9,10,11}, i.e. the
-// rows crow(8s .. 8s+7, G) -- exactly the reduction indices that C-fragment
-// registers 8s..8s+7 of group G stand for. Lane (G, m) then reads the A
-// fragment A[m = channel][k = those 8 rows] with one 16-byte load.
-__device__ __forceinline__ int octet_row(int o, int e) {
-  const int sub = o >> 2, s = (o >> 1) & 1, G = o & 1;
-  return 32 * sub + 16 * s + 4 * G + (e & 3) + ((e >> 2) << 3);
-}
-
-template <int D>
-__device__ __forceinline__ bf16x8 octet_frag(const __bf16 *oct, int sub, int s, int G, int ch) {
-  const int o = 4 * sub + 2 * s + G;
-  return *reinterpret_cast<const bf16x8 *>(oct + ((size_t)o * D + ch) * 8);
-}
-
 // Transposed operand fragment for fp32 tiles (row layout): the value of row
 // crow(s, G) of subtile `sub` at channel ch (one element per lane per step).
 template <int D>
@@ -157,49 +140,6 @@ __device__ __forceinline__ void load_rows(T *tile, RowPtr rowptr, int nvalid, in
   }
 }
 
-__device__ __forceinline__ uint32_t lo16(uint32_t w) { return w & 0xffffu; }
-__device__ __forceinline__ uint32_t hi16(uint32_t w) { return w >> 16; }
-
-// bf16 tile of R rows into the octet layout, and optionally also into the row
-// layout. Each thread moves 8-row x 8-channel blocks and transposes them in
-// registers.
-template <int D, int R, bool ALSO_ROWS, typename RowPtr>
-__device__ __forceinline__ void load_octets(__bf16 *oct, __bf16 *rows_tile, RowPtr rowptr,
-                                            int nvalid, int tid) {
-  constexpr int NB = (R / 8) * (D / 8);
-  constexpr int RS = lds_row_stride<__bf16, D>();
-  for (int blk = tid; blk < NB; blk += kThreads) {
-    const int o = blk / (D / 8), db = blk % (D / 8);
-    u32x4 r[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int row = octet_row(o, e);
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (row < nvalid) v = *reinterpret_cast<const u32x4 *>(rowptr(row) + db * 8);
-      r[e] = v;
-    }
-    if constexpr (ALSO_ROWS) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int row = octet_row(o, e);
-        *reinterpret_cast<u32x4 *>(rows_tile + row * RS + db * 8) = r[e];
-      }
-    }
-    // out[c] = (r[0][c], r[1][c], ..., r[7][c]) for channel c = db*8 + 0..7
-#pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const int w = c >> 1;
-      u32x4 outv;
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const uint32_t a = (c & 1) ? hi16(r[2 * p][w]) : lo16(r[2 * p][w]);
-        const uint32_t b = (c & 1) ? hi16(r[2 * p + 1][w]) : lo16(r[2 * p + 1][w]);
-        outv[p] = a | (b << 16);
-      }
-      *reinterpret_cast<u32x4 *>(oct + ((size_t)o * D + db * 8 + c) * 8) = outv;
-    }
-  }
-}
 
 __device__ __forceinline__ float xor32(float v) { return __shfl_xor(v, 32, 64); }
 

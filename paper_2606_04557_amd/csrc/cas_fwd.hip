@@ -7,8 +7,9 @@
 //   S^T = K Q^T   (MFMA; K from LDS in row layout, Q held in registers)
 //   online softmax on S^T (a lane owns one query column: row max/sum are
 //   lane-local plus one exchange with the partner lane 32 away)
-//   O^T += V^T P^T (MFMA; V from LDS in octet layout, P^T straight from the
-//   S^T registers, rounded to bf16 on the bf16 path, kept fp32 on fp32)
+//   O^T += V^T P^T (MFMA; V from LDS, P^T straight from the S^T registers)
+// This is the fp32 path (v_mfma_f32_32x32x2f32, no down-conversion); bf16
+// runs the kernels of cas_bf16.hip.
 // Segment tiles stop at segment ends, so a ragged tail is the only masked
 // prefix tile; self tiles are masked only where they cross the diagonal.
 // With splits > 1 each workgroup takes a contiguous share of the key tiles
@@ -17,8 +18,9 @@
 
 namespace cas {
 
-template <typename T, int D>
+template <int D>
 __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdParams p) {
+  using T = float;
   using M = Mma<T>;
   using Frag = typename M::Frag;
   constexpr int NSTEP = D / M::kStep;
@@ -27,11 +29,9 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdParams p) {
   constexpr int NSUB = KT / 32;
   constexpr int DT = D / 32;
   constexpr int RS = lds_row_stride<T, D>();
-  constexpr bool BF16 = sizeof(T) == 2;
-  constexpr int VSZ = BF16 ? KT * D : KT * RS;
 
   __shared__ __attribute__((aligned(16))) T k_lds[KT * RS];
-  __shared__ __attribute__((aligned(16))) T v_lds[VSZ];
+  __shared__ __attribute__((aligned(16))) T v_lds[KT * RS];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int G = lane >> 5, n = lane & 31;
@@ -116,11 +116,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdParams p) {
     }
     __syncthreads();
     load_rows<T, D, KT>(k_lds, [&](int r) { return kp + r * st; }, nvalid, tid);
-    if constexpr (BF16) {
-      load_octets<D, KT, false>(v_lds, nullptr, [&](int r) { return vp + r * st; }, nvalid, tid);
-    } else {
-      load_rows<T, D, KT>(v_lds, [&](int r) { return vp + r * st; }, nvalid, tid);
-    }
+    load_rows<T, D, KT>(v_lds, [&](int r) { return vp + r * st; }, nvalid, tid);
     __syncthreads();
 
     if (!wave_active) continue;
@@ -179,35 +175,16 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(FwdParams p) {
       for (int dt = 0; dt < DT; ++dt) oacc[dt][qs] *= alpha;
     }
 
-    if constexpr (BF16) {
 #pragma unroll
-      for (int sub = 0; sub < NSUB; ++sub)
+    for (int sub = 0; sub < NSUB; ++sub)
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          Frag pf[QS];
+      for (int s = 0; s < 16; ++s)
 #pragma unroll
-          for (int qs = 0; qs < QS; ++qs)
+        for (int dt = 0; dt < DT; ++dt) {
+          const float a = trans_frag_f32<D>(v_lds, sub, s, G, dt * 32 + n);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) pf[qs][e] = (__bf16)sacc[sub][qs][8 * s + e];
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) {
-            const Frag a = octet_frag<D>((const __bf16 *)v_lds, sub, s, G, dt * 32 + n);
-#pragma unroll
-            for (int qs = 0; qs < QS; ++qs) oacc[dt][qs] = M::run(a, pf[qs], oacc[dt][qs]);
-          }
+          for (int qs = 0; qs < QS; ++qs) oacc[dt][qs] = M::run(a, sacc[sub][qs][s], oacc[dt][qs]);
         }
-    } else {
-#pragma unroll
-      for (int sub = 0; sub < NSUB; ++sub)
-#pragma unroll
-        for (int s = 0; s < 16; ++s)
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) {
-            const float a = trans_frag_f32<D>((const float *)v_lds, sub, s, G, dt * 32 + n);
-#pragma unroll
-            for (int qs = 0; qs < QS; ++qs) oacc[dt][qs] = M::run(a, sacc[sub][qs][s], oacc[dt][qs]);
-          }
-    }
   }
 
 #pragma unroll
@@ -279,16 +256,16 @@ __global__ __launch_bounds__(kThreads) void fwd_merge_kernel(MergeParams p) {
   if (c4 == 0 && p.lse != nullptr) p.lse[(int64_t)row.lse0 + (int64_t)h * p.lse_hs + t] = mx + logf(w_sum);
 }
 
-template <typename T, int D>
+template <int D>
 static hipError_t launch_fwd_t(const FwdParams &p, hipStream_t s) {
   const int64_t grid = (int64_t)p.nqblk * p.Hkv * p.splits * p.B;
-  hipLaunchKernelGGL((fwd_kernel<T, D>), dim3((unsigned)grid), dim3(kThreads), 0, s, p);
+  hipLaunchKernelGGL((fwd_kernel<D>), dim3((unsigned)grid), dim3(kThreads), 0, s, p);
   return hipGetLastError();
 }
 
 hipError_t launch_fwd(const FwdParams &p, DType dt, int D, hipStream_t s) {
   if (dt == kBF16) return launch_fwd_bf16(p, D, s);
-  return D == 64 ? launch_fwd_t<float, 64>(p, s) : launch_fwd_t<float, 128>(p, s);
+  return D == 64 ? launch_fwd_t<64>(p, s) : launch_fwd_t<128>(p, s);
 }
 
 template <typename T, int D>

@@ -103,6 +103,7 @@ struct FwdParams {
   int64_t plane;      // T * Hq: rows of one split partial plane
   int32_t B, Smax, Hkv, g, nrows_max, nqblk, splits;
   int32_t lse_hs;     // lse head stride (q_len, or T for packed samples)
+  int32_t xcds;       // XCDs of the device (bf16 workgroup order)
   float scale_log2;   // softmax_scale * log2(e)
 };
 
@@ -143,6 +144,7 @@ struct DqParams {
   const DevTile *tiles;
   int64_t plane;
   int32_t B, Smax, Hkv, g, nrows_max, nqblk, splits;
+  int32_t xcds;       // XCDs of the device (bf16 workgroup order)
   float scale_log2;
   float scale;
 };
