@@ -134,6 +134,8 @@ def plan_info(problem: Problem) -> dict:
 
 
 def set_tuning(fwd_splits: int = 0, dq_splits: int = 0) -> None:
+    """Launch-plan knobs (0 = automatic): key-axis splits of the forward and
+    of the dQ pass."""
     t = _lib.Tuning(fwd_splits, dq_splits)
     _check(load().cas_set_tuning(ctypes.byref(t)))
 

@@ -476,6 +476,22 @@ void build_dkdv_order(Plan &pl, bool with_self) {
     return a.tile < b.tile;
   });
   pl.order.resize(v.size());
+  const int X = pl.xcds;
+  if (X > 1 && pl.Hkv % X == 0) {
+    // XCD-affine: workgroup i runs on XCD i % X (round-robin dispatch), so
+    // entry i takes the next workgroup of KV heads h with h % X == i % X.
+    // Every KV head has the same tiles, so the X lists are equally long and
+    // each keeps the longest-first order; the query blocks of one (row, KV
+    // head) are then streamed by one XCD's L2 only.
+    std::vector<size_t> next(X, 0);
+    std::vector<std::vector<E>> q(X);
+    for (const E &e : v) q[e.kvh % X].push_back(e);
+    for (size_t i = 0; i < v.size(); ++i) {
+      const E &e = q[i % X][next[i % X]++];
+      pl.order[i] = {e.tile, e.kvh};
+    }
+    return;
+  }
   for (size_t i = 0; i < v.size(); ++i) pl.order[i] = {v[i].tile, v[i].kvh};
 }
 
@@ -1260,6 +1276,46 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
   if (e != hipSuccess) return hip_fail("bwd_pre launch", e);
 
   const int n_wg = (int)pl.order.size();
+  auto run_dq = [&]() -> hipError_t {
+    if (!dq) return hipSuccess;
+    DqParams dp{};
+    dp.q = q;
+    dp.k_self = k_self;
+    dp.v_self = v_self;
+    dp.d_o = d_o;
+    dp.nd = nd;
+    dp.lse2 = lse2;
+    dp.dq = dq;
+    dp.part_dq = pl.dq_splits > 1 ? (float *)(ws + pl.off_part_dq) : nullptr;
+    dp.segs = (const DevSeg *)(ws + pl.off_segs);
+    dp.tiles = (const DevTile *)(ws + pl.off_tiles);
+    dp.rows = (const DevRow *)(ws + pl.off_rows);
+    dp.plane = pl.T * pl.Hq;
+    dp.B = pl.B;
+    dp.Smax = pl.Smax;
+    dp.Hkv = pl.Hkv;
+    dp.g = pl.g;
+    dp.nrows_max = pl.nrows_max;
+    dp.nqblk = pl.nqblk_dq;
+    dp.splits = pl.dq_splits;
+    dp.xcds = pl.xcds;
+    dp.scale_log2 = scale_log2;
+    dp.scale = pl.scale;
+    hipError_t r = timed("dq", stream, [&] { return launch_dq(dp, pl.dt, pl.D, stream); });
+    if (r != hipSuccess || pl.dq_splits <= 1) return r;
+    DqReduceParams rp{};
+    rp.part_dq = dp.part_dq;
+    rp.dq = dq;
+    rp.rows = dp.rows;
+    rp.plane = dp.plane;
+    rp.B = pl.B;
+    rp.Hkv = pl.Hkv;
+    rp.g = pl.g;
+    rp.nrows_max = pl.nrows_max;
+    rp.splits = pl.dq_splits;
+    rp.scale = pl.scale;
+    return timed("dq_reduce", stream, [&] { return launch_dq_reduce(rp, pl.dt, pl.D, stream); });
+  };
   if (n_wg > 0) {
     DkdvParams kp{};
     kp.q = q;
@@ -1291,49 +1347,8 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
     e = timed("dkdv", stream, [&] { return launch_dkdv(kp, pl.dt, pl.D, n_wg, stream); });
     if (e != hipSuccess) return hip_fail("dkdv launch", e);
   }
-
-  if (dq) {
-    DqParams dp{};
-    dp.q = q;
-    dp.k_self = k_self;
-    dp.v_self = v_self;
-    dp.d_o = d_o;
-    dp.nd = nd;
-    dp.lse2 = lse2;
-    dp.dq = dq;
-    dp.part_dq = pl.dq_splits > 1 ? (float *)(ws + pl.off_part_dq) : nullptr;
-    dp.segs = (const DevSeg *)(ws + pl.off_segs);
-    dp.tiles = (const DevTile *)(ws + pl.off_tiles);
-    dp.rows = (const DevRow *)(ws + pl.off_rows);
-    dp.plane = pl.T * pl.Hq;
-    dp.B = pl.B;
-    dp.Smax = pl.Smax;
-    dp.Hkv = pl.Hkv;
-    dp.g = pl.g;
-    dp.nrows_max = pl.nrows_max;
-    dp.nqblk = pl.nqblk_dq;
-    dp.splits = pl.dq_splits;
-    dp.xcds = pl.xcds;
-    dp.scale_log2 = scale_log2;
-    dp.scale = pl.scale;
-    e = timed("dq", stream, [&] { return launch_dq(dp, pl.dt, pl.D, stream); });
-    if (e != hipSuccess) return hip_fail("dq launch", e);
-    if (pl.dq_splits > 1) {
-      DqReduceParams rp{};
-      rp.part_dq = dp.part_dq;
-      rp.dq = dq;
-      rp.rows = dp.rows;
-      rp.plane = dp.plane;
-      rp.B = pl.B;
-      rp.Hkv = pl.Hkv;
-      rp.g = pl.g;
-      rp.nrows_max = pl.nrows_max;
-      rp.splits = pl.dq_splits;
-      rp.scale = pl.scale;
-      e = timed("dq_reduce", stream, [&] { return launch_dq_reduce(rp, pl.dt, pl.D, stream); });
-      if (e != hipSuccess) return hip_fail("dq_reduce launch", e);
-    }
-  }
+  e = run_dq();
+  if (e != hipSuccess) return hip_fail("dq launch", e);
   return CAS_OK;
 }
 
