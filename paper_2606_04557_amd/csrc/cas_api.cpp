@@ -95,6 +95,7 @@ struct Plan {
   std::vector<DevSeg> segs;
   std::vector<DevRow> rows;
   std::vector<DevTile> tiles;
+  std::vector<int32_t> row_order;   // batch rows, most key tiles first (forward and dQ order)
   std::vector<DevCart> carts;
   std::vector<int32_t> uses;
   std::vector<DevWg> order;       // dK/dV workgroups, longest first
@@ -107,7 +108,8 @@ struct Plan {
   int cart_tiles = 0;
   bool want_self_grad = false;
   // workspace layout
-  size_t off_segs = 0, off_rows = 0, off_tiles = 0, off_carts = 0, off_uses = 0, off_order = 0, table_bytes = 0;
+  size_t off_segs = 0, off_rows = 0, off_tiles = 0, off_rorder = 0, off_carts = 0, off_uses = 0, off_order = 0,
+         table_bytes = 0;
   size_t off_part_o = 0, off_part_lse = 0, off_ovf = 0, ws_fwd = 0;
   size_t off_nd = 0, off_lse2 = 0, off_part_dq = 0, off_qT = 0, off_doT = 0, ws_bwd = 0;
 };
@@ -295,6 +297,15 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl, int fwd_spli
     min_row_tiles = std::min(min_row_tiles, tiles + 1);
   }
 
+  // Forward and dQ workgroups take their batch row through this order: the
+  // rows whose workgroups walk the most key tiles (prefix plus self) first,
+  // so the longest workgroups do not end up in the tail (ties: row order).
+  pl.row_order.resize(pl.B);
+  for (int b = 0; b < pl.B; ++b) pl.row_order[b] = b;
+  std::stable_sort(pl.row_order.begin(), pl.row_order.end(), [&](int a, int c) {
+    return pl.rows[a].prefix_tiles + ceil_div(pl.len[a], kKeyTile) >
+           pl.rows[c].prefix_tiles + ceil_div(pl.len[c], kKeyTile);
+  });
   const cas_tuning_t tu = tuning();
   const bool bf16 = pl.dt == kBF16;
   const int rpw_fwd = bf16 ? kBf16RowsPerWg : kRowsPerWg, rpw_dq = bf16 ? kBf16RowsPerWg : kDqRowsPerWg;
@@ -399,6 +410,8 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl, int fwd_spli
   off = align_up(off + pl.rows.size() * sizeof(DevRow), 256);
   pl.off_tiles = off;
   off = align_up(off + pl.tiles.size() * sizeof(DevTile), 256);
+  pl.off_rorder = off;
+  off = align_up(off + pl.row_order.size() * sizeof(int32_t), 256);
   if (bwd) {
     pl.off_carts = off;
     off = align_up(off + pl.carts.size() * sizeof(DevCart), 256);
@@ -600,6 +613,7 @@ void fill_tables(const Plan &pl, bool bwd, char *h) {
   if (!pl.segs.empty()) std::memcpy(h + pl.off_segs, pl.segs.data(), pl.segs.size() * sizeof(DevSeg));
   std::memcpy(h + pl.off_rows, pl.rows.data(), pl.rows.size() * sizeof(DevRow));
   if (!pl.tiles.empty()) std::memcpy(h + pl.off_tiles, pl.tiles.data(), pl.tiles.size() * sizeof(DevTile));
+  std::memcpy(h + pl.off_rorder, pl.row_order.data(), pl.row_order.size() * sizeof(int32_t));
   if (bwd) {
     if (!pl.carts.empty()) std::memcpy(h + pl.off_carts, pl.carts.data(), pl.carts.size() * sizeof(DevCart));
     if (!pl.uses.empty()) std::memcpy(h + pl.off_uses, pl.uses.data(), pl.uses.size() * sizeof(int32_t));
@@ -999,6 +1013,7 @@ cas_status_t prefix_attn_fwd_run(const cas_problem_t *p, const void *q, const vo
   fp.segs = (const DevSeg *)(ws + pl.off_segs);
   fp.rows = (const DevRow *)(ws + pl.off_rows);
   fp.tiles = (const DevTile *)(ws + pl.off_tiles);
+  fp.row_order = (const int32_t *)(ws + pl.off_rorder);
   fp.ovf_flag = pl.dt == kBF16 ? (int32_t *)(ws + pl.off_ovf) : nullptr;
   fp.plane = pl.T * pl.Hq;
   fp.B = pl.B;
@@ -1289,6 +1304,7 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
     dp.part_dq = pl.dq_splits > 1 ? (float *)(ws + pl.off_part_dq) : nullptr;
     dp.segs = (const DevSeg *)(ws + pl.off_segs);
     dp.tiles = (const DevTile *)(ws + pl.off_tiles);
+    dp.row_order = (const int32_t *)(ws + pl.off_rorder);
     dp.rows = (const DevRow *)(ws + pl.off_rows);
     dp.plane = pl.T * pl.Hq;
     dp.B = pl.B;

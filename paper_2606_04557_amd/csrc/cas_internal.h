@@ -99,6 +99,7 @@ struct FwdParams {
   const DevSeg *segs;
   const DevRow *rows;
   const DevTile *tiles;
+  const int32_t *row_order;   // [B] bf16 workgroup order: batch rows, most key tiles first
   int32_t *ovf_flag;  // [grid] bf16: workgroup needs the exact-maximum pass
   int64_t plane;      // T * Hq: rows of one split partial plane
   int32_t B, Smax, Hkv, g, nrows_max, nqblk, splits;
@@ -142,6 +143,7 @@ struct DqParams {
   const DevSeg *segs;
   const DevRow *rows;
   const DevTile *tiles;
+  const int32_t *row_order;   // [B] bf16 workgroup order: batch rows, most key tiles first
   int64_t plane;
   int32_t B, Smax, Hkv, g, nrows_max, nqblk, splits;
   int32_t xcds;       // XCDs of the device (bf16 workgroup order)
