@@ -142,7 +142,11 @@ typedef struct {
 cas_status_t cas_prefix_attn_workspace_size(const cas_problem_t *p, int backward, size_t *bytes);
 
 /*
- * Forward: writes o (dtype) and, when lse != NULL, the row log-sum-exp lse
+ * Forward (paper: Section "Inference", several cartridges concatenated in
+ * order ahead of the prompt; Limitations, "Cartridge KV position", ordinary
+ * causal masking of the tokens that follow): softmax attention of every
+ * query over its row's segments in table order, then its own tokens 0..t.
+ * Writes o (dtype) and, when lse != NULL, the row log-sum-exp lse
  * (float32, natural log). All tensors are device memory, 16-byte aligned
  * (lse 4-byte aligned). hip_stream is a hipStream_t (NULL = default stream).
  * Validation happens before anything is enqueued; on error nothing is
@@ -153,6 +157,10 @@ cas_status_t cas_prefix_attn_fwd(const cas_problem_t *p, const void *q, const vo
                                  size_t ws_bytes, void *hip_stream);
 
 /*
+ * Backward (paper: Section "Cartridges at Scale (CAS) Training", Background
+ * paragraph: the model is frozen and only the cartridges' keys and values
+ * are trained, so the gradient flows through the attention into every
+ * referenced cartridge; a cartridge used several times gets the sum).
  * Backward of sum(d_o * o): consumes q, the self and segment K/V, and the o
  * and lse written by cas_prefix_attn_fwd on the same inputs, and OVERWRITES
  * dq, dk_self, dv_self and every non-NULL segments[i].dk / .dv (NULL outputs
