@@ -88,6 +88,9 @@ SMALL = [
          head_dim=128, cart_lens=[300, 65], rows=[[0], [1, 0]]),
     dict(name="g5_d64", dtype="bf16", batch=1, q_len=45, num_q_heads=10, num_kv_heads=2,
          head_dim=64, cart_lens=[90, 40], rows=[[1, 0]]),
+    # 16 KV heads: two per XCD in the XCD-affine dK/dV order
+    dict(name="kv16", dtype="bf16", batch=2, q_len=70, num_q_heads=32, num_kv_heads=16,
+         head_dim=64, cart_lens=[130, 64, 200], rows=[[0, 1], [2, 0]], layouts=["tok", "head", "padded"]),
     dict(name="fp32_d128", dtype="fp32", batch=1, q_len=33, num_q_heads=4, num_kv_heads=2,
          head_dim=128, cart_lens=[65, 3], rows=[[0, 1]]),
     dict(name="fp32_alias", dtype="fp32", batch=2, q_len=20, num_q_heads=2, num_kv_heads=1,
