@@ -88,6 +88,12 @@ SMALL = [
          head_dim=128, cart_lens=[300, 65], rows=[[0], [1, 0]]),
     dict(name="g5_d64", dtype="bf16", batch=1, q_len=45, num_q_heads=10, num_kv_heads=2,
          head_dim=64, cart_lens=[90, 40], rows=[[1, 0]]),
+    # one query per row: a single 4-row block per (row, KV head) against a
+    # long prefix (the planner splits the key axis), and rows with no prefix
+    dict(name="q1_long", dtype="bf16", batch=2, q_len=1, num_q_heads=8, num_kv_heads=2, head_dim=128,
+         cart_lens=[3000, 1, 70], rows=[[0], [1, 0, 2]], layouts=["head", "tok", "padded"]),
+    dict(name="q1_nocart", dtype="bf16", batch=3, q_len=1, num_q_heads=4, num_kv_heads=1, head_dim=64,
+         cart_lens=[], rows=[[], [], []]),
     # 16 KV heads: two per XCD in the XCD-affine dK/dV order
     dict(name="kv16", dtype="bf16", batch=2, q_len=70, num_q_heads=32, num_kv_heads=16,
          head_dim=64, cart_lens=[130, 64, 200], rows=[[0, 1], [2, 0]], layouts=["tok", "head", "padded"]),
