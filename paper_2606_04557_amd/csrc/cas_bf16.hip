@@ -196,11 +196,12 @@ void fwd_bf16_kernel(FwdParams p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2;
   const int G = lane >> 5, n = lane & 31;
-  // Logical order: row block fastest, then split, batch row (the rows with
-  // the most key tiles first), KV head (the KV heads split the XCDs evenly
-  // whatever the rows' lengths).
+  // Logical order: row block fastest (the last one, with the most causal
+  // self tiles, first), then split, batch row (the rows with the most key
+  // tiles first), KV head (the KV heads split the XCDs evenly whatever the
+  // rows' lengths).
   int bid = xcd_order(blockIdx.x, gridDim.x, p.xcds);
-  const int qblk = __builtin_amdgcn_readfirstlane(bid % p.nqblk);
+  const int qblk = __builtin_amdgcn_readfirstlane(p.nqblk - 1 - bid % p.nqblk);
   bid /= p.nqblk;
   const int split = __builtin_amdgcn_readfirstlane(bid % p.splits);
   bid /= p.splits;
@@ -597,11 +598,12 @@ void dq_bf16_kernel(DqParams p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2;
   const int G = lane >> 5, n = lane & 31;
-  // Logical order: row block fastest, then split, batch row (the rows with
-  // the most key tiles first), KV head (the KV heads split the XCDs evenly
-  // whatever the rows' lengths).
+  // Logical order: row block fastest (the last one, with the most causal
+  // self tiles, first), then split, batch row (the rows with the most key
+  // tiles first), KV head (the KV heads split the XCDs evenly whatever the
+  // rows' lengths).
   int bid = xcd_order(blockIdx.x, gridDim.x, p.xcds);
-  const int qblk = __builtin_amdgcn_readfirstlane(bid % p.nqblk);
+  const int qblk = __builtin_amdgcn_readfirstlane(p.nqblk - 1 - bid % p.nqblk);
   bid /= p.nqblk;
   const int split = __builtin_amdgcn_readfirstlane(bid % p.splits);
   bid /= p.splits;
