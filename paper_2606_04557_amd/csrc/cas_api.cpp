@@ -95,7 +95,7 @@ struct Plan {
   std::vector<DevSeg> segs;
   std::vector<DevRow> rows;
   std::vector<DevTile> tiles;
-  std::vector<int32_t> row_order;   // batch rows, most key tiles first (forward and dQ order)
+  std::vector<DevItem> items;       // bf16 forward (or, backward plan, dQ) workgroups in dispatch order
   std::vector<DevCart> carts;
   std::vector<int32_t> uses;
   std::vector<DevWg> order;       // dK/dV workgroups, longest first
@@ -108,7 +108,7 @@ struct Plan {
   int cart_tiles = 0;
   bool want_self_grad = false;
   // workspace layout
-  size_t off_segs = 0, off_rows = 0, off_tiles = 0, off_rorder = 0, off_carts = 0, off_uses = 0, off_order = 0,
+  size_t off_segs = 0, off_rows = 0, off_tiles = 0, off_items = 0, off_carts = 0, off_uses = 0, off_order = 0,
          table_bytes = 0;
   size_t off_part_o = 0, off_part_lse = 0, off_ovf = 0, ws_fwd = 0;
   size_t off_nd = 0, off_lse2 = 0, off_part_dq = 0, off_qT = 0, off_doT = 0, ws_bwd = 0;
@@ -151,6 +151,57 @@ int auto_splits(int64_t base_wgs, int64_t min_row_tiles, int cus) {
   int64_t s = ceil_div(target, std::max<int64_t>(1, base_wgs));
   s = std::min<int64_t>(s, std::max<int64_t>(1, min_row_tiles / 8));
   return (int)std::max<int64_t>(1, std::min<int64_t>(s, kMaxSplits));
+}
+
+// Workgroups of the bf16 forward and dQ kernels, in dispatch order, with
+// `splits` key-axis splits. Workgroup i is dispatched to XCD i mod X (X = 8 on
+// a whole MI355X, each XCD with its own L2), and each XCD hands its next
+// workgroup to whichever of its CUs frees first. The items are enumerated
+// KV head slowest, then batch row (most key tiles first), split, query block,
+// and cut into X contiguous shares, share x for XCD x: the workgroups that
+// stream one (row, KV head)'s K/V tiles share an L2 and, when X divides the
+// KV heads, every XCD gets whole KV heads (the same work). Within a share the
+// items go longest first (key tiles walked; ties keep the enumeration
+// order): with one workgroup per CU at a time that is the
+// longest-processing-time rule, so the shortest start last and the CUs
+// finish together. Only query blocks that hold rows are listed.
+void build_items(Plan &pl, int splits) {
+  std::vector<int> rows(pl.B);
+  for (int b = 0; b < pl.B; ++b) rows[b] = b;
+  std::stable_sort(rows.begin(), rows.end(), [&](int a, int c) {
+    return pl.rows[a].prefix_tiles + ceil_div(pl.len[a], kKeyTile) >
+           pl.rows[c].prefix_tiles + ceil_div(pl.len[c], kKeyTile);
+  });
+  struct E {
+    DevItem it;
+    int64_t tiles;
+  };
+  std::vector<E> v;
+  for (int kvh = 0; kvh < pl.Hkv; ++kvh)
+    for (int b : rows) {
+      const int64_t nrows = (int64_t)pl.len[b] * pl.g;
+      const int nq = (int)ceil_div(nrows, kBf16RowsPerWg);
+      for (int sp = 0; sp < splits; ++sp)
+        for (int qb = nq - 1; qb >= 0; --qb) {
+          // The kernels' tile range: the prefix, then the self tiles up to
+          // the block's last query position, cut evenly over the splits.
+          const int64_t r1 = std::min<int64_t>(nrows, (int64_t)(qb + 1) * kBf16RowsPerWg);
+          const int64_t nt = pl.rows[b].prefix_tiles + ((r1 - 1) / pl.g) / kKeyTile + 1;
+          v.push_back({{qb, sp, b, kvh}, nt * (sp + 1) / splits - nt * sp / splits});
+        }
+    }
+  const size_t n = v.size(), X = (size_t)std::max(1, pl.xcds), per = n / X;
+  auto sort_share = [&](size_t lo, size_t hi) {
+    std::stable_sort(v.begin() + lo, v.begin() + hi, [](const E &a, const E &c) { return a.tiles > c.tiles; });
+  };
+  pl.items.resize(n);
+  for (size_t x = 0; x < X; ++x) {
+    sort_share(x * per, (x + 1) * per);
+    for (size_t k = 0; k < per; ++k) pl.items[k * X + x] = v[x * per + k].it;
+  }
+  // The remainder (fewer than X) is dispatched last.
+  sort_share(X * per, n);
+  for (size_t i = X * per; i < n; ++i) pl.items[i] = v[i].it;
 }
 
 // Shapes, segment table and planning. `bwd` additionally folds aliases and
@@ -297,15 +348,6 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl, int fwd_spli
     min_row_tiles = std::min(min_row_tiles, tiles + 1);
   }
 
-  // Forward and dQ workgroups take their batch row through this order: the
-  // rows whose workgroups walk the most key tiles (prefix plus self) first,
-  // so the longest workgroups do not end up in the tail (ties: row order).
-  pl.row_order.resize(pl.B);
-  for (int b = 0; b < pl.B; ++b) pl.row_order[b] = b;
-  std::stable_sort(pl.row_order.begin(), pl.row_order.end(), [&](int a, int c) {
-    return pl.rows[a].prefix_tiles + ceil_div(pl.len[a], kKeyTile) >
-           pl.rows[c].prefix_tiles + ceil_div(pl.len[c], kKeyTile);
-  });
   const cas_tuning_t tu = tuning();
   const bool bf16 = pl.dt == kBF16;
   const int rpw_fwd = bf16 ? kBf16RowsPerWg : kRowsPerWg, rpw_dq = bf16 ? kBf16RowsPerWg : kDqRowsPerWg;
@@ -327,6 +369,7 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl, int fwd_spli
   if ((int64_t)pl.B * Hkv * pl.nqblk_fwd * pl.fwd_splits > INT32_MAX ||
       (int64_t)pl.B * Hkv * pl.nqblk_dq * pl.dq_splits > INT32_MAX)
     return fail(CAS_ERR_UNSUPPORTED, "grid too large");
+  if (bf16) build_items(pl, bwd ? pl.dq_splits : pl.fwd_splits);
 
   if (bwd) {
     // Fold entries that name the same cartridge storage into one cartridge.
@@ -410,8 +453,8 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl, int fwd_spli
   off = align_up(off + pl.rows.size() * sizeof(DevRow), 256);
   pl.off_tiles = off;
   off = align_up(off + pl.tiles.size() * sizeof(DevTile), 256);
-  pl.off_rorder = off;
-  off = align_up(off + pl.row_order.size() * sizeof(int32_t), 256);
+  pl.off_items = off;
+  off = align_up(off + pl.items.size() * sizeof(DevItem), 256);
   if (bwd) {
     pl.off_carts = off;
     off = align_up(off + pl.carts.size() * sizeof(DevCart), 256);
@@ -578,8 +621,12 @@ cas_status_t ring_upload(size_t bytes, void *ws, hipStream_t stream, Fill &&fill
       if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipEventSynchronize: ") + hipGetErrorString(e));
       r.used[i] = false;
     }
-    if (r.host) hipHostFree(r.host);
-    r.host = nullptr;
+    if (r.host) {
+      e = hipHostFree(r.host);
+      r.host = nullptr;
+      r.slot_bytes = 0;
+      if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipHostFree: ") + hipGetErrorString(e));
+    }
     size_t sb = kMinSlotBytes;
     while (sb < bytes) sb *= 2;
     e = hipHostMalloc((void **)&r.host, sb * kSlots, hipHostMallocDefault);
@@ -613,7 +660,7 @@ void fill_tables(const Plan &pl, bool bwd, char *h) {
   if (!pl.segs.empty()) std::memcpy(h + pl.off_segs, pl.segs.data(), pl.segs.size() * sizeof(DevSeg));
   std::memcpy(h + pl.off_rows, pl.rows.data(), pl.rows.size() * sizeof(DevRow));
   if (!pl.tiles.empty()) std::memcpy(h + pl.off_tiles, pl.tiles.data(), pl.tiles.size() * sizeof(DevTile));
-  std::memcpy(h + pl.off_rorder, pl.row_order.data(), pl.row_order.size() * sizeof(int32_t));
+  if (!pl.items.empty()) std::memcpy(h + pl.off_items, pl.items.data(), pl.items.size() * sizeof(DevItem));
   if (bwd) {
     if (!pl.carts.empty()) std::memcpy(h + pl.off_carts, pl.carts.data(), pl.carts.size() * sizeof(DevCart));
     if (!pl.uses.empty()) std::memcpy(h + pl.off_uses, pl.uses.data(), pl.uses.size() * sizeof(int32_t));
@@ -1013,7 +1060,7 @@ cas_status_t prefix_attn_fwd_run(const cas_problem_t *p, const void *q, const vo
   fp.segs = (const DevSeg *)(ws + pl.off_segs);
   fp.rows = (const DevRow *)(ws + pl.off_rows);
   fp.tiles = (const DevTile *)(ws + pl.off_tiles);
-  fp.row_order = (const int32_t *)(ws + pl.off_rorder);
+  fp.items = (const DevItem *)(ws + pl.off_items);
   fp.ovf_flag = pl.dt == kBF16 ? (int32_t *)(ws + pl.off_ovf) : nullptr;
   fp.plane = pl.T * pl.Hq;
   fp.B = pl.B;
@@ -1024,7 +1071,7 @@ cas_status_t prefix_attn_fwd_run(const cas_problem_t *p, const void *q, const vo
   fp.nqblk = pl.nqblk_fwd;
   fp.splits = pl.fwd_splits;
   fp.lse_hs = pl.packed ? (int32_t)pl.T : pl.Sq;
-  fp.xcds = pl.xcds;
+  fp.n_items = (int32_t)pl.items.size();
   fp.scale_log2 = pl.scale * 1.4426950408889634f;
   hipError_t e = launch("fwd", [&] { return launch_fwd(fp, pl.dt, pl.D, stream); });
   if (e != hipSuccess) return hip_fail("fwd launch", e);
@@ -1214,7 +1261,7 @@ cas_status_t cas_plan_info(const cas_problem_t *p, cas_plan_info_t *out) {
   if (s != CAS_OK) return s;
   out->fwd_splits = pf.fwd_splits;
   out->dq_splits = pb.dq_splits;
-  out->fwd_workgroups = pf.nqblk_fwd * pf.Hkv * pf.B * pf.fwd_splits;
+  out->fwd_workgroups = pf.dt == kBF16 ? (int32_t)pf.items.size() : pf.nqblk_fwd * pf.Hkv * pf.B * pf.fwd_splits;
   out->dkdv_workgroups = (int32_t)pb.order_cap;
   out->unique_segments = (int32_t)pb.carts.size();
   out->total_key_tiles = (int32_t)(pb.order_cap / pb.Hkv);
@@ -1304,7 +1351,7 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
     dp.part_dq = pl.dq_splits > 1 ? (float *)(ws + pl.off_part_dq) : nullptr;
     dp.segs = (const DevSeg *)(ws + pl.off_segs);
     dp.tiles = (const DevTile *)(ws + pl.off_tiles);
-    dp.row_order = (const int32_t *)(ws + pl.off_rorder);
+    dp.items = (const DevItem *)(ws + pl.off_items);
     dp.rows = (const DevRow *)(ws + pl.off_rows);
     dp.plane = pl.T * pl.Hq;
     dp.B = pl.B;
@@ -1314,7 +1361,7 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
     dp.nrows_max = pl.nrows_max;
     dp.nqblk = pl.nqblk_dq;
     dp.splits = pl.dq_splits;
-    dp.xcds = pl.xcds;
+    dp.n_items = (int32_t)pl.items.size();
     dp.scale_log2 = scale_log2;
     dp.scale = pl.scale;
     hipError_t r = timed("dq", stream, [&] { return launch_dq(dp, pl.dt, pl.D, stream); });

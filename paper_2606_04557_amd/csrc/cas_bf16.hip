@@ -96,21 +96,6 @@ __device__ __forceinline__ void fence_regs(T (&v)[N]) {
   for (int i = 0; i < N; ++i) asm volatile("" : "+v"(v[i]));
 }
 
-// XCD-aware workgroup order. Consecutive workgroup ids are dispatched
-// round-robin over the XCDs (8 on a whole MI355X, each with its own L2);
-// this remaps them so that each XCD receives one contiguous range of
-// logical ids. Workgroups that
-// stream the same K/V tiles (same batch row and KV head, adjacent logical
-// ids) then share one L2 instead of fetching every tile once per XCD. With
-// the KV head as the slowest logical index, each XCD gets whole KV heads
-// (when their count is a multiple of the XCD count): the same work on every XCD even
-// when the batch rows differ in length.
-__device__ __forceinline__ int xcd_order(int bid, int n, int xcds) {
-  const int per = n / xcds;
-  if (bid >= per * xcds) return bid;   // the remainder keeps its id
-  return (bid % xcds) * per + bid / xcds;
-}
-
 // Workgroup barrier that orders LDS use: this wave's LDS reads have returned,
 // and the compiler moves no memory access across it. Outstanding direct
 // global->LDS copies are not waited for (wait_vmcnt does that).
@@ -196,23 +181,19 @@ void fwd_bf16_kernel(FwdParams p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2;
   const int G = lane >> 5, n = lane & 31;
-  // Logical order: row block fastest (the last one, with the most causal
-  // self tiles, first), then split, batch row (the rows with the most key
-  // tiles first), KV head (the KV heads split the XCDs evenly whatever the
-  // rows' lengths).
-  int bid = xcd_order(blockIdx.x, gridDim.x, p.xcds);
-  const int qblk = __builtin_amdgcn_readfirstlane(p.nqblk - 1 - bid % p.nqblk);
-  bid /= p.nqblk;
-  const int split = __builtin_amdgcn_readfirstlane(bid % p.splits);
-  bid /= p.splits;
-  const int b = __builtin_amdgcn_readfirstlane(load_const(p.row_order, bid % p.B));
-  const int kvh = __builtin_amdgcn_readfirstlane(bid / p.B);
+  // The host lists the workgroups in dispatch order: per XCD, whole KV heads
+  // where they divide evenly, longest first.
+  const DevItem item = load_const(p.items, (int)blockIdx.x);
+  const int qblk = __builtin_amdgcn_readfirstlane(item.qblk);
+  const int split = __builtin_amdgcn_readfirstlane(item.split);
+  const int b = __builtin_amdgcn_readfirstlane(item.b);
+  const int kvh = __builtin_amdgcn_readfirstlane(item.kvh);
   const int g = p.g, Hkv = p.Hkv, Hq = Hkv * g;
   const DevRow row = load_const(p.rows, b);
   const int tok0 = __builtin_amdgcn_readfirstlane(row.tok0);
   const int nrows = __builtin_amdgcn_readfirstlane(row.len) * g;
   const int wg_row0 = qblk * kFastRowsPerWg;
-  if (wg_row0 >= nrows) return;   // grid sized for the longest row
+  if (wg_row0 >= nrows) return;   // (the host lists only blocks with rows)
   if constexpr (FIXUP) {
     if (load_const(p.ovf_flag, (int)blockIdx.x) == 0) return;
   }
@@ -598,24 +579,20 @@ void dq_bf16_kernel(DqParams p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2;
   const int G = lane >> 5, n = lane & 31;
-  // Logical order: row block fastest (the last one, with the most causal
-  // self tiles, first), then split, batch row (the rows with the most key
-  // tiles first), KV head (the KV heads split the XCDs evenly whatever the
-  // rows' lengths).
-  int bid = xcd_order(blockIdx.x, gridDim.x, p.xcds);
-  const int qblk = __builtin_amdgcn_readfirstlane(p.nqblk - 1 - bid % p.nqblk);
-  bid /= p.nqblk;
-  const int split = __builtin_amdgcn_readfirstlane(bid % p.splits);
-  bid /= p.splits;
-  const int b = __builtin_amdgcn_readfirstlane(load_const(p.row_order, bid % p.B));
-  const int kvh = __builtin_amdgcn_readfirstlane(bid / p.B);
+  // The host lists the workgroups in dispatch order: per XCD, whole KV heads
+  // where they divide evenly, longest first.
+  const DevItem item = load_const(p.items, (int)blockIdx.x);
+  const int qblk = __builtin_amdgcn_readfirstlane(item.qblk);
+  const int split = __builtin_amdgcn_readfirstlane(item.split);
+  const int b = __builtin_amdgcn_readfirstlane(item.b);
+  const int kvh = __builtin_amdgcn_readfirstlane(item.kvh);
 
   const int g = p.g, Hkv = p.Hkv, Hq = Hkv * g;
   const DevRow row = load_const(p.rows, b);
   const int tok0 = __builtin_amdgcn_readfirstlane(row.tok0);
   const int nrows = __builtin_amdgcn_readfirstlane(row.len) * g;
   const int wg_row0 = qblk * kFastRowsPerWg;
-  if (wg_row0 >= nrows) return;   // grid sized for the longest row
+  if (wg_row0 >= nrows) return;   // (the host lists only blocks with rows)
   const int wg_row1 = min(nrows, wg_row0 + kFastRowsPerWg);
   const int row0 = wg_row0 + wave * kFastRowsPerWave;
   const bool wave_active = row0 < nrows;
@@ -1600,7 +1577,7 @@ void dkdv_bf16_kernel(DkdvParams p) {
 }
 
 hipError_t launch_fwd_bf16(const FwdParams &p, int D, hipStream_t s) {
-  const int64_t grid = (int64_t)p.nqblk * p.Hkv * p.splits * p.B;
+  const int64_t grid = p.n_items;
   if (D == 64) {
     hipLaunchKernelGGL((fwd_bf16_kernel<64, false>), dim3((unsigned)grid), dim3(kFastThreads), 0, s, p);
     hipLaunchKernelGGL((fwd_bf16_kernel<64, true>), dim3((unsigned)grid), dim3(kFastThreads), 0, s, p);
@@ -1612,7 +1589,7 @@ hipError_t launch_fwd_bf16(const FwdParams &p, int D, hipStream_t s) {
 }
 
 hipError_t launch_dq_bf16(const DqParams &p, int D, hipStream_t s) {
-  const int64_t grid = (int64_t)p.nqblk * p.Hkv * p.splits * p.B;
+  const int64_t grid = p.n_items;
   if (D == 64)
     hipLaunchKernelGGL(dq_bf16_kernel<64>, dim3((unsigned)grid), dim3(kFastThreads), 0, s, p);
   else

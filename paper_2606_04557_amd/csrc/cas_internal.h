@@ -86,6 +86,15 @@ struct DevWg {
   int32_t kvh;
 };
 
+// One workgroup of the bf16 forward or dQ kernel: 256-row query block qblk
+// of batch row b at KV head kvh, key-axis split `split`.
+struct DevItem {
+  int32_t qblk;
+  int32_t split;
+  int32_t b;
+  int32_t kvh;
+};
+
 enum DType : int32_t { kBF16 = 0, kFP32 = 1 };
 
 struct FwdParams {
@@ -99,12 +108,12 @@ struct FwdParams {
   const DevSeg *segs;
   const DevRow *rows;
   const DevTile *tiles;
-  const int32_t *row_order;   // [B] bf16 workgroup order: batch rows, most key tiles first
+  const DevItem *items;       // [n_items] bf16: workgroup i takes items[i]
   int32_t *ovf_flag;  // [grid] bf16: workgroup needs the exact-maximum pass
   int64_t plane;      // T * Hq: rows of one split partial plane
   int32_t B, Smax, Hkv, g, nrows_max, nqblk, splits;
   int32_t lse_hs;     // lse head stride (q_len, or T for packed samples)
-  int32_t xcds;       // XCDs of the device (bf16 workgroup order)
+  int32_t n_items;    // bf16 grid
   float scale_log2;   // softmax_scale * log2(e)
 };
 
@@ -143,10 +152,10 @@ struct DqParams {
   const DevSeg *segs;
   const DevRow *rows;
   const DevTile *tiles;
-  const int32_t *row_order;   // [B] bf16 workgroup order: batch rows, most key tiles first
+  const DevItem *items;       // [n_items] bf16: workgroup i takes items[i]
   int64_t plane;
   int32_t B, Smax, Hkv, g, nrows_max, nqblk, splits;
-  int32_t xcds;       // XCDs of the device (bf16 workgroup order)
+  int32_t n_items;    // bf16 grid
   float scale_log2;
   float scale;
 };
