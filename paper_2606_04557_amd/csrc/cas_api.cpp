@@ -502,19 +502,23 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl, int fwd_spli
 
 // dK/dV workgroup list: every cartridge tile (and, with self gradients, every
 // self tile of every row) at every KV head, sorted by the number of 64-row
-// query blocks the workgroup walks, most first; ties keep KV head, then tile
-// order. Longest-first dispatch keeps the long workgroups off the tail.
+// query blocks the workgroup walks, most first; ties go by KV head, then by
+// the tile's position within its cartridge (or the row's self keys), then
+// tile order. Longest-first dispatch keeps the long workgroups off the tail;
+// the position tie-break lets the workgroups that run side by side on an XCD
+// come from all the cartridges (and so rows) of their KV head, instead of
+// all walking one row's query blocks.
 void build_dkdv_order(Plan &pl, bool with_self) {
   struct E {
     int64_t nblk;
-    int32_t tile, kvh;
+    int32_t tile, kvh, pos;   // pos: tile within its cartridge or the row's self keys
   };
   std::vector<E> v;
   v.reserve((size_t)pl.order_cap);
   for (const DevCart &c : pl.carts) {
     const int n = (int)ceil_div(c.len, kDkdvKeyTile);
     for (int kvh = 0; kvh < pl.Hkv; ++kvh)
-      for (int t = 0; t < n; ++t) v.push_back({c.nblk, c.tile_begin + t, kvh});
+      for (int t = 0; t < n; ++t) v.push_back({c.nblk, c.tile_begin + t, kvh, t});
   }
   if (with_self) {
     for (int b = 0; b < pl.B; ++b) {
@@ -523,12 +527,13 @@ void build_dkdv_order(Plan &pl, bool with_self) {
       for (int kvh = 0; kvh < pl.Hkv; ++kvh)
         for (int j = 0; j < n; ++j)
           v.push_back({nqb - ((int64_t)j * kDkdvKeyTile * pl.g) / kDkdvQBlock,
-                       pl.cart_tiles + b * pl.self_tiles_max + j, kvh});
+                       pl.cart_tiles + b * pl.self_tiles_max + j, kvh, j});
     }
   }
   std::stable_sort(v.begin(), v.end(), [](const E &a, const E &b) {
     if (a.nblk != b.nblk) return a.nblk > b.nblk;
     if (a.kvh != b.kvh) return a.kvh < b.kvh;
+    if (a.pos != b.pos) return a.pos < b.pos;
     return a.tile < b.tile;
   });
   pl.order.resize(v.size());
