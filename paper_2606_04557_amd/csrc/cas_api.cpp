@@ -99,16 +99,20 @@ struct Plan {
   std::vector<DevCart> carts;
   std::vector<int32_t> uses;
   std::vector<DevWg> order;       // dK/dV workgroups, longest first
+  std::vector<DevQueue> queues;   // bf16 dK/dV: per-XCD lists of `order` (empty: entry = workgroup id)
+  int64_t dkdv_grid = 0;          // dK/dV workgroups launched
   int self_tiles_max = 0;         // dK/dV self tiles of the longest row
   int64_t order_cap = 0;          // order entries with every self tile
   int64_t max_prefix = 0;
   int fwd_splits = 1, dq_splits = 1;
   int xcds = 8;                   // XCDs of the device (workgroup order of the bf16 kernels)
+  int cus = 256;                  // compute units of the device
   int nqblk_fwd = 0, nqblk_dq = 0;
   int cart_tiles = 0;
   bool want_self_grad = false;
   // workspace layout
   size_t off_segs = 0, off_rows = 0, off_tiles = 0, off_items = 0, off_carts = 0, off_uses = 0, off_order = 0,
+         off_queues = 0, off_claim = 0,
          table_bytes = 0;
   size_t off_part_o = 0, off_part_lse = 0, off_ovf = 0, ws_fwd = 0;
   size_t off_nd = 0, off_lse2 = 0, off_part_dq = 0, off_qT = 0, off_doT = 0, ws_bwd = 0;
@@ -362,6 +366,7 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl, int fwd_spli
   }
   const Topology topo = device_topology();
   pl.xcds = topo.xcds;
+  pl.cus = topo.cus;
   pl.fwd_splits = tu.fwd_splits > 0 ? std::min(tu.fwd_splits, kMaxSplits)
                                     : auto_splits(base_fwd, min_row_tiles, topo.cus);
   if (fwd_split_cap > 0) pl.fwd_splits = std::min(pl.fwd_splits, fwd_split_cap);
@@ -462,6 +467,10 @@ cas_status_t build_plan(const cas_problem_t *p, bool bwd, Plan &pl, int fwd_spli
     off = align_up(off + pl.uses.size() * sizeof(int32_t), 256);
     pl.off_order = off;
     off = align_up(off + (size_t)pl.order_cap * sizeof(DevWg), 256);
+    pl.off_queues = off;
+    off = align_up(off + (size_t)pl.xcds * sizeof(DevQueue), 256);
+    pl.off_claim = off;   // claim counters: zero in every table upload
+    off = align_up(off + (size_t)pl.xcds * sizeof(int32_t), 256);
   }
   pl.table_bytes = off;
   const size_t plane = (size_t)pl.T * pl.Hq;   // packed rows of all batch rows and KV heads
@@ -537,16 +546,38 @@ void build_dkdv_order(Plan &pl, bool with_self) {
     return a.tile < b.tile;
   });
   pl.order.resize(v.size());
+  pl.queues.clear();
+  pl.dkdv_grid = (int64_t)v.size();
   const int X = pl.xcds;
+  if (v.empty()) return;
   if (X > 1 && pl.Hkv % X == 0) {
-    // XCD-affine: workgroup i runs on XCD i % X (round-robin dispatch), so
-    // entry i takes the next workgroup of KV heads h with h % X == i % X.
-    // Every KV head has the same tiles, so the X lists are equally long and
-    // each keeps the longest-first order; the query blocks of one (row, KV
-    // head) are then streamed by one XCD's L2 only.
-    std::vector<size_t> next(X, 0);
+    // XCD-affine: workgroup i runs on XCD i % X (round-robin dispatch), and
+    // XCD x takes the entries of KV heads h with h % X == x, longest first.
+    // Every KV head has the same tiles, so the X lists are equally long; the
+    // query blocks of one (row, KV head) are then streamed by one XCD's L2.
     std::vector<std::vector<E>> q(X);
     for (const E &e : v) q[e.kvh % X].push_back(e);
+    const int64_t per_cu = std::max(1, pl.cus / X);   // CUs of one XCD
+    const int64_t cnt = (int64_t)q[0].size();
+    if (pl.dt == kBF16 && (int64_t)X * (cnt + per_cu) <= INT32_MAX) {
+      // Each XCD's list in one piece: a static head, taken by workgroup
+      // index, and a tail of its shortest entries (two rounds of the XCD's
+      // CUs, or an eighth of the list) claimed at run time, by the XCD's own
+      // workgroups first and then by XCDs that finished their own lists; one
+      // more round of workgroups per XCD is launched for that. XCDs run at
+      // different speeds (up to 4 % apart on one chip), so a fixed share per
+      // XCD ends with the slowest.
+      const int64_t tail = std::min(cnt, std::max(2 * per_cu, cnt / 8));
+      pl.queues.resize(X);
+      size_t at = 0;
+      for (int x = 0; x < X; ++x) {
+        pl.queues[x] = {(int32_t)at, (int32_t)cnt, (int32_t)(cnt - tail), 0};
+        for (const E &e : q[x]) pl.order[at++] = {e.tile, e.kvh};
+      }
+      pl.dkdv_grid = (int64_t)X * (cnt + per_cu);
+      return;
+    }
+    std::vector<size_t> next(X, 0);
     for (size_t i = 0; i < v.size(); ++i) {
       const E &e = q[i % X][next[i % X]++];
       pl.order[i] = {e.tile, e.kvh};
@@ -670,6 +701,8 @@ void fill_tables(const Plan &pl, bool bwd, char *h) {
     if (!pl.carts.empty()) std::memcpy(h + pl.off_carts, pl.carts.data(), pl.carts.size() * sizeof(DevCart));
     if (!pl.uses.empty()) std::memcpy(h + pl.off_uses, pl.uses.data(), pl.uses.size() * sizeof(int32_t));
     if (!pl.order.empty()) std::memcpy(h + pl.off_order, pl.order.data(), pl.order.size() * sizeof(DevWg));
+    if (!pl.queues.empty())
+      std::memcpy(h + pl.off_queues, pl.queues.data(), pl.queues.size() * sizeof(DevQueue));
   }
 }
 
@@ -1342,7 +1375,7 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
   hipError_t e = timed("bwd_pre", stream, [&] { return launch_bwd_pre(pp, pl.dt, pl.D, stream); });
   if (e != hipSuccess) return hip_fail("bwd_pre launch", e);
 
-  const int n_wg = (int)pl.order.size();
+  const int n_wg = (int)pl.dkdv_grid;
   auto run_dq = [&]() -> hipError_t {
     if (!dq) return hipSuccess;
     DqParams dp{};
@@ -1400,6 +1433,9 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
     kp.uses = (const int32_t *)(ws + pl.off_uses);
     kp.rows = pp.rows;
     kp.order = (const DevWg *)(ws + pl.off_order);
+    kp.queues = pl.queues.empty() ? nullptr : (const DevQueue *)(ws + pl.off_queues);
+    kp.claim = pl.queues.empty() ? nullptr : (int32_t *)(ws + pl.off_claim);
+    kp.xcds = pl.xcds;
     kp.n_carts = (int32_t)pl.carts.size();
     kp.cart_tiles = pl.cart_tiles;
     kp.self_tiles = std::max(pl.self_tiles_max, 1);

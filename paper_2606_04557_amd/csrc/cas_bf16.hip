@@ -106,6 +106,44 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// The dK/dV order entry of this workgroup when the lists are per XCD
+// (DevQueue): workgroup j of XCD x takes entry j of the XCD's static head;
+// past the head, thread 0 claims the next tail entry with an atomic counter,
+// of its own XCD first, then of the XCD with the most unclaimed entries
+// left, and the workgroup reads it from LDS. -1: nothing left. Every tail
+// entry is claimed exactly once: each XCD launches at least as many tail
+// workgroups as its tail holds, and each tries its own tail first.
+__device__ __forceinline__ int dkdv_entry(const DkdvParams &p, int tid, int &slot) {
+  const int X = p.xcds;
+  const int x = (int)blockIdx.x % X, j = (int)blockIdx.x / X;
+  const DevQueue own = load_const(p.queues, x);
+  if (j < own.head) return own.off + j;
+  if (tid == 0) {
+    int e = -1, y = x;
+    for (int attempt = 0; attempt < 2 * X && e < 0; ++attempt) {
+      if (attempt > 0) {
+        int best = -1, most = 0;
+        for (int z = 0; z < X; ++z) {
+          const DevQueue qz = p.queues[z];
+          const int left = (qz.cnt - qz.head) - __hip_atomic_load(p.claim + z, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          if (left > most) {
+            most = left;
+            best = z;
+          }
+        }
+        if (best < 0) break;
+        y = best;
+      }
+      const DevQueue qy = p.queues[y];
+      const int i = __hip_atomic_fetch_add(p.claim + y, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (i < qy.cnt - qy.head) e = qy.off + qy.head + i;
+    }
+    slot = e;
+  }
+  __syncthreads();
+  return __builtin_amdgcn_readfirstlane(slot);
+}
+
 // Key tiles of one batch row at one KV head, from the row's slice of the
 // host-built tile table (one scalar load per tile): the prefix tiles in
 // segment order, then the causal self tiles.
@@ -985,7 +1023,11 @@ void dkdv_bf16_kernel(DkdvParams p) {
   // immediates.
   constexpr int XCH = 8 * RB;                  // P of each SIMD's 32 keys x 64 rows, 4 KiB per SIMD
   constexpr int STATS = XCH + 16384;           // LSE2 x2, D x2
-  __shared__ __attribute__((aligned(1024))) char smem[STATS + 4 * QB * 4];
+  constexpr int CLAIM = STATS + 4 * QB * 4;   // claimed order entry (DevQueue lists)
+  // One arena for every LDS use: a second LDS object would keep the
+  // compiler from telling the direct-to-LDS copies' targets from the LDS
+  // reads, and it would then wait for every outstanding copy before each read.
+  __shared__ __attribute__((aligned(1024))) char smem[CLAIM + 16];
   char *const qr0 = smem, *const qr1 = smem + RB, *const ot0 = smem + 2 * RB, *const ot1 = smem + 3 * RB;
   char *const or0 = smem + 4 * RB, *const or1 = smem + 5 * RB, *const qt0 = smem + 6 * RB,
               *const qt1 = smem + 7 * RB;
@@ -999,7 +1041,12 @@ void dkdv_bf16_kernel(DkdvParams p) {
   const int G = lane >> 5, n = lane & 31;
   const int q = wave & 3;                      // SIMD, key quarter, index within the wave's group
   const bool pwave = wave < 4;
-  const DevWg wg = load_const(p.order, (int)blockIdx.x);
+  int entry = (int)blockIdx.x;
+  if (p.queues) {
+    entry = dkdv_entry(p, tid, *reinterpret_cast<int *>(smem + CLAIM));
+    if (entry < 0) return;   // every list is done
+  }
+  const DevWg wg = load_const(p.order, entry);
   const int tile = __builtin_amdgcn_readfirstlane(wg.tile), kvh = __builtin_amdgcn_readfirstlane(wg.kvh);
   const int g = p.g, Hkv = p.Hkv, Hq = Hkv * g;
   const float c = p.scale_log2;

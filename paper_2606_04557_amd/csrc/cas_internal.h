@@ -86,6 +86,17 @@ struct DevWg {
   int32_t kvh;
 };
 
+// The bf16 dK/dV list of one XCD: entries [off, off + cnt) of the order table.
+// Workgroup j of the XCD takes entry off + j while j < head; the entries from
+// head on (the list's shortest) are claimed at run time, first by the XCD's
+// own workgroups, then by any XCD that has run out of its own.
+struct DevQueue {
+  int32_t off;
+  int32_t cnt;
+  int32_t head;
+  int32_t pad;
+};
+
 // One workgroup of the bf16 forward or dQ kernel: 256-row query block qblk
 // of batch row b at KV head kvh, key-axis split `split`.
 struct DevItem {
@@ -183,7 +194,10 @@ struct DkdvParams {
   const DevCart *carts;
   const int32_t *uses;
   const DevRow *rows;
-  const DevWg *order;       // [grid] the workgroups' tiles and KV heads
+  const DevWg *order;       // the workgroups' tiles and KV heads ([grid] without queues)
+  const DevQueue *queues;   // bf16: [xcds] per-XCD lists of `order`, or null (entry = workgroup id)
+  int32_t *claim;           // bf16: [xcds] tail entries claimed so far (zero at launch)
+  int32_t xcds;             // bf16 with queues: workgroup i runs on XCD i % xcds
   int32_t n_carts;
   int32_t cart_tiles;       // dK/dV tiles over all distinct cartridges
   int32_t self_tiles;       // dK/dV tiles per batch row over the self keys (longest row)
