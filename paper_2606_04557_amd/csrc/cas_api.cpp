@@ -1372,7 +1372,10 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
   pp.q = q;
   pp.qT = pl.dt == kBF16 ? ws + pl.off_qT : nullptr;
   pp.doT = pl.dt == kBF16 ? ws + pl.off_doT : nullptr;
-  hipError_t e = timed("bwd_pre", stream, [&] { return launch_bwd_pre(pp, pl.dt, pl.D, stream); });
+  // bf16: the statistics and the transposed Q / dO blocks in one pass.
+  hipError_t e = timed("bwd_pre", stream, [&] {
+    return pl.dt == kBF16 ? launch_bwd_prologue_bf16(pp, pl.D, stream) : launch_bwd_pre(pp, pl.dt, pl.D, stream);
+  });
   if (e != hipSuccess) return hip_fail("bwd_pre launch", e);
 
   const int n_wg = (int)pl.dkdv_grid;
@@ -1444,10 +1447,6 @@ cas_status_t cas_prefix_attn_bwd(const cas_problem_t *p, const void *q, const vo
     kp.g = pl.g;
     kp.scale_log2 = scale_log2;
     kp.scale = pl.scale;
-    if (pl.dt == kBF16) {
-      e = timed("bwd_transpose", stream, [&] { return launch_bwd_transpose_bf16(pp, pl.D, stream); });
-      if (e != hipSuccess) return hip_fail("bwd_transpose launch", e);
-    }
     e = timed("dkdv", stream, [&] { return launch_dkdv(kp, pl.dt, pl.D, n_wg, stream); });
     if (e != hipSuccess) return hip_fail("dkdv launch", e);
   }

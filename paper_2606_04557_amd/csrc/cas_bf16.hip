@@ -925,15 +925,18 @@ void dq_bf16_kernel(DqParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Backward prologue for the bf16 dK/dV kernel: Q and dO of every 64-row
-// query block of each (batch row, KV head), transposed to [channel][64 rows],
-// zero beyond the row's last packed row. Within each 16-row group the rows
-// are stored in the order 0-3, 8-11, 4-7, 12-15, so the 8 rows that one lane
-// group of a 32x32 MFMA fragment needs (4G..4G+3 and 8+4G..8+4G+3) are one
-// 16-byte chunk.
+// bf16 backward prologue, per 64-row query block of each (batch row, KV
+// head):
+//  * the row statistics: -D = -rowsum(dO * O) and LSE * log2(e);
+//  * Q and dO transposed to [channel][64 rows] for the dK/dV kernel, zero
+//    beyond the row's last packed row. Within each 16-row group the rows are
+//    stored in the order 0-3, 8-11, 4-7, 12-15, so the 8 rows that one lane
+//    group of a 32x32 MFMA fragment needs (4G..4G+3 and 8+4G..8+4G+3) are
+//    one 16-byte chunk.
+// dO is read once for both.
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(256) void bwd_transpose_bf16_kernel(PreParams p) {
+__global__ __launch_bounds__(256) void bwd_prologue_bf16_kernel(PreParams p) {
   __shared__ __attribute__((aligned(16))) __bf16 tile[64][D + 8];
   const int tid = threadIdx.x;
   const int qb = blockIdx.x % p.nqb_max;
@@ -957,6 +960,32 @@ __global__ __launch_bounds__(256) void bwd_transpose_bf16_kernel(PreParams p) {
       *reinterpret_cast<uint4 *>(&tile[r][c8 * 8]) = v;
     }
     __syncthreads();
+    if (which == 1) {
+      // -D and LSE2 of the block's rows: four lanes per row, D/4 channels each.
+      constexpr int CQ = D / 4;
+      const int r = tid >> 2, k = tid & 3;
+      const int rr = qb * 64 + r;
+      float acc = 0.0f;
+      int t = 0, h = 0;
+      if (rr < nrows) {
+        t = rr / g;
+        h = kvh * g + (rr - t * g);
+        const __bf16 *op = (const __bf16 *)p.o + (((int64_t)row.tok0 + t) * Hq + h) * D + k * CQ;
+#pragma unroll
+        for (int c8 = 0; c8 < CQ / 8; ++c8) {
+          const bf16x8 ov = *reinterpret_cast<const bf16x8 *>(op + c8 * 8);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc += (float)ov[e] * (float)tile[r][k * CQ + c8 * 8 + e];
+        }
+      }
+      acc += __shfl_xor(acc, 1, 4);
+      acc += __shfl_xor(acc, 2, 4);
+      if (rr < nrows && k == 0) {
+        const int64_t R = (int64_t)row.tok0 * Hq + (int64_t)kvh * nrows + rr;
+        p.nd[R] = -acc;
+        p.lse2[R] = p.lse[(int64_t)row.lse0 + (int64_t)h * p.lse_hs + t] * kLog2e;
+      }
+    }
     for (int i = tid; i < D * 8; i += 256) {
       const int d = i / 8, pg = i % 8;
       bf16x8 out;
@@ -1657,12 +1686,12 @@ hipError_t launch_dkdv_bf16(const DkdvParams &p, int D, int n_wg, hipStream_t s)
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_transpose_bf16(const PreParams &p, int D, hipStream_t s) {
+hipError_t launch_bwd_prologue_bf16(const PreParams &p, int D, hipStream_t s) {
   const dim3 grid((unsigned)(p.Hkv * p.nqb_max), (unsigned)p.B);
   if (D == 64)
-    hipLaunchKernelGGL(bwd_transpose_bf16_kernel<64>, grid, dim3(256), 0, s, p);
+    hipLaunchKernelGGL(bwd_prologue_bf16_kernel<64>, grid, dim3(256), 0, s, p);
   else
-    hipLaunchKernelGGL(bwd_transpose_bf16_kernel<128>, grid, dim3(256), 0, s, p);
+    hipLaunchKernelGGL(bwd_prologue_bf16_kernel<128>, grid, dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

@@ -299,7 +299,7 @@ constexpr int kBf16RowsPerWg = 256;
 hipError_t launch_fwd_bf16(const FwdParams &p, int D, hipStream_t s);
 hipError_t launch_dq_bf16(const DqParams &p, int D, hipStream_t s);
 hipError_t launch_dkdv_bf16(const DkdvParams &p, int D, int n_wg, hipStream_t s);
-hipError_t launch_bwd_transpose_bf16(const PreParams &p, int D, hipStream_t s);
+hipError_t launch_bwd_prologue_bf16(const PreParams &p, int D, hipStream_t s);
 hipError_t launch_adam_bf16(const AdamParams &p, int D, int n_chunks, hipStream_t s);
 hipError_t launch_decode_bf16(const DecodeParams &p, int D, int n_work, hipStream_t s);
 hipError_t launch_decode_merge_bf16(const DecodeParams &p, int D, hipStream_t s);
