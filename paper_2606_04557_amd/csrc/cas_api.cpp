@@ -618,7 +618,8 @@ void add_segment_intervals(const Plan &pl, const cas_problem_t *p, bool with_gra
 }
 
 // ---------------------------------------------------------------------------
-// Pinned staging ring for segment tables (host -> workspace copies).
+// Pinned staging ring for launch tables (host -> workspace, copied by a
+// small kernel on the launch stream).
 // ---------------------------------------------------------------------------
 constexpr size_t kMinSlotBytes = 1 << 20;
 constexpr int kSlots = 8;
@@ -665,7 +666,9 @@ cas_status_t ring_upload(size_t bytes, void *ws, hipStream_t stream, Fill &&fill
     }
     size_t sb = kMinSlotBytes;
     while (sb < bytes) sb *= 2;
-    e = hipHostMalloc((void **)&r.host, sb * kSlots, hipHostMallocDefault);
+    // Coherent: the upload kernel reads the slots the host has just
+    // rewritten, so no GPU cache may keep an earlier upload's lines.
+    e = hipHostMalloc((void **)&r.host, sb * kSlots, hipHostMallocCoherent);
     if (e != hipSuccess) {
       r.host = nullptr;
       r.slot_bytes = 0;
@@ -682,8 +685,8 @@ cas_status_t ring_upload(size_t bytes, void *ws, hipStream_t stream, Fill &&fill
   char *h = r.host + (size_t)slot * r.slot_bytes;
   std::memset(h, 0, bytes);
   fill(h);
-  e = hipMemcpyAsync(ws, h, bytes, hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipMemcpyAsync: ") + hipGetErrorString(e));
+  e = launch_table_upload(ws, h, bytes, stream);
+  if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("table upload launch: ") + hipGetErrorString(e));
   e = hipEventRecord(r.ev[slot], stream);
   if (e != hipSuccess) return fail(CAS_ERR_HIP, std::string("hipEventRecord: ") + hipGetErrorString(e));
   r.used[slot] = true;

@@ -14,6 +14,8 @@
 // prefix tile; self tiles are masked only where they cross the diagonal.
 // With splits > 1 each workgroup takes a contiguous share of the key tiles
 // and writes a normalised partial O and its LSE, merged afterwards.
+#include <algorithm>
+
 #include "cas_device.h"
 
 namespace cas {
@@ -273,6 +275,26 @@ static hipError_t launch_merge_t(const MergeParams &p, hipStream_t s) {
   const int64_t n = (int64_t)p.Hkv * p.nrows_max * (D / 4);
   const dim3 grid((unsigned)((n + kThreads - 1) / kThreads), (unsigned)p.B);
   hipLaunchKernelGGL((fwd_merge_kernel<T, D>), grid, dim3(kThreads), 0, s, p);
+  return hipGetLastError();
+}
+
+// Launch-table upload: copies `bytes` from pinned host memory to the device
+// workspace (both 16-byte aligned), 16 bytes per thread and the last
+// bytes % 16 one by one. A kernel on the launch stream instead of a
+// copy-engine transfer, so the kernels that read the tables follow it
+// without a hand-over between engines.
+__global__ __launch_bounds__(256) void table_upload_kernel(char *dst, const char *src, int64_t bytes) {
+  const int64_t n16 = bytes / 16;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (int64_t)gridDim.x * 256)
+    reinterpret_cast<uint4 *>(dst)[i] = reinterpret_cast<const uint4 *>(src)[i];
+  if (blockIdx.x == 0 && threadIdx.x < (unsigned)(bytes - n16 * 16)) dst[n16 * 16 + threadIdx.x] = src[n16 * 16 + threadIdx.x];
+}
+
+hipError_t launch_table_upload(void *dst, const void *src, size_t bytes, hipStream_t s) {
+  if (bytes == 0) return hipSuccess;
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>(((int64_t)bytes / 16 + 255) / 256, 64));
+  hipLaunchKernelGGL(table_upload_kernel, dim3((unsigned)blocks), dim3(256), 0, s, (char *)dst, (const char *)src,
+                     (int64_t)bytes);
   return hipGetLastError();
 }
 

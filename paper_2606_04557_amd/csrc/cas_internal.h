@@ -290,6 +290,7 @@ hipError_t launch_table_upload(const void *host, size_t bytes, void *dst, hipStr
 // Kernel launchers (defined in the .hip files).
 hipError_t launch_fwd(const FwdParams &p, DType dt, int D, hipStream_t s);
 hipError_t launch_fwd_merge(const MergeParams &p, DType dt, int D, hipStream_t s);
+hipError_t launch_table_upload(void *dst, const void *src, size_t bytes, hipStream_t s);
 hipError_t launch_bwd_pre(const PreParams &p, DType dt, int D, hipStream_t s);
 hipError_t launch_dq(const DqParams &p, DType dt, int D, hipStream_t s);
 hipError_t launch_dq_reduce(const DqReduceParams &p, DType dt, int D, hipStream_t s);
