@@ -25,6 +25,9 @@
 //              before the barrier that starts it
 //   inter      no barriers: every wave interleaves its own conversion of last
 //              step's scores with this step's 32 LDS-fed MFMAs
+//   one_blk    one wave per SIMD (4-wave workgroups, the whole register
+//              file): 32 MFMAs per step on 16 LDS fragments, each used for
+//              two MFMAs, with last step's conversion interleaved
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -48,7 +51,7 @@ namespace {
 constexpr int kLds = 64 * 1024;
 constexpr int kLead = 6;   // fragments in flight ahead of their MFMA
 
-enum Mode { REG, LDS1, LDS2, LDSONLY, PP_REG, PP_LDS, PP_NOEXP, PP_SINK, PP_PRE, INTER };
+enum Mode { REG, LDS1, LDS2, LDSONLY, PP_REG, PP_LDS, PP_NOEXP, PP_SINK, PP_PRE, INTER, ONE_BLK };
 
 __device__ __forceinline__ uint32_t mix(uint32_t x) {
   x ^= x >> 16;
@@ -266,23 +269,96 @@ void probe(int steps, float *out) {
   out[blockIdx.x * 512 + tid] = s;
 }
 
+// One wave per SIMD: each LDS fragment feeds two MFMAs (two stationary
+// operand sets), and the conversion of last step's 32 scores per lane is
+// interleaved with this step's 32 MFMAs.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void probe_one(int steps, float *out) {
+  __shared__ __attribute__((aligned(1024))) char smem[kLds];
+  const int tid = threadIdx.x, lane = tid & 63;
+  for (int i = tid; i < kLds / 4; i += 256) reinterpret_cast<uint32_t *>(smem)[i] = two_bf16(mix(i + blockIdx.x * 77777u));
+  __syncthreads();
+  bf16x8 k0[8], k1[8], pk[4];
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    k0[s] = rand_frag(tid * 32 + s + blockIdx.x * 8192);
+    k1[s] = rand_frag(tid * 32 + s + 8 + blockIdx.x * 8192);
+  }
+#pragma unroll
+  for (int s = 0; s < 4; ++s) pk[s] = rand_frag(tid * 32 + s + 16 + blockIdx.x * 8192);
+  f32x16 acc[4], sq[2];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = zero16();
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) sq[j][e] = 0.01f * e;
+  const char *base = smem + lane * 16;
+  const float c = 0.0883883f, sub = 3.0f;
+  for (int it = 0; it < steps; ++it) {
+    bf16x8 ring[kLead + 1];
+#pragma unroll
+    for (int k = 0; k < kLead; ++k) ring[k] = lds_frag(base + k * 1024);
+    f32x16 sn[2] = {zero16(), zero16()};
+    bf16x8 pn[4];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      if (k + kLead < 16) ring[(k + kLead) % (kLead + 1)] = lds_frag(base + (k + kLead) * 1024);
+      const bf16x8 f = ring[k % (kLead + 1)];
+      if (k < 8) {   // scores of two key halves from one fragment
+        sn[0] = mfma(f, k0[k & 7], sn[0]);
+        sn[1] = mfma(f, k1[k & 7], sn[1]);
+      } else {       // products of two channel halves from one fragment
+        acc[(k - 8) >> 2] = mfma(f, pk[k & 3], acc[(k - 8) >> 2]);
+        acc[2 + ((k - 8) >> 2)] = mfma(f, pk[(k + 1) & 3], acc[2 + ((k - 8) >> 2)]);
+      }
+      // two scores of last step per fragment
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int q = 2 * k + t, j = q >> 4, e = q & 15;
+        sq[j][e] = __builtin_amdgcn_exp2f(fmaf(sq[j][e], c, -sub));
+      }
+      if ((k & 3) == 3) {
+        const int q = 2 * k + 1, j = q >> 4, h = (q >> 3) & 1;
+        bf16x8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = (__bf16)sq[j][8 * h + e];
+        pn[2 * j + h] = o;
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) pk[s] = pn[s];
+    sq[0] = sn[0];
+    sq[1] = sn[1];
+    asm volatile("" ::: "memory");
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s += acc[j][e];
+  out[blockIdx.x * 512 + tid] = s;
+}
+
 // Runs variant M over `steps` steps; MFMAs (or 1 KiB LDS reads) per wave and step.
 template <int M>
 int run(const char *name, int steps, int mfma_per_wave_step, int lds_kib_per_wave_step, int cus, float *out) {
   hipEvent_t e0, e1;
   CHECK(hipEventCreate(&e0));
   CHECK(hipEventCreate(&e1));
-  probe<M><<<cus, 512>>>(steps / 10, out);   // warm-up
+  if constexpr (M == ONE_BLK) probe_one<<<cus, 256>>>(steps / 10, out);   // warm-up
+  else probe<M><<<cus, 512>>>(steps / 10, out);
   CHECK(hipGetLastError());
   CHECK(hipDeviceSynchronize());
   CHECK(hipEventRecord(e0));
-  probe<M><<<cus, 512>>>(steps, out);
+  if constexpr (M == ONE_BLK) probe_one<<<cus, 256>>>(steps, out);
+  else probe<M><<<cus, 512>>>(steps, out);
   CHECK(hipGetLastError());
   CHECK(hipEventRecord(e1));
   CHECK(hipEventSynchronize(e1));
   float ms = 0.f;
   CHECK(hipEventElapsedTime(&ms, e0, e1));
-  const double waves = cus * 8.0;
+  const double waves = cus * (M == ONE_BLK ? 4.0 : 8.0);
   const double tflops = waves * steps * mfma_per_wave_step * 32768.0 / (ms * 1e-3) / 1e12;
   const double lds_tbs = waves * steps * lds_kib_per_wave_step * 1024.0 / (ms * 1e-3) / 1e12;
   printf("%-10s %9.3f ms  %8.1f TFLOP/s  LDS reads %6.1f TB/s (%.0f B per CU per ns)\n", name, ms, tflops, lds_tbs,
@@ -313,6 +389,7 @@ int main() {
   rc |= run<PP_SINK>("pp_sink", n / 2, 32, 32, cus, out);
   rc |= run<PP_PRE>("pp_pre", n / 2, 32, 32, cus, out);
   rc |= run<INTER>("inter", n, 32, 32, cus, out);
+  rc |= run<ONE_BLK>("one_blk", n, 32, 16, cus, out);
   rc |= run<REG>("reg", n, 32, 0, cus, out);
   CHECK(hipFree(out));
   return rc;
