@@ -1078,7 +1078,7 @@ cas_status_t prefix_attn_fwd_run(const cas_problem_t *p, const void *q, const vo
     // No pinned staging ring: the tables travel as kernel arguments.
     std::vector<char> h(pl.table_bytes, 0);
     fill_tables(pl, false, h.data());
-    hipError_t e = launch_table_upload(h.data(), pl.table_bytes, workspace, stream);
+    hipError_t e = launch_table_args_upload(h.data(), pl.table_bytes, workspace, stream);
     if (e != hipSuccess) return hip_fail("table upload launch", e);
   } else {
     s = upload_tables(pl, false, workspace, stream);

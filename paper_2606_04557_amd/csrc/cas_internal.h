@@ -285,11 +285,13 @@ cas_status_t prefix_attn_fwd_run(const cas_problem_t *p, const void *q, const vo
 // stream s as the kernel arguments of a copy kernel, kTableArgChunk bytes per
 // launch: no host or device allocation.
 constexpr int kTableArgChunk = 2048;
-hipError_t launch_table_upload(const void *host, size_t bytes, void *dst, hipStream_t s);
+hipError_t launch_table_args_upload(const void *host, size_t bytes, void *dst, hipStream_t s);
 
 // Kernel launchers (defined in the .hip files).
 hipError_t launch_fwd(const FwdParams &p, DType dt, int D, hipStream_t s);
 hipError_t launch_fwd_merge(const MergeParams &p, DType dt, int D, hipStream_t s);
+// Copies `bytes` of pinned host memory to device memory (both 16-byte
+// aligned) with a kernel on stream s.
 hipError_t launch_table_upload(void *dst, const void *src, size_t bytes, hipStream_t s);
 hipError_t launch_bwd_pre(const PreParams &p, DType dt, int D, hipStream_t s);
 hipError_t launch_dq(const DqParams &p, DType dt, int D, hipStream_t s);

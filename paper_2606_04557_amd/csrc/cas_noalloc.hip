@@ -46,7 +46,7 @@ struct TableChunk {
   uint32_t pieces;
 };
 
-__global__ __launch_bounds__(cas::kTableArgChunk / 16) void table_upload_kernel(TableChunk c) {
+__global__ __launch_bounds__(cas::kTableArgChunk / 16) void table_args_kernel(TableChunk c) {
   const uint32_t i = threadIdx.x;
   if (i < c.pieces) c.dst[i] = c.data[i];
 }
@@ -55,7 +55,7 @@ __global__ __launch_bounds__(cas::kTableArgChunk / 16) void table_upload_kernel(
 
 namespace cas {
 
-hipError_t launch_table_upload(const void *host, size_t bytes, void *dst, hipStream_t s) {
+hipError_t launch_table_args_upload(const void *host, size_t bytes, void *dst, hipStream_t s) {
   const char *src = (const char *)host;
   for (size_t off = 0; off < bytes; off += kTableArgChunk) {
     const size_t n = bytes - off < (size_t)kTableArgChunk ? bytes - off : (size_t)kTableArgChunk;
@@ -63,7 +63,7 @@ hipError_t launch_table_upload(const void *host, size_t bytes, void *dst, hipStr
     __builtin_memcpy(c.data, src + off, n);
     c.dst = (uint4 *)((char *)dst + off);
     c.pieces = (uint32_t)(n / 16);
-    hipLaunchKernelGGL(table_upload_kernel, dim3(1), dim3(kTableArgChunk / 16), 0, s, c);
+    hipLaunchKernelGGL(table_args_kernel, dim3(1), dim3(kTableArgChunk / 16), 0, s, c);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
