@@ -125,6 +125,17 @@ def test_small_forced_splits(spec):
         cas.set_tuning(0, 0)
 
 
+def test_large_launch_tables():
+    """512 rows that each list the same 16 cartridges, in a rotated order:
+    8,192 segment entries and 8,704 key tiles, about 600 KB of launch tables,
+    which the table upload copies in several grid-stride passes. Every
+    cartridge's gradient sums over all 512 rows. Every output element."""
+    rows = [[(i + b) % 16 for i in range(16)] for b in range(512)]
+    wl = casgen.custom("bigtables", "bf16", batch=512, q_len=16, num_q_heads=4, num_kv_heads=1,
+                       head_dim=128, cart_lens=[64] * 16, rows=rows, seed=321, cart_std=0.5)
+    _check_full(GpuCase(wl), "bigtables")
+
+
 def _sampled_check(case, n_rows=24, key_targets=None, seed=0, forward_only=False, results=None):
     """Oracle evaluated on sampled query rows (O, LSE, dQ) and sampled keys (dK, dV)."""
     wl = case.wl
