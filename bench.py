@@ -35,12 +35,11 @@ METRIC = "prefix-attn fwd+bwd TFLOP/s & MFMA util, 8B GQA shape, 16×2K cartridg
 
 # Algorithmic FLOPs per visible (query, key) pair per query head, in units of
 # head_dim, that each kernel owns: forward QK^T and PV; dK/dV pass dV, dP and
-# dK; dQ pass dQ (together 12d per pair). The fused backward owns dV, dP, dK
-# and dQ.
-KERNEL_FLOPS_PER_PAIR = {"fwd": 4, "dkdv": 6, "dq": 2, "dkdvq": 8}
+# dK; dQ pass dQ (together 12d per pair).
+KERNEL_FLOPS_PER_PAIR = {"fwd": 4, "dkdv": 6, "dq": 2}
 # What each kernel executes, recomputation included (S in every backward
 # kernel, dP again in the dQ pass).
-KERNEL_EXEC_FLOPS_PER_PAIR = {"fwd": 4, "dkdv": 8, "dq": 6, "dkdvq": 10}
+KERNEL_EXEC_FLOPS_PER_PAIR = {"fwd": 4, "dkdv": 8, "dq": 6}
 
 
 def kernel_hbm_bytes(wl, kernel: str):
@@ -60,8 +59,6 @@ def kernel_hbm_bytes(wl, kernel: str):
         return 2 * qb + 2 * (kvc + kvs) + 2 * stat + 2 * (kvc + kvs)
     if kernel == "dq":        # Q, dO, K, V, LSE, D in; dQ out
         return 2 * qb + 2 * (kvc + kvs) + 2 * stat + qb
-    if kernel == "dkdvq":     # the dK/dV pass plus dQ out
-        return 2 * qb + 2 * (kvc + kvs) + 2 * stat + 2 * (kvc + kvs) + qb
     return None
 
 
