@@ -1,6 +1,7 @@
-"""GPU parity on seeded random problems: batch, query length, KV heads, GQA
-group, head_dim, cartridge lengths, storage layouts, aliasing and dtype are
-drawn per case, and every output element is compared with the fp64 oracle
+"""GPU parity on seeded random problems: batch, query length (or, in the
+packed layout, the samples' lengths), KV heads, GQA group, head_dim,
+cartridge lengths, storage layouts, aliasing and dtype are drawn per case,
+and every output element is compared with the fp64 oracle
 (bars as in test_gpu_parity: 2e-2 relative for bf16, 1e-5 for fp32; LSE
 absolute 1e-3 / 1e-5). The draws are fixed by the case number, so a failing
 case is reproducible by its id.
@@ -58,3 +59,33 @@ def test_random_problem(i):
     for k, v in errs.items():
         lim = LSE_TOL[wl.dtype] if k == "lse" else TOL[wl.dtype]
         assert v <= lim, (name, k, v)
+
+
+def draw_packed(i):
+    """Packed samples (one token axis; samples of 0..300 tokens, some empty),
+    each over a random subset of a shared cartridge pool."""
+    r = np.random.RandomState(2000 + i)
+    dtype = "fp32" if i % 4 == 3 else "bf16"
+    D = int(r.choice([64, 128]))
+    Hkv = int(r.randint(1, 3))
+    g = int(r.choice([1, 2, 4, 5, 8]))
+    n_s = int(r.randint(1, 7))
+    q_lens = [int(r.choice([0, 1, 15, 64, 65, 130, 300])) for _ in range(n_s)]
+    if sum(q_lens) == 0:
+        q_lens[0] = 33
+    n_carts = int(r.randint(1, 6))
+    cart_lens = [int(r.choice([1, 31, 64, 100, 129, 257])) for _ in range(n_carts)]
+    layouts = [str(r.choice(["tok", "padded", "head"])) for _ in range(n_carts)]
+    rows = [[int(c) for c in r.randint(0, n_carts, size=int(r.randint(0, 4)))] for _ in range(n_s)]
+    return dict(name=f"prand{i}", dtype=dtype, batch=n_s, q_len=0, q_lens=q_lens, num_q_heads=Hkv * g,
+                num_kv_heads=Hkv, head_dim=D, cart_lens=cart_lens, rows=rows, layouts=layouts)
+
+
+@pytest.mark.parametrize("i", range(8), ids=[f"packed{i}" for i in range(8)])
+def test_random_packed_problem(i):
+    from test_gpu_parity import _check_full
+    spec = draw_packed(i)
+    name = spec.pop("name")
+    wl = casgen.custom(name, seed=6000 + i, cart_std=0.5, **spec)
+    print(name, "q_lens", wl.q_lens, "g", wl.group_size, "d", wl.head_dim, "carts", wl.cart_lens, "rows", wl.rows)
+    _check_full(GpuCase(wl), name)
