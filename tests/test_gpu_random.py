@@ -1,6 +1,8 @@
 """GPU parity on seeded random problems: batch, query length (or, in the
 packed layout, the samples' lengths), KV heads, GQA group, head_dim,
-cartridge lengths, storage layouts, aliasing and dtype are drawn per case,
+cartridge lengths, storage layouts, aliasing and dtype are drawn per case
+(for the paged decode path: page size, heads, group, head_dim, the
+cartridge pool and each request's cartridges, own tokens and queries),
 and every output element is compared with the fp64 oracle
 (bars as in test_gpu_parity: 2e-2 relative for bf16, 1e-5 for fp32; LSE
 absolute 1e-3 / 1e-5). The draws are fixed by the case number, so a failing
@@ -89,3 +91,33 @@ def test_random_packed_problem(i):
     wl = casgen.custom(name, seed=6000 + i, cart_std=0.5, **spec)
     print(name, "q_lens", wl.q_lens, "g", wl.group_size, "d", wl.head_dim, "carts", wl.cart_lens, "rows", wl.rows)
     _check_full(GpuCase(wl), name)
+
+
+def draw_decode(i):
+    """Paged decode: page size, heads, group, head_dim, a cartridge pool, and
+    requests over random (possibly repeated) cartridges with their own
+    tokens and 1..12 queries."""
+    r = np.random.RandomState(3000 + i)
+    P = int(r.choice([16, 32, 64, 128]))
+    Hkv = int(r.choice([1, 2, 4]))
+    g = int(r.choice([1, 2, 4, 8]))
+    D = int(r.choice([64, 128]))
+    n_carts = int(r.randint(1, 6))
+    cart_pages = int(r.randint(1, 7))
+    reqs = []
+    for _ in range(int(r.randint(1, 7))):
+        carts = [int(c) for c in r.randint(0, n_carts, size=int(r.randint(0, 5)))]
+        own = int(r.randint(1, 101))
+        kv = len(carts) * cart_pages * P + own
+        reqs.append((carts, own, int(r.randint(1, min(kv, 12) + 1))))
+    return dict(P=P, Hkv=Hkv, g=g, D=D, n_carts=n_carts, cart_pages=cart_pages, reqs=reqs)
+
+
+@pytest.mark.parametrize("i", range(8), ids=[f"decode{i}" for i in range(8)])
+def test_random_decode_problem(i):
+    from test_gpu_decode import _pool, _run
+    c = draw_decode(i)
+    print(f"decode{i}", c)
+    kp, vp, kl, qc, pages = _pool(7000 + i, c["n_carts"], c["cart_pages"], c["P"], c["Hkv"], c["D"], c["reqs"],
+                                  own_extra=int(i % 3))
+    _run(kp, vp, kl, qc, pages, c["Hkv"], c["g"], c["D"], 7100 + i)
