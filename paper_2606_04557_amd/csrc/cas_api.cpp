@@ -926,13 +926,15 @@ cas_status_t build_decode(const cas_decode_problem_t *p, DecodePlan &dp) {
   dp.Tq = (int)Tq;
   dp.Hq = (int)Hq;
   const int g = p->group_size, Hkv = p->num_kv_heads;
-  // Split planning: about 1024 workgroups of at least 8 tiles (two per wave).
+  // Split planning: workgroups of at least 8 tiles (two per wave), about as
+  // many as the compute units hold at once (two each), so the whole step
+  // runs in one round of workgroups when the requests allow it.
   int64_t total = 0;
   for (int b = 0; b < B; ++b) {
     const int64_t n = p->q_offsets[b + 1] - p->q_offsets[b];
     total += ceil_div(p->kv_lens[b], kDecTile) * Hkv * ceil_div(n * g, kDecRows);
   }
-  const int64_t per_wg = std::max<int64_t>(8, ceil_div(total, 1024));
+  const int64_t per_wg = std::max<int64_t>(8, ceil_div(total, 2 * (int64_t)device_topology().cus));
   dp.reqs.resize(B);
   dp.tok_req.resize(Tq);
   struct W {
