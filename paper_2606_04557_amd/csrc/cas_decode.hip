@@ -77,9 +77,9 @@ void decode_bf16_kernel(DecodeParams p) {
 #pragma unroll
     for (int st = 0; st < NSTEP; ++st) qf[st] = Mma<__bf16>::zero();
   }
-  // Tile loads are waited for with partial vmcnt counts, which must not
-  // include these loads.
-  wait_vmcnt<0>();
+  // No wait here: these loads are older than every tile load, so the first
+  // tile's partial wait covers them, and their latency overlaps the first
+  // tile's.
 
   TrOffsets<D> to;
   to.init(lane);

@@ -17,6 +17,10 @@
 //   pages U S     the decode's bytes: one 256-thread workgroup per
 //                 (request, KV head, key range), S ranges per (request, KV
 //                 head), U 32-key tiles of K and V in flight per lane
+//   dma S         the same bytes by direct buffer->LDS copies, each of the
+//                 four waves on every fourth tile (the decode kernel's
+//                 assignment), one 16 KiB tile (K and V) in flight per wave,
+//                 two workgroups per compute unit
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -110,6 +114,49 @@ __global__ __launch_bounds__(256) void pages_kernel(const uint16_t *kp, const ui
   keep(acc, sink);
 }
 
+typedef __amdgpu_buffer_rsrc_t BufRsrc;
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// Wave w of a workgroup copies tiles t0 + w, t0 + w + 4, ... of its
+// (request, KV head): instruction i moves key rows 4 i .. 4 i + 3 (16 lanes
+// per 256-byte row) of K, then of V, into the wave's 16 KiB LDS area; the
+// wave waits for the tile and folds 16 bytes of it.
+__global__ __launch_bounds__(256) void dma_kernel(const uint16_t *kp, const uint16_t *vp, const int *table,
+                                                  int splits, u32x4 *sink) {
+  __shared__ __attribute__((aligned(1024))) char lds[4 * 16384];
+  const int w = blockIdx.x;
+  const int split = w % splits, pair = w / splits;
+  const int h = pair % kHkv, r = pair / kHkv;
+  const int t0 = (int)((int64_t)kTiles * split / splits), t1 = (int)((int64_t)kTiles * (split + 1) / splits);
+  const int *pt = table + r * kReqPages;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  char *const mine = lds + wave * 16384;
+  const int64_t row_el = (int64_t)kHkv * kD;
+  u32x4 acc = {0, 0, 0, 0};
+  for (int t = t0 + wave; t < t1; t += 4) {
+    const int pa = pt[2 * t];
+    const int pb = t * kTile + 16 < kKvLen ? pt[2 * t + 1] : pa;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int k0 = t * kTile + 4 * i;                  // first key of the instruction
+      const int half = (4 * i) / 16;
+      const int page = half ? pb : pa;
+      const int valid = k0 < kKvLen ? kKvLen - (k0 - (4 * i) % 16) : 0;   // tokens of this page in range
+      const int nv = valid > kPage ? kPage : valid;
+      const int bytes = nv > 0 ? (int)(((int64_t)(nv - 1) * row_el + kD) * 2) : 0;
+      const int64_t pbase = ((int64_t)page * kPage * kHkv + h) * kD;
+      const int voff = (int)((((4 * i) % 16 + lane / 16) * row_el + (lane % 16) * 8) * 2);
+      const BufRsrc rk = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(kp + pbase), (short)0, bytes, 0x00020000);
+      const BufRsrc rv = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(vp + pbase), (short)0, bytes, 0x00020000);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void_t *)(mine + i * 1024), 16, voff, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void_t *)(mine + 8192 + i * 1024), 16, voff, 0, 0, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (15 << 8));   // vmcnt(0)
+    acc ^= *reinterpret_cast<volatile u32x4 *>(mine + lane * 16);
+  }
+  keep(acc, sink);
+}
+
 template <typename L>
 float time_ms(L &&launch, int reps) {
   hipEvent_t a, b;
@@ -193,6 +240,12 @@ int main() {
     run_pages(std::integral_constant<int, 1>{}, splits);
     run_pages(std::integral_constant<int, 2>{}, splits);
     run_pages(std::integral_constant<int, 4>{}, splits);
+  }
+  for (int splits : {1, 2, 4}) {
+    const int grid = kReqs * kHkv * splits;
+    const float ms = time_ms([&] { hipLaunchKernelGGL(dma_kernel, dim3(grid), dim3(256), 0, 0, kp, vp, dt, splits,
+                                                      sink); }, 20);
+    printf("dma     grid %5d    : %.4f ms  %.0f GB/s of decode bytes\n", grid, ms, dec_bytes / ms / 1e6);
   }
   CHECK(hipGetLastError());
   CHECK(hipDeviceSynchronize());
