@@ -41,7 +41,7 @@ void decode_bf16_kernel(DecodeParams p) {
   constexpr int NI = kDecTile / RPI;          // copy instructions per V tile
   constexpr int OS = DT * 16 * 64;            // floats of one wave's O^T in the closing combine
   static_assert(kDecTile % RPI == 0 && 16 % RPI == 0, "copy instructions stay within a page");
-  static_assert(2 * OS * 4 == kDecWaves / 2 * TB * 2, "two waves' O^T fill one stage object");
+  static_assert(2 * OS * 4 == kDecWaves * TB, "two waves' O^T fill one stage object");
   static_assert(2 * (2 * kDecWaves * TB + kDecWaves * 128 * 4) <= 160 * 1024, "two workgroups per compute unit");
   // V stages 0 and 1 of every wave; the closing combine puts the O^T of
   // waves 0-1 into the first and of waves 2-3 into the second, m and l into ml.
