@@ -133,9 +133,12 @@ typedef struct {
 /*
  * Bytes of device workspace a forward (backward == 0) or backward
  * (backward != 0) call on this problem needs, written to *bytes. The size
- * depends only on the problem and the current tuning (cas_set_tuning), not on
- * the device. Workspace is caller-owned, 256-byte aligned, and may be reused
- * by the next call once the stream has passed the previous one. Besides the
+ * depends on the problem, the current tuning (cas_set_tuning) and, through
+ * the automatic key-axis splits, the compute-unit count of the current
+ * device (the same on every whole MI355X): query it with the device current
+ * that will run the call. Workspace is caller-owned, 256-byte aligned, and
+ * may be reused by the next call once the stream has passed the previous
+ * one. Besides the
  * segment tables and per-row statistics, a bf16 backward keeps a transposed
  * copy of q and d_o in it (about twice the bytes of q).
  */
@@ -325,6 +328,9 @@ typedef struct {
   const int32_t *page_ids;     /* host, page_offsets[batch] entries */
 } cas_decode_problem_t;
 
+/* Workspace bytes of a cas_paged_decode_fwd call (launch tables and the
+ * split partials), written to *bytes; like the prefix-attention query it
+ * depends on the compute-unit count of the current device. */
 cas_status_t cas_paged_decode_workspace_size(const cas_decode_problem_t *p, size_t *bytes);
 
 cas_status_t cas_paged_decode_fwd(const cas_decode_problem_t *p, const void *q, const void *k_pages,
