@@ -32,16 +32,20 @@ def host(x) -> np.ndarray:
     return x.detach().float().cpu().numpy().astype(np.float64)
 
 
+WIDE_STRIDE = 1 << 21   # elements between tokens of the "wide" layout (4 MiB in bf16)
+
+
 def alloc_like_layout(L: int, Hkv: int, D: int, layout: str, dtype, fill=float("nan")):
     """A [L, Hkv, D] view with the requested storage: token-major, padded
-    token stride, or head-major."""
+    token stride, head-major, or "wide" (a token stride of 2^21 elements, so
+    a segment of a thousand tokens spans several GiB)."""
     t = torch()
     if layout == "tok":
         x = t.full((L, Hkv, D), fill, dtype=dtype, device="cuda")
         return x, x
-    if layout == "padded":
-        pad = 64
-        base = t.full((L, Hkv * D + pad), fill, dtype=dtype, device="cuda")
+    if layout in ("padded", "wide"):
+        row = Hkv * D + 64 if layout == "padded" else WIDE_STRIDE
+        base = t.full((L, row), fill, dtype=dtype, device="cuda")
         return base[:, : Hkv * D].view(L, Hkv, D), base
     if layout == "head":
         base = t.full((Hkv, L, D), fill, dtype=dtype, device="cuda")

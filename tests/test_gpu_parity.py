@@ -125,6 +125,31 @@ def test_small_forced_splits(spec):
         cas.set_tuning(0, 0)
 
 
+def test_wide_token_stride():
+    """A 1,024-token cartridge stored with a token stride of 2^21 elements
+    (4 MiB), so that its keys and gradients span 4 GiB: byte offsets within a
+    segment pass 2^31 and 2^32 (the largest stride the library accepts is
+    2^22 elements). It is used by both rows, once beside a compact one; every
+    element is compared, with the automatic plan and with forced key-axis
+    splits, and the 4 MiB gaps between gradient rows stay unwritten."""
+    import paper_2606_04557_amd as cas
+    import torch
+    spec = dict(dtype="bf16", batch=2, q_len=40, num_q_heads=4, num_kv_heads=1, head_dim=64,
+                cart_lens=[1024, 100], rows=[[0, 1], [1, 0]], layouts=["wide", "tok"])
+    wl = casgen.custom("wide", seed=321, cart_std=0.5, **spec)
+    case = GpuCase(wl)
+    print("wide: K span %.2f GiB" % ((wl.cart_lens[0] - 1) * case.k[0].stride(0) * 2 / 2 ** 30))
+    _check_full(case, "wide")
+    del case
+    torch.cuda.empty_cache()
+    try:
+        cas.set_tuning(fwd_splits=4, dq_splits=3)
+        _check_full(GpuCase(wl), "wide split")
+    finally:
+        cas.set_tuning(0, 0)
+    torch.cuda.empty_cache()
+
+
 def test_large_launch_tables():
     """512 rows that each list the same 16 cartridges, in a rotated order:
     8,192 segment entries and 8,704 key tiles, about 600 KB of launch tables,
