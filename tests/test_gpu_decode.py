@@ -106,3 +106,48 @@ def test_decode_rejects_bad_tables():
         cas.paged_decode_fwd(q, kp, kp.clone(), [1, 1], [20, 3], [[0], [1]], 2, 2, 0.125)
     with pytest.raises(cas.CasError):       # more queries than keys
         cas.paged_decode_fwd(q, kp, kp.clone(), [2, 0], [1, 3], [[0], [1]], 2, 2, 0.125)
+
+
+def test_decode_pool_beyond_4gib():
+    """Pages past the first 4 GiB of a 5 GB pool (page ids above 16,384 with
+    256 KiB pages: 128 tokens x 8 KV heads x 128): every page address is
+    computed in 64 bits. Only the listed pages hold data; the oracle reads a
+    compact copy of them under renumbered ids. Every output is compared."""
+    import torch
+    import paper_2606_04557_amd as cas
+    P, Hkv, g, D = 128, 8, 4, 128
+    n_pool = 20_000                               # 20,000 x 256 KiB = 5.2 GB per tensor
+    reqs = [(3, 300, 1), (2, 129, 3), (4, 1, 1)]   # (pages, tokens in the last page, queries)
+    ids, kv_lens, q_counts = [], [], []
+    nxt = 16_380
+    for npg, last, nq in reqs:
+        ids.append(list(range(nxt, nxt + npg)))
+        nxt += npg + 997                          # scattered, and all but the first few past 2^32 bytes
+        kv_lens.append((npg - 1) * P + min(last, P))
+        q_counts.append(nq)
+    used = sorted({i for r in ids for i in r})
+    assert max(used) < n_pool and max(used) * P * Hkv * D * 2 > 2 ** 32
+    shape = (len(used), P, Hkv, D)
+    bits = lambda tag: rng.f64_to_bf16_bits(rng.normal(rng.stream_key(991, tag), int(np.prod(shape)), 0.5))
+    kc = rng.bf16_bits_to_f32(bits(1)).reshape(shape)
+    vc = rng.bf16_bits_to_f32(bits(2)).reshape(shape)
+    kp = torch.empty((n_pool, P, Hkv, D), dtype=torch.bfloat16, device="cuda")
+    vp = torch.empty_like(kp)
+    idx = torch.tensor(used, device="cuda")
+    kp[idx] = torch.from_numpy(kc).to(torch.bfloat16).cuda()
+    vp[idx] = torch.from_numpy(vc).to(torch.bfloat16).cuda()
+    Tq, Hq = sum(q_counts), Hkv * g
+    q = rng.bf16_bits_to_f32(rng.f64_to_bf16_bits(rng.normal(rng.stream_key(992, 3), Tq * Hq * D, 1.0))).reshape(
+        Tq, Hq, D)
+    scale = float(np.float32(1.0 / np.sqrt(D)))
+    o, lse = cas.paged_decode_fwd(torch.from_numpy(q).to(torch.bfloat16).cuda(), kp, vp, q_counts, kv_lens, ids,
+                                  Hkv, g, scale)
+    torch.cuda.synchronize()
+    remap = {p: i for i, p in enumerate(used)}
+    O, LSE = oracle.paged_decode_forward(q, kc, vc, q_counts, kv_lens, [[remap[i] for i in r] for r in ids], scale, g)
+    e_o = rel_err(host(o), O)
+    e_l = float(np.abs(host(lse) - LSE).max())
+    print(f"pool past 4 GiB: O {e_o:.2e} LSE {e_l:.2e}")
+    assert e_o <= TOL["bf16"] and e_l <= LSE_TOL["bf16"], (e_o, e_l)
+    del kp, vp
+    torch.cuda.empty_cache()
