@@ -6,22 +6,20 @@
 //
 // A decode step has very few query rows per (request, KV head) (n * g, e.g.
 // 4) against thousands of keys, so the work is streaming K and V out of HBM.
-// One workgroup takes a block of up to 32 packed rows of one (request, KV
+// One workgroup takes a block of up to 16 packed rows of one (request, KV
 // head) and a range of 32-key tiles (the host splits a request's key axis
 // so that every compute unit holds two workgroups; partials are merged by
 // their LSE). Its four waves work independently on every fourth tile of the
 // range, so no wave ever waits on another until the end, where the four
-// partial softmax states are combined through LDS. K goes straight from
-// memory into the MFMA operand registers (each lane loads 16 bytes of one
-// key row per step); V goes through two LDS stages per wave, filled by
-// direct buffer->LDS copies, for the transposed reads of the PV product.
-// The two stages are separate LDS objects and the loop alternates them at
-// compile time, so the compiler can tell a stage's transposed reads from
-// the copies into the other one and does not wait for those copies.
-// Page addresses come from the page table (one scalar load per page, a tile
-// ahead). Per tile and wave: S^T = K Q^T (MFMA, K and Q in registers), an
-// online-softmax update, and O^T += V^T P^T (MFMA, V^T by transposed LDS
-// reads, P straight from the score registers).
+// partial softmax states are combined through LDS. The products use
+// v_mfma_f32_16x16x32_bf16, whose 16 columns fit the few rows of a decode
+// step. K and V go from memory straight into registers, one tile ahead of
+// their use: K already in the MFMA operand layout (each lane loads 16 bytes
+// of one key row per step), V in whole rows, written into the wave's LDS
+// tile just before its transposed reads for the PV product. Page addresses
+// come from the page table (scalar loads, a tile ahead of the loads that
+// use them). Per tile and wave: S^T = K Q^T, an online-softmax update, and
+// O^T += V^T P^T with P^T straight from the score registers.
 #include "cas_device.h"
 
 namespace cas {
@@ -30,34 +28,38 @@ namespace {
 
 constexpr int kDecWaves = 4;
 
+typedef __attribute__((address_space(3))) char lds_char_t;
+
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
 template <int D>
 __global__ __launch_bounds__(kDecWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void decode_bf16_kernel(DecodeParams p) {
-  constexpr int NSTEP = D / 16;
-  constexpr int DT = D / 32;
+  static_assert(kDecRows == 16, "one 16-column MFMA block of rows");
+  constexpr int NQ = D / 32;                  // 32-channel steps of the score product
+  constexpr int NDB = D / 16;                 // 16-channel blocks of the PV product
   constexpr int TB = kDecTile * D * 2;        // bytes of one 32-key V tile
   constexpr int CPR = D / 8;                  // 16-byte chunks per key row
-  constexpr int RPI = 64 / CPR;               // key rows per copy instruction
-  constexpr int NI = kDecTile / RPI;          // copy instructions per V tile
-  constexpr int OS = DT * 16 * 64;            // floats of one wave's O^T in the closing combine
-  static_assert(kDecTile % RPI == 0 && 16 % RPI == 0, "copy instructions stay within a page");
-  static_assert(2 * OS * 4 == kDecWaves * TB, "two waves' O^T fill one stage object");
-  static_assert(2 * (2 * kDecWaves * TB + kDecWaves * 128 * 4) <= 160 * 1024, "two workgroups per compute unit");
-  // V stages 0 and 1 of every wave; the closing combine puts the O^T of
-  // waves 0-1 into the first and of waves 2-3 into the second, m and l into ml.
-  __shared__ __attribute__((aligned(1024))) char vs0[kDecWaves * TB];
-  __shared__ __attribute__((aligned(1024))) char vs1[kDecWaves * TB];
+  constexpr int RPI = 64 / CPR;               // key rows per V load instruction
+  constexpr int NI = kDecTile / RPI;          // V load instructions per tile
+  constexpr int OS = NDB * 4 * 64;            // floats of one wave's O^T in the closing combine
+  static_assert(OS * 4 == TB, "a wave's O^T fills its V tile");
+  // Each wave's V tile (the closing combine reuses it for the wave's O^T);
+  // m and l of every wave.
+  __shared__ __attribute__((aligned(1024))) char vs[kDecWaves * TB];
   __shared__ __attribute__((aligned(16))) float ml[kDecWaves * 128];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int G = lane >> 5, n = lane & 31;
+  const int j = lane & 15, bq = lane >> 4;    // MFMA column (row of the block) and k-group
   const DevDecodeWork w = load_const(p.work, (int)blockIdx.x);
   const DevDecodeReq rq = load_const(p.reqs, w.b);
   const int g = p.g, Hkv = p.Hkv, Hq = Hkv * g, P = p.page_size;
   const int kvh = __builtin_amdgcn_readfirstlane(w.kvh);
   const int kv_len = __builtin_amdgcn_readfirstlane(rq.kv_len);
   const int nrows = rq.n * g;
-  const int my_row = w.row0 + n;
+  const int my_row = w.row0 + j;
   const bool row_ok = my_row < nrows;
   const int my_i = my_row / g;                            // query index within the request
   const int my_h = kvh * g + (my_row - my_i * g);
@@ -65,37 +67,20 @@ void decode_bf16_kernel(DecodeParams p) {
   // Q is zero and nothing of theirs is stored).
   const int my_lim = row_ok ? kv_len - rq.n + my_i : kv_len - 1;
   const float c = p.scale_log2;
-  char *const st0 = vs0 + wave * TB;
-  char *const st1 = vs1 + wave * TB;
+  char *const vt = vs + wave * TB;
 
-  bf16x8 qf[NSTEP];
-  if (row_ok) {
-    const __bf16 *qp = (const __bf16 *)p.q + ((int64_t)(rq.q0 + my_i) * Hq + my_h) * D;
+  // Q as the B operand: step st of lane (j, bq) is channels 32 st + 8 bq ..
+  // + 7 of row j.
+  bf16x8 qf[NQ];
+  {
+    const __bf16 *qp = (const __bf16 *)p.q + ((int64_t)(rq.q0 + (row_ok ? my_i : 0)) * Hq + my_h) * D + 8 * bq;
 #pragma unroll
-    for (int st = 0; st < NSTEP; ++st) qf[st] = *reinterpret_cast<const bf16x8 *>(qp + st * 16 + G * 8);
-  } else {
-#pragma unroll
-    for (int st = 0; st < NSTEP; ++st) qf[st] = Mma<__bf16>::zero();
+    for (int st = 0; st < NQ; ++st)
+      qf[st] = row_ok ? *reinterpret_cast<const bf16x8 *>(qp + 32 * st) : Mma<__bf16>::zero();
   }
-  // No wait here: these loads are older than every tile load, so the first
-  // tile's partial wait covers them, and their latency overlaps the first
-  // tile's.
-
-  TrOffsets<D> to;
-  to.init(lane);
-
-  // Copy lanes: instruction i of a V tile moves key rows RPI*i .. RPI*i+RPI-1;
-  // this lane moves 16 bytes of row RPI*i + lrow into tile position (row,
-  // lane % CPR), i.e. global chunk (lane % CPR) ^ swz(row).
-  const int lrow = lane / CPR;
-  int coff[NI];
-#pragma unroll
-  for (int i = 0; i < NI; ++i) coff[i] = ((lane % CPR) ^ swz<D>(RPI * i + lrow)) * 8;
-  const int64_t row_el = (int64_t)Hkv * D;            // elements between consecutive tokens of a page
 
   // The pages of a tile's keys 0..15 (a) and 16..31 (b): one page when pages
-  // hold 32 or more tokens, since tiles start at multiples of 32. Read one
-  // tile ahead of their loads, so the scalar-load latency never delays one.
+  // hold 32 or more tokens, since tiles start at multiples of 32.
   struct TilePages {
     int a, b;
   };
@@ -108,132 +93,159 @@ void decode_bf16_kernel(DecodeParams p) {
     }
     return tp;
   };
-  // K of a tile into the MFMA A-operand registers: step st of lane (n, G)
-  // is channels 16 st + 8 G .. + 7 of the tile's key n. Keys past kv_len
-  // load the tile's first key instead; their scores are masked.
-  auto load_k = [&](int tile, const TilePages &tp, bf16x8 (&kr)[NSTEP]) __attribute__((always_inline)) {
-    const int k0 = tile * kDecTile;
-    const int kk = k0 + n < kv_len ? n : 0;
-    const int page = kk < 16 ? tp.a : tp.b;
-    const int tok = (k0 + kk) & (P - 1);
-    const __bf16 *src = (const __bf16 *)p.k_pages + (((int64_t)page * P + tok) * Hkv + kvh) * D + 8 * G;
-#pragma unroll
-    for (int st = 0; st < NSTEP; ++st) kr[st] = *reinterpret_cast<const bf16x8 *>(src + 16 * st);
+  // Element offset of key k0 + r (r < 32) of a tile in the pool; keys past
+  // kv_len stand in for the tile's first key.
+  auto key_off = [&](int k0, int r, const TilePages &tp) __attribute__((always_inline)) {
+    const int rr = k0 + r < kv_len ? r : 0;
+    const int page = rr < 16 ? tp.a : tp.b;
+    return (((int64_t)page * P + ((k0 + rr) & (P - 1))) * Hkv + kvh) * D;
   };
-  // V of a tile into the wave's stage vd; rows past kv_len, and every row
-  // when the tile is not live, read as zero.
-  auto issue_v = [&](int tile, const TilePages &tp, char *vd, bool live) __attribute__((always_inline)) {
+  // K of a tile as the A operand: fragment kb * NQ + st of lane (j, bq) is
+  // channels 32 st + 8 bq .. + 7 of key 16 kb + j.
+  auto load_k = [&](int tile, const TilePages &tp, bf16x8 (&kr)[2 * NQ]) __attribute__((always_inline)) {
+    const int k0 = tile * kDecTile;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const __bf16 *src = (const __bf16 *)p.k_pages + key_off(k0, 16 * kb + j, tp) + 8 * bq;
+#pragma unroll
+      for (int st = 0; st < NQ; ++st) kr[kb * NQ + st] = *reinterpret_cast<const bf16x8 *>(src + 32 * st);
+    }
+  };
+  // V of a tile in whole rows: load i of a lane is chunk lane % CPR of key
+  // row RPI * i + lane / CPR.
+  auto load_v = [&](int tile, const TilePages &tp, bf16x8 (&vr)[NI]) __attribute__((always_inline)) {
+    const int k0 = tile * kDecTile;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
-      const int k0 = tile * kDecTile + RPI * i;       // first key of the instruction (uniform)
-      BufRsrc rv = make_rsrc(p.v_pages, 0);
-      int voff = 0;
-      if (live && k0 < kv_len) {
-        const int pidx = k0 / P;
-        const int page = RPI * i < 16 ? tp.a : tp.b;
-        const int valid = min(P, kv_len - pidx * P);  // tokens held by this page
-        const int64_t pbase = ((int64_t)page * P * Hkv + kvh) * D;
-        const int bytes = (int)(((int64_t)(valid - 1) * row_el + D) * 2);
-        rv = make_rsrc((const __bf16 *)p.v_pages + pbase, bytes);
-        voff = (int)(((int64_t)(k0 - pidx * P + lrow) * row_el + coff[i]) * 2);
-      }
-      dma16(rv, voff, vd + i * 1024);
+      const __bf16 *src = (const __bf16 *)p.v_pages + key_off(k0, RPI * i + lane / CPR, tp) + (lane % CPR) * 8;
+      vr[i] = *reinterpret_cast<const bf16x8 *>(src);
     }
+  };
+  // V rows into the wave's LDS tile (16-byte chunks XOR-swizzled by row);
+  // rows past kv_len are written as zeros.
+  auto write_v = [&](int tile, const bf16x8 (&vr)[NI]) __attribute__((always_inline)) {
+    const int k0 = tile * kDecTile;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int r = RPI * i + lane / CPR;
+      const bf16x8 v = k0 + r < kv_len ? vr[i] : Mma<__bf16>::zero();
+      *reinterpret_cast<bf16x8 *>(vt + r * (D * 2) + (((lane % CPR) ^ swz<D>(r)) << 4)) = v;
+    }
+  };
+  // V^T as the A operand of the PV product for channel block db: lane (j, bq)
+  // holds channel 16 db + j of keys 4 bq .. 4 bq + 3 and 16 + 4 bq .. + 3, the
+  // keys its P^T registers hold. Each transposed read of a 16-lane group
+  // covers 4 key rows x 16 channels; lane j addresses row j / 4, channels
+  // 4 (j % 4) .. + 3 of it and receives channel j of all four rows.
+  auto vt_frag = [&](int db) __attribute__((always_inline)) {
+    const lds_char_t *base = (const lds_char_t *)vt;
+    i16x4 part[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int row = 16 * h + 4 * bq + (j >> 2);
+      const int col = 16 * db + 4 * (j & 3);
+      const int off = row * (D * 2) + (((col >> 3) ^ swz<D>(row)) << 4) + ((col >> 2) & 1) * 8;
+      part[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t *)(base + off));
+    }
+    typedef short i16x8 __attribute__((ext_vector_type(8)));
+    return __builtin_bit_cast(bf16x8, (i16x8)__builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7));
   };
 
   float m_run = -INFINITY, l_run = 0.0f;
-  f32x16 oacc[DT];
+  f32x4 oacc[NDB];
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt) oacc[dt] = zero16();
+  for (int db = 0; db < NDB; ++db) oacc[db] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
-  // S^T of a tile from K in registers; K of the wave's next tile (pages
-  // nk) is then loaded into the same registers, so its latency hides behind
-  // this tile's softmax and PV product.
-  bf16x8 kr[NSTEP];
-  auto compute = [&](int tile, const char *vb, int tnext, const TilePages &nk) __attribute__((always_inline)) {
+  auto compute = [&](int tile, const bf16x8 (&kr)[2 * NQ]) __attribute__((always_inline)) {
     const int key0 = tile * kDecTile;
-    f32x16 s = zero16();
+    // S^T: register e of score block kb of lane (j, bq) is key 16 kb + 4 bq + e, row j.
+    f32x4 s[2];
 #pragma unroll
-    for (int st = 0; st < NSTEP; ++st) s = Mma<__bf16>::run(kr[st], qf[st], s);
-    if (tnext < w.tile1) load_k(tnext, nk, kr);
-    // Register j of lane group G holds key key0 + crow(j, G).
+    for (int kb = 0; kb < 2; ++kb) {
+      s[kb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int st = 0; st < NQ; ++st) s[kb] = mfma16(kr[kb * NQ + st], qf[st], s[kb]);
+    }
     if (key0 + kDecTile - 1 > kv_len - rq.n) {
-      const int lim = my_lim - key0 - 4 * G;
+      const int lim = my_lim - key0 - 4 * bq;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) s[j] = crow(j, 0) <= lim ? s[j] : -INFINITY;
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s[kb][e] = 16 * kb + e <= lim ? s[kb][e] : -INFINITY;
     }
     float mx = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[j]);
-    mx = fmaxf(mx, xor32(mx)) * c;
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) mx = fmaxf(mx, s[kb][e]);
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c;
     const float m_new = fmaxf(m_run, mx);
     const float mu = m_new == -INFINITY ? 0.0f : m_new;
     const float alpha = fast_exp2(m_run - mu);
     float ls = 0.0f;
+    bf16x8 pf;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      s[j] = fast_exp2(fmaf(s[j], c, -mu));
-      ls += s[j];
-    }
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float pv = fast_exp2(fmaf(s[kb][e], c, -mu));
+        ls += pv;
+        pf[4 * kb + e] = (__bf16)pv;
+      }
     l_run = l_run * alpha + ls;
     m_run = m_new;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const bf16x8 pf = pack_bf16x8(s, h);
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) oacc[dt] = Mma<__bf16>::run(tr_frag_at<D>(vb, to, 16 * h, dt), pf, oacc[dt]);
+    for (int db = 0; db < NDB; ++db) {
+      oacc[db] *= alpha;
+      oacc[db] = mfma16(vt_frag(db), pf, oacc[db]);
     }
   };
 
-  // Tiles tile0 + wave, + 4, ..., alternately from stage 0 and stage 1.
-  // Outstanding loads, oldest first, when a tile's wait comes: its V copies
-  // (issued an iteration earlier), its K (issued during the previous tile's
-  // softmax), then the next tile's V copies (issued just before the wait),
-  // which alone may stay in flight. After the wave's last tile the next
-  // copies still go out, reading nothing and writing zeros: with the copy
-  // and the wait unconditional the compiler keeps the partial count instead
-  // of waiting for every copy before the transposed reads.
+  // Tiles tile0 + wave, + 4, ...: the K and V loads of the wave's next tile
+  // go out before this tile's V is written to LDS and its products run;
+  // the page ids come one tile earlier still.
+  bf16x8 kra[2 * NQ], krb[2 * NQ], vra[NI], vrb[NI];
   int t = w.tile0 + wave;
   TilePages next{};
   if (t < w.tile1) {
     const TilePages tp = tile_pages(t);
-    load_k(t, tp, kr);
-    issue_v(t, tp, st0, true);
+    load_k(t, tp, kra);
+    load_v(t, tp, vra);
     next = tile_pages(t + kDecWaves);
   }
-  auto step = [&](int tile, const char *cur, char *other) __attribute__((always_inline)) {
+  auto step = [&](int tile, bf16x8 (&kc)[2 * NQ], bf16x8 (&vc)[NI], bf16x8 (&kn)[2 * NQ], bf16x8 (&vn)[NI])
+                  __attribute__((always_inline)) {
     const int tn = tile + kDecWaves;
-    const TilePages pn = next;
-    issue_v(tn, pn, other, tn < w.tile1);
-    next = tile_pages(tn + kDecWaves);
-    wait_vmcnt<NI>();
-    compute(tile, cur, tn, pn);
+    if (tn < w.tile1) {
+      const TilePages pn = next;
+      load_k(tn, pn, kn);
+      load_v(tn, pn, vn);
+      next = tile_pages(tn + kDecWaves);
+    }
+    write_v(tile, vc);
+    compute(tile, kc);
   };
   for (; t < w.tile1; t += 2 * kDecWaves) {
-    step(t, st0, st1);
+    step(t, kra, vra, krb, vrb);
     if (t + kDecWaves >= w.tile1) break;
-    step(t + kDecWaves, st1, st0);
+    step(t + kDecWaves, krb, vrb, kra, vra);
   }
-  wait_vmcnt<0>();   // the closing copies land before the combine reuses the stages
 
-  // Combine the four waves' partial softmax states (each wave has waited for
-  // all of its copies). Per wave: O^T [dt][j][lane], and m and l per lane.
-  __syncthreads();
-  auto obuf = [&](int v) __attribute__((always_inline)) {
-    return reinterpret_cast<float *>(v < 2 ? vs0 : vs1) + (v & 1) * OS;
-  };
-  float *mine = obuf(wave);
+  // Combine the four waves' partial softmax states. Per wave: O^T
+  // [db][e][lane] in its V tile, m and the row sum of l per lane in ml.
+  const float l_row = l_run + __shfl_xor(l_run, 16, 64);
+  const float l_all = l_row + __shfl_xor(l_row, 32, 64);
+  __syncthreads();   // every wave is done with its V tile
+  float *const mine = reinterpret_cast<float *>(vt);
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt)
+  for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int j = 0; j < 16; ++j) mine[(dt * 16 + j) * 64 + lane] = oacc[dt][j];
+    for (int e = 0; e < 4; ++e) mine[(db * 4 + e) * 64 + lane] = oacc[db][e];
   ml[wave * 128 + lane] = m_run;
-  ml[wave * 128 + 64 + lane] = l_run + xor32(l_run);
+  ml[wave * 128 + 64 + lane] = l_all;
   __syncthreads();
-  if (wave >= DT || !row_ok) return;
-  const int dt = wave;
+  if (!row_ok) return;
   float M = -INFINITY;
 #pragma unroll
   for (int v = 0; v < kDecWaves; ++v) M = fmaxf(M, ml[v * 128 + lane]);
@@ -245,26 +257,31 @@ void decode_bf16_kernel(DecodeParams p) {
     wv[v] = (M == -INFINITY || mv == -INFINITY) ? 0.0f : fast_exp2(mv - M);
     L += wv[v] * ml[v * 128 + 64 + lane];
   }
-  f32x16 o = zero16();
-#pragma unroll
-  for (int v = 0; v < kDecWaves; ++v)
-#pragma unroll
-    for (int j = 0; j < 16; ++j) o[j] += wv[v] * obuf(v)[(dt * 16 + j) * 64 + lane];
   const int64_t R = (int64_t)(rq.q0 + my_i) * Hq + my_h;   // row of q, o and the partial planes
   const float inv = L > 0.0f ? 1.0f / L : 0.0f;
-  const float lse = L > 0.0f ? (M + log2f(L)) * kLn2 : -INFINITY;
-  if (w.split < 0) {
-    __bf16 *op = (__bf16 *)p.o + R * D + dt * 32;
+  // Wave v stores channel blocks v, v + 4, ...: lane (j, bq) channels
+  // 16 db + 4 bq .. + 3 of row j.
+  for (int db = wave; db < NDB; db += kDecWaves) {
+    f32x4 o = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj)
-      store4(op + jj * 8 + G * 4, o[jj * 4] * inv, o[jj * 4 + 1] * inv, o[jj * 4 + 2] * inv, o[jj * 4 + 3] * inv);
-    if (dt == 0 && G == 0 && p.lse != nullptr) p.lse[(int64_t)my_h * p.Tq + rq.q0 + my_i] = lse;
-  } else {
-    float *op = p.part_o + (w.split * p.plane + R) * D + dt * 32;
+    for (int v = 0; v < kDecWaves; ++v) {
+      const float *ov = reinterpret_cast<const float *>(vs + v * TB);
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj)
-      store4(op + jj * 8 + G * 4, o[jj * 4] * inv, o[jj * 4 + 1] * inv, o[jj * 4 + 2] * inv, o[jj * 4 + 3] * inv);
-    if (dt == 0 && G == 0) p.part_lse[w.split * p.plane + R] = lse;
+      for (int e = 0; e < 4; ++e) o[e] += wv[v] * ov[(db * 4 + e) * 64 + lane];
+    }
+    const int ch = 16 * db + 4 * bq;
+    if (w.split < 0)
+      store4((__bf16 *)p.o + R * D + ch, o[0] * inv, o[1] * inv, o[2] * inv, o[3] * inv);
+    else
+      store4(p.part_o + (w.split * p.plane + R) * D + ch, o[0] * inv, o[1] * inv, o[2] * inv, o[3] * inv);
+  }
+  if (wave == 0 && bq == 0) {
+    const float lse = L > 0.0f ? (M + log2f(L)) * kLn2 : -INFINITY;
+    if (w.split < 0) {
+      if (p.lse != nullptr) p.lse[(int64_t)my_h * p.Tq + rq.q0 + my_i] = lse;
+    } else {
+      p.part_lse[w.split * p.plane + R] = lse;
+    }
   }
 }
 

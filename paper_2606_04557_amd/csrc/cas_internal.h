@@ -238,10 +238,10 @@ struct AdamParams {
 
 // Paged decode: one request (its queries are tokens q0 .. q0+n-1; its keys
 // the pages page_ids[page0 ..] in order, kv_len of them) and one workgroup's
-// share: packed rows row0 .. row0+31 (row r = query r / g, head kvh*g + r % g)
+// share: packed rows row0 .. row0+15 (row r = query r / g, head kvh*g + r % g)
 // over 32-key tiles [tile0, tile1) of the request's key axis.
 constexpr int kDecTile = 32;
-constexpr int kDecRows = 32;
+constexpr int kDecRows = 16;
 struct DevDecodeReq {
   int32_t q0, n, kv_len, page0;
   int32_t nsplit;        // key-axis splits of every row block of the request
