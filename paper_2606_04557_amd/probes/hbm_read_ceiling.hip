@@ -17,6 +17,9 @@
 //   pages U S     the decode's bytes: one 256-thread workgroup per
 //                 (request, KV head, key range), S ranges per (request, KV
 //                 head), U 32-key tiles of K and V in flight per lane
+//   wave S        register loads as in `pages` U 1, but each of the four
+//                 waves on every fourth tile of its own (one 16 KiB tile of
+//                 K and V per wave and iteration)
 //   dma S         the same bytes by direct buffer->LDS copies, each of the
 //                 four waves on every fourth tile (the decode kernel's
 //                 assignment), one 16 KiB tile (K and V) in flight per wave,
@@ -110,6 +113,40 @@ __global__ __launch_bounds__(256) void pages_kernel(const uint16_t *kp, const ui
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int e = 0; e < 4; ++e) acc ^= v[u][e];
+  }
+  keep(acc, sink);
+}
+
+// Wave w of a workgroup reads tiles t0 + w, t0 + w + 4, ... of its (request,
+// KV head): per tile each lane loads 8 pieces of 16 bytes (K and V of keys
+// 4 i + lane / 16, chunk lane % 16, i = 0..3), then folds them.
+__global__ __launch_bounds__(256) void wave_kernel(const uint16_t *kp, const uint16_t *vp, const int *table,
+                                                   int splits, u32x4 *sink) {
+  const int w = blockIdx.x;
+  const int split = w % splits, pair = w / splits;
+  const int h = pair % kHkv, r = pair / kHkv;
+  const int t0 = (int)((int64_t)kTiles * split / splits), t1 = (int)((int64_t)kTiles * (split + 1) / splits);
+  const int *pt = table + r * kReqPages;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int c = lane & 15;
+  u32x4 acc = {0, 0, 0, 0};
+  for (int t = t0 + wave; t < t1; t += 4) {
+    u32x4 v[16];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int key = t * kTile + 4 * i + lane / 16;
+      if (key < kKvLen) {
+        const int page = pt[2 * t + i / 4];
+        const int64_t off = (((int64_t)page * kPage + (4 * i) % 16 + lane / 16) * kHkv + h) * kD + c * 8;
+        v[2 * i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(kp + off));
+        v[2 * i + 1] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(vp + off));
+      } else {
+        v[2 * i] = u32x4{0, 0, 0, 0};
+        v[2 * i + 1] = u32x4{0, 0, 0, 0};
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc ^= v[e];
   }
   keep(acc, sink);
 }
@@ -240,6 +277,12 @@ int main() {
     run_pages(std::integral_constant<int, 1>{}, splits);
     run_pages(std::integral_constant<int, 2>{}, splits);
     run_pages(std::integral_constant<int, 4>{}, splits);
+  }
+  for (int splits : {1, 2, 4}) {
+    const int grid = kReqs * kHkv * splits;
+    const float ms = time_ms([&] { hipLaunchKernelGGL(wave_kernel, dim3(grid), dim3(256), 0, 0, kp, vp, dt, splits,
+                                                      sink); }, 20);
+    printf("wave    grid %5d    : %.4f ms  %.0f GB/s of decode bytes\n", grid, ms, dec_bytes / ms / 1e6);
   }
   for (int splits : {1, 2, 4}) {
     const int grid = kReqs * kHkv * splits;
